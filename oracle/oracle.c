@@ -1,0 +1,400 @@
+/*
+ * CPU oracle for expand / FIFO batch / ordered gather / streaming emission.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the CPU
+ * baseline leg of the benchmark load this file's library.  It shares no code,
+ * header, table or helper with the HIP library: it is the plain definition of
+ * what the lineage-controlled dataflow computes, written slowly and obviously,
+ * single threaded, so that a reader can check it against the paper by eye.
+ *
+ * Sources (RayOrch, arXiv 2609.18703):
+ *   - Sec. 4 "Lineage State and Parent Completion", Eq. (flat-facts): every
+ *     object publishes exactly one terminal fact; an Expansion is the ordered
+ *     child set of one parent; an empty successful Expansion is terminal;
+ *     each child carries its parent's immutable zero-based ordinal.
+ *   - same section, publication rules: facts are irreversible and conflicting
+ *     publications are rejected (a second report for one child is an error).
+ *   - same section, Reduce rule: a parent Item is emitted only once its
+ *     Expansion and every member outcome are resolved; dropped members are
+ *     excluded, failed/suppressed members suppress the parent, present values
+ *     are emitted in ordinal order, zero survivors give a present empty list.
+ *   - Sec. 4 "Scheduling Ready Grains": one FIFO Ready Queue per Call holds
+ *     ready Grains in enqueue order; elastic reservation removes at most B
+ *     entries from its head and may mix parents.
+ *
+ * Readings where the paper is silent (all listed in the design notes):
+ *   state SUCCESS = Present, FAILED = Failed (and Suppressed passed up from a
+ *   lower level), SKIPPED = Dropped, PENDING = no report yet; bytes of a
+ *   non-SUCCESS report are never copied; a parent with a failed member keeps
+ *   its packed surviving bytes and is flagged FAILED; an incomplete parent is
+ *   PENDING with the bytes seen so far packed in ordinal order.
+ *
+ * Parity status: every function here is pinned by the CPU test suite (worked
+ * examples from the paper's figures, brute-force enumeration on tiny inputs,
+ * closed forms and invariants).  No function is "parity unpinned".
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+enum { OR_OK = 0, OR_EINVAL = -1, OR_ERANGE = -2, OR_EDUP = -3, OR_ECAP = -4,
+       OR_EOVERFLOW = -5, OR_ESTATE = -6 };
+enum { ST_SUCCESS = 0, ST_FAILED = 1, ST_SKIPPED = 2, ST_PENDING = 3 };
+
+/* ------------------------------------------------------------------------ */
+/* F.expand: child counts -> Expansion offsets and per-child lineage keys.   */
+/* ------------------------------------------------------------------------ */
+/* offsets[0] = 0, offsets[p+1] = offsets[p] + counts[p]: parent p's ordered
+ * child set is the canonical id range [offsets[p], offsets[p+1]).  Child
+ * number o of parent p gets the key (p, o). */
+int oracle_expand(const int32_t *counts, int64_t n_parents, int64_t *offsets,
+                  uint32_t *child_parent, uint32_t *child_ordinal, int64_t child_cap)
+{
+    if (n_parents < 0 || offsets == NULL || (n_parents > 0 && counts == NULL))
+        return OR_EINVAL;
+    offsets[0] = 0;
+    for (int64_t p = 0; p < n_parents; ++p) {
+        if (counts[p] < 0)
+            return OR_EINVAL;
+        offsets[p + 1] = offsets[p] + (int64_t)counts[p];
+    }
+    int64_t n = offsets[n_parents];
+    if (n >= ((int64_t)1 << 32))
+        return OR_EOVERFLOW;
+    if (child_parent != NULL || child_ordinal != NULL) {
+        if (n > child_cap)
+            return OR_ECAP;
+        int64_t c = 0;
+        for (int64_t p = 0; p < n_parents; ++p) {
+            for (int64_t o = 0; o < counts[p]; ++o) {
+                if (child_parent)  child_parent[c] = (uint32_t)p;
+                if (child_ordinal) child_ordinal[c] = (uint32_t)o;
+                ++c;
+            }
+        }
+    }
+    return OR_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* FIFO Ready Queue + elastic reservation of at most B entries.              */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+    uint32_t *slot;
+    int64_t head, tail;          /* pop at head, push at tail */
+} fifo_t;
+
+static void fifo_push(fifo_t *q, uint32_t v) { q->slot[q->tail++] = v; }
+static int fifo_empty(const fifo_t *q) { return q->head == q->tail; }
+static uint32_t fifo_pop(fifo_t *q) { return q->slot[q->head++]; }
+
+/* Every ready entry i with keep[i] != 0 (all entries if keep == NULL) is
+ * appended to the queue in order; then reservations repeatedly take at most
+ * B entries from the head until the queue is empty.  Batch j is written to
+ * slots [j*B, j*B + size_j) of the outputs; batch_size_out (optional) gets
+ * size_j.  The (parent, ordinal) tags of child c come from the same per-parent
+ * enumeration as oracle_expand. */
+int oracle_batch(const uint32_t *queue, const uint8_t *keep, int64_t q_len,
+                 const int64_t *offsets, int64_t n_parents, int32_t batch_size,
+                 uint32_t *out_child, uint32_t *out_parent, uint32_t *out_ordinal,
+                 int64_t out_cap, int64_t *n_out, int64_t *n_batches,
+                 int64_t *batch_size_out)
+{
+    if (q_len < 0 || n_parents < 0 || batch_size <= 0 || offsets == NULL ||
+        (q_len > 0 && queue == NULL))
+        return OR_EINVAL;
+    int64_t n = offsets[n_parents];
+    uint32_t *par = (uint32_t *)malloc(sizeof(uint32_t) * (size_t)(n > 0 ? n : 1));
+    uint32_t *ord = (uint32_t *)malloc(sizeof(uint32_t) * (size_t)(n > 0 ? n : 1));
+    fifo_t q;
+    q.slot = (uint32_t *)malloc(sizeof(uint32_t) * (size_t)(q_len > 0 ? q_len : 1));
+    q.head = q.tail = 0;
+    int rc = OR_OK;
+    if (!par || !ord || !q.slot) { rc = OR_EINVAL; goto done; }
+    for (int64_t p = 0; p < n_parents; ++p)
+        for (int64_t c = offsets[p]; c < offsets[p + 1]; ++c) {
+            par[c] = (uint32_t)p;
+            ord[c] = (uint32_t)(c - offsets[p]);
+        }
+    for (int64_t i = 0; i < q_len; ++i) {
+        if (keep != NULL && keep[i] == 0)
+            continue;
+        if ((int64_t)queue[i] >= n) { rc = OR_ERANGE; goto done; }
+        fifo_push(&q, queue[i]);
+    }
+    if (q.tail > out_cap) { rc = OR_ECAP; goto done; }
+    int64_t slot = 0, nb = 0;
+    while (!fifo_empty(&q)) {
+        /* one elastic reservation: at most B entries, parents may mix */
+        int64_t taken = 0;
+        while (taken < batch_size && !fifo_empty(&q)) {
+            uint32_t c = fifo_pop(&q);
+            if (out_child)   out_child[slot] = c;
+            if (out_parent)  out_parent[slot] = par[c];
+            if (out_ordinal) out_ordinal[slot] = ord[c];
+            ++slot;
+            ++taken;
+        }
+        if (batch_size_out) batch_size_out[nb] = taken;
+        ++nb;
+    }
+    if (n_out) *n_out = slot;
+    if (n_batches) *n_batches = nb;
+done:
+    free(par);
+    free(ord);
+    free(q.slot);
+    return rc;
+}
+
+/* ------------------------------------------------------------------------ */
+/* F.reduce: ordered gather of child reports into parent slots.              */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+    uint32_t parent, ordinal;
+    int64_t index;               /* report position: makes the sort stable */
+} key_t;
+
+static int key_cmp(const void *a, const void *b)
+{
+    const key_t *x = (const key_t *)a, *y = (const key_t *)b;
+    if (x->parent != y->parent) return x->parent < y->parent ? -1 : 1;
+    if (x->ordinal != y->ordinal) return x->ordinal < y->ordinal ? -1 : 1;
+    if (x->index != y->index) return x->index < y->index ? -1 : 1;
+    return 0;
+}
+
+/* Reports r_i = (parent, ordinal, state, bytes data[off[i], off[i+1])) in any
+ * order.  Outputs per parent p: counts of SUCCESS/FAILED/SKIPPED reports,
+ * complete = all k_p children have a terminal report, parent_state, and the
+ * slot out_data[out_off[p], out_off[p+1]) holding the SUCCESS bytes in
+ * ordinal order.  out_data may be NULL (metadata only). */
+int oracle_gather(const uint32_t *rep_parent, const uint32_t *rep_ordinal,
+                  const uint8_t *rep_state, const int64_t *rep_off,
+                  const uint8_t *data, int64_t n_reports,
+                  const int64_t *offsets, int64_t n_parents,
+                  int64_t *out_off, uint8_t *out_data, int64_t out_cap,
+                  int32_t *n_success, int32_t *n_failed, int32_t *n_skipped,
+                  uint8_t *complete, uint8_t *parent_state)
+{
+    if (n_reports < 0 || n_parents < 0 || offsets == NULL || out_off == NULL)
+        return OR_EINVAL;
+    if (n_reports > 0 && (rep_parent == NULL || rep_ordinal == NULL ||
+                          rep_state == NULL || rep_off == NULL))
+        return OR_EINVAL;
+    if (n_reports > 0 && rep_off[0] < 0)
+        return OR_EINVAL;
+    /* 1. validate every report */
+    int64_t n_valid = 0;
+    for (int64_t i = 0; i < n_reports; ++i) {
+        if (rep_off[i + 1] < rep_off[i])
+            return OR_EINVAL;
+        if (rep_state[i] > ST_PENDING)
+            return OR_ESTATE;
+        if (rep_state[i] == ST_PENDING)
+            continue;                         /* no report for this slot */
+        uint32_t p = rep_parent[i];
+        if ((int64_t)p >= n_parents)
+            return OR_ERANGE;
+        if ((int64_t)rep_ordinal[i] >= offsets[p + 1] - offsets[p])
+            return OR_ERANGE;
+        ++n_valid;
+    }
+    /* 2. stable sort of the report indices by (parent, ordinal) */
+    key_t *keys = (key_t *)malloc(sizeof(key_t) * (size_t)(n_valid > 0 ? n_valid : 1));
+    if (!keys)
+        return OR_EINVAL;
+    int64_t m = 0;
+    for (int64_t i = 0; i < n_reports; ++i) {
+        if (rep_state[i] == ST_PENDING)
+            continue;
+        keys[m].parent = rep_parent[i];
+        keys[m].ordinal = rep_ordinal[i];
+        keys[m].index = i;
+        ++m;
+    }
+    qsort(keys, (size_t)m, sizeof(key_t), key_cmp);
+    for (int64_t j = 1; j < m; ++j) {
+        if (keys[j].parent == keys[j - 1].parent && keys[j].ordinal == keys[j - 1].ordinal) {
+            free(keys);
+            return OR_EDUP;                   /* conflicting second fact */
+        }
+    }
+    /* 3. total surviving bytes, checked against the output capacity */
+    int64_t total = 0;
+    for (int64_t j = 0; j < m; ++j) {
+        int64_t i = keys[j].index;
+        if (rep_state[i] == ST_SUCCESS)
+            total += rep_off[i + 1] - rep_off[i];
+    }
+    if (out_data != NULL && total > out_cap) {
+        free(keys);
+        return OR_ECAP;
+    }
+    /* 4. per parent, ascending: counts, completion, state, ordered bytes */
+    int64_t j = 0, pos = 0;
+    for (int64_t p = 0; p < n_parents; ++p) {
+        int32_t ns = 0, nf = 0, nk = 0;
+        out_off[p] = pos;
+        while (j < m && (int64_t)keys[j].parent == p) {
+            int64_t i = keys[j].index;
+            if (rep_state[i] == ST_SUCCESS) {
+                int64_t len = rep_off[i + 1] - rep_off[i];
+                if (out_data != NULL && len > 0)
+                    memcpy(out_data + pos, data + rep_off[i], (size_t)len);
+                pos += len;
+                ++ns;
+            } else if (rep_state[i] == ST_FAILED) {
+                ++nf;
+            } else {
+                ++nk;
+            }
+            ++j;
+        }
+        int64_t k = offsets[p + 1] - offsets[p];
+        int done = ((int64_t)ns + nf + nk == k);
+        if (n_success) n_success[p] = ns;
+        if (n_failed)  n_failed[p] = nf;
+        if (n_skipped) n_skipped[p] = nk;
+        if (complete)  complete[p] = (uint8_t)done;
+        if (parent_state)
+            parent_state[p] = !done ? ST_PENDING : (nf > 0 ? ST_FAILED : ST_SUCCESS);
+    }
+    out_off[n_parents] = pos;
+    free(keys);
+    return OR_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Streaming: reports arrive in waves; complete parents are emitted in       */
+/* ascending parent order at the end of each wave, exactly once.             */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+    int64_t n_parents, n_children;
+    int64_t *offsets;            /* own copy */
+    uint8_t *seen;               /* per child: a terminal report was accepted */
+    uint8_t *state;              /* per child */
+    const uint8_t **src;         /* per child: first byte of its SUCCESS record */
+    int64_t *len;                /* per child: SUCCESS record length, else 0 */
+    int32_t *cnt[3];             /* per parent: SUCCESS / FAILED / SKIPPED */
+    uint8_t *emitted;            /* per parent */
+} oracle_stream;
+
+void oracle_stream_destroy(oracle_stream *s)
+{
+    if (!s) return;
+    free(s->offsets); free(s->seen); free(s->state); free((void *)s->src); free(s->len);
+    for (int t = 0; t < 3; ++t) free(s->cnt[t]);
+    free(s->emitted);
+    free(s);
+}
+
+oracle_stream *oracle_stream_create(const int64_t *offsets, int64_t n_parents)
+{
+    if (n_parents < 0 || offsets == NULL)
+        return NULL;
+    oracle_stream *s = (oracle_stream *)calloc(1, sizeof(oracle_stream));
+    if (!s) return NULL;
+    int64_t n = offsets[n_parents];
+    size_t np = (size_t)(n_parents + 1), nc = (size_t)(n > 0 ? n : 1);
+    s->n_parents = n_parents;
+    s->n_children = n;
+    s->offsets = (int64_t *)malloc(sizeof(int64_t) * np);
+    s->seen = (uint8_t *)calloc(nc, 1);
+    s->state = (uint8_t *)calloc(nc, 1);
+    s->src = (const uint8_t **)calloc(nc, sizeof(uint8_t *));
+    s->len = (int64_t *)calloc(nc, sizeof(int64_t));
+    for (int t = 0; t < 3; ++t) s->cnt[t] = (int32_t *)calloc(np, sizeof(int32_t));
+    s->emitted = (uint8_t *)calloc(np, 1);
+    if (!s->offsets || !s->seen || !s->state || !s->src || !s->len ||
+        !s->cnt[0] || !s->cnt[1] || !s->cnt[2] || !s->emitted) {
+        oracle_stream_destroy(s);
+        return NULL;
+    }
+    memcpy(s->offsets, offsets, sizeof(int64_t) * np);
+    return s;
+}
+
+/* Record one wave of reports.  A child reported in an earlier wave, or twice
+ * in this one, is a conflicting publication.  The bytes stay in the caller's
+ * buffer until the parent is emitted. */
+int oracle_stream_report(oracle_stream *s, const uint32_t *rep_parent,
+                         const uint32_t *rep_ordinal, const uint8_t *rep_state,
+                         const int64_t *rep_off, const uint8_t *data, int64_t n_reports)
+{
+    if (!s || n_reports < 0)
+        return OR_EINVAL;
+    if (n_reports > 0 && (!rep_parent || !rep_ordinal || !rep_state || !rep_off))
+        return OR_EINVAL;
+    if (n_reports > 0 && rep_off[0] < 0)
+        return OR_EINVAL;
+    for (int64_t i = 0; i < n_reports; ++i) {      /* validate first */
+        if (rep_off[i + 1] < rep_off[i]) return OR_EINVAL;
+        if (rep_state[i] > ST_PENDING) return OR_ESTATE;
+        if (rep_state[i] == ST_PENDING) continue;
+        uint32_t p = rep_parent[i];
+        if ((int64_t)p >= s->n_parents) return OR_ERANGE;
+        if ((int64_t)rep_ordinal[i] >= s->offsets[p + 1] - s->offsets[p]) return OR_ERANGE;
+    }
+    for (int64_t i = 0; i < n_reports; ++i) {
+        if (rep_state[i] == ST_PENDING) continue;
+        uint32_t p = rep_parent[i];
+        int64_t c = s->offsets[p] + rep_ordinal[i];
+        if (s->seen[c])
+            return OR_EDUP;
+        s->seen[c] = 1;
+        s->state[c] = rep_state[i];
+        s->src[c] = data + rep_off[i];
+        s->len[c] = rep_state[i] == ST_SUCCESS ? rep_off[i + 1] - rep_off[i] : 0;
+        s->cnt[rep_state[i]][p] += 1;
+    }
+    return OR_OK;
+}
+
+/* Emit every parent that is complete now and was not emitted before, in
+ * ascending parent order: its id, its slot offset inside emit_data, its
+ * counts, its derived state and its SUCCESS bytes in ordinal order. */
+int oracle_stream_emit(oracle_stream *s, uint32_t *emit_parent, int64_t *emit_off,
+                       uint8_t *emit_data, int64_t cap_parents, int64_t cap_bytes,
+                       int32_t *n_success, int32_t *n_failed, int32_t *n_skipped,
+                       uint8_t *parent_state, int64_t *n_emitted, int64_t *n_bytes)
+{
+    if (!s || !emit_off)
+        return OR_EINVAL;
+    int64_t e = 0, pos = 0;
+    /* first pass: sizes, checked against the capacities */
+    for (int64_t p = 0; p < s->n_parents; ++p) {
+        int64_t k = s->offsets[p + 1] - s->offsets[p];
+        if (s->emitted[p] || (int64_t)s->cnt[0][p] + s->cnt[1][p] + s->cnt[2][p] != k)
+            continue;
+        ++e;
+        for (int64_t c = s->offsets[p]; c < s->offsets[p + 1]; ++c)
+            pos += s->len[c];
+    }
+    if (e > cap_parents || (emit_data != NULL && pos > cap_bytes))
+        return OR_ECAP;
+    e = 0;
+    pos = 0;
+    for (int64_t p = 0; p < s->n_parents; ++p) {
+        int64_t k = s->offsets[p + 1] - s->offsets[p];
+        if (s->emitted[p] || (int64_t)s->cnt[0][p] + s->cnt[1][p] + s->cnt[2][p] != k)
+            continue;
+        if (emit_parent) emit_parent[e] = (uint32_t)p;
+        emit_off[e] = pos;
+        for (int64_t c = s->offsets[p]; c < s->offsets[p + 1]; ++c) {
+            if (emit_data != NULL && s->len[c] > 0)
+                memcpy(emit_data + pos, s->src[c], (size_t)s->len[c]);
+            pos += s->len[c];
+        }
+        if (n_success) n_success[e] = s->cnt[0][p];
+        if (n_failed)  n_failed[e] = s->cnt[1][p];
+        if (n_skipped) n_skipped[e] = s->cnt[2][p];
+        if (parent_state) parent_state[e] = s->cnt[1][p] > 0 ? ST_FAILED : ST_SUCCESS;
+        s->emitted[p] = 1;
+        ++e;
+    }
+    emit_off[e] = pos;
+    if (n_emitted) *n_emitted = e;
+    if (n_bytes) *n_bytes = pos;
+    return OR_OK;
+}

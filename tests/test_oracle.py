@@ -1,0 +1,442 @@
+"""Pins for the CPU oracle (no GPU): worked examples from the paper's figures,
+brute-force enumeration on tiny inputs, closed forms and invariants."""
+import itertools
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle as O
+from oracle import brute
+import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _key_ids(fx):
+    names = fx["parents"]
+    counts = fx["counts"]
+    offs = np.concatenate([[0], np.cumsum(counts)])
+    return lambda k: int(offs[names.index(k[0])] + k[1]), offs
+
+
+# ---------------------------------------------------------------- worked examples
+def test_teaser_fifo_batches_and_completion():
+    fx = json.load(open(os.path.join(GOLDEN, "teaser_fifo.json")))
+    cid, _ = _key_ids(fx)
+    offsets = O.expand(fx["counts"], tags=False)
+    queue = np.array([cid(k) for k in fx["queue"]], np.uint32)
+    child, parent, ordinal, sizes = O.batch(queue, None, offsets, fx["reserve"])
+    assert list(sizes) == [len(b) for b in fx["batches"]]
+    flat = [tuple(k) for b in fx["batches"] for k in b]
+    got = [(fx["parents"][p], o) for p, o in zip(parent, ordinal)]
+    assert got == flat
+    # the eight batched children turn terminal (SUCCESS, one byte each)
+    n = len(child)
+    g = O.gather(parent, ordinal, np.zeros(n, np.uint8), np.arange(n + 1), np.arange(n, dtype=np.uint8),
+                 offsets)
+    for i, name in enumerate(fx["parents"]):
+        done, total = fx["terminal_over_total"][name]
+        assert g["n_success"][i] + g["n_failed"][i] + g["n_skipped"][i] == done
+        assert offsets[i + 1] - offsets[i] == total
+        assert bool(g["complete"][i]) == fx["proceeds"][name]
+        assert g["parent_state"][i] == (O.SUCCESS if fx["proceeds"][name] else O.PENDING)
+
+
+def test_failure_figure_reservation():
+    fx = json.load(open(os.path.join(GOLDEN, "failure_fifo.json")))
+    cid, _ = _key_ids(fx)
+    offsets = O.expand(fx["counts"], tags=False)
+    queue = np.array([cid(k) for k in fx["queue"]], np.uint32)
+    child, parent, ordinal, sizes = O.batch(queue, None, offsets, fx["reserve"])
+    first = [(fx["parents"][p], o) for p, o in zip(parent[:sizes[0]], ordinal[:sizes[0]])]
+    rest = [(fx["parents"][p], o) for p, o in zip(parent[sizes[0]:], ordinal[sizes[0]:])]
+    assert first == [tuple(k) for k in fx["first_batch"]]
+    assert rest == [tuple(k) for k in fx["left_in_queue"]]
+
+
+# ---------------------------------------------------------------- expand
+def test_expand_exhaustive_vs_brute():
+    for P in range(0, 4):
+        for counts in itertools.product(range(4), repeat=P):
+            offs, par, ordi = O.expand(np.array(counts, np.int32))
+            bo, bp, bord = brute.expand(counts)
+            assert list(offs) == bo
+            assert list(par) == bp and list(ordi) == bord
+
+
+def test_expand_invariants_config2_small():
+    c = W.config2(n_parents=3000)
+    offs, par, ordi = O.expand(c.counts)
+    assert offs[0] == 0 and offs[-1] == c.counts.astype(np.int64).sum()
+    assert np.all(np.diff(par.astype(np.int64)) >= 0)               # parents nondecreasing
+    # ordinals run 0..k-1 for every parent, each child exactly once
+    for p in np.random.default_rng(0).choice(len(c.counts), 200, replace=False):
+        seg = ordi[offs[p]:offs[p + 1]]
+        assert np.array_equal(seg, np.arange(c.counts[p]))
+        assert np.all(par[offs[p]:offs[p + 1]] == p)
+    keys = par.astype(np.int64) * (1 << 32) + ordi
+    assert len(np.unique(keys)) == len(keys)
+
+
+def test_expand_errors(olib):
+    with pytest.raises(O.OracleError) as e:
+        O.expand(np.array([1, -1, 2], np.int32))
+    assert e.value.code == O.EINVAL
+    big = np.full(3, 2 ** 31 - 1, np.int32)
+    with pytest.raises(O.OracleError) as e:
+        O.expand(big, tags=False)
+    assert e.value.code == O.EOVERFLOW
+
+
+def test_expand_empty():
+    offs, par, ordi = O.expand(np.zeros(0, np.int32))
+    assert list(offs) == [0] and len(par) == 0
+    offs, par, ordi = O.expand(np.zeros(5, np.int32))
+    assert list(offs) == [0] * 6 and len(par) == 0
+
+
+# ---------------------------------------------------------------- batch
+def test_batch_exhaustive_vs_brute():
+    for counts in [(2, 1), (0, 3, 1), (1, 0, 0, 2), (4,)]:
+        n = sum(counts)
+        offsets = O.expand(np.array(counts, np.int32), tags=False)
+        keys = brute.children(counts)
+        for perm in itertools.permutations(range(n)):
+            for mask in itertools.product((0, 1), repeat=n):
+                for B in range(1, n + 2):
+                    q = np.array(perm, np.uint32)
+                    keep = np.array(mask, np.uint8)
+                    child, parent, ordinal, sizes = O.batch(q, keep, offsets, B)
+                    bb, _ = brute.batch(list(perm), list(mask), counts, B)
+                    assert list(sizes) == [len(b) for b in bb]
+                    flat = [c for b in bb for c in b]
+                    assert list(child) == flat
+                    assert [(int(p), int(o)) for p, o in zip(parent, ordinal)] == [keys[c] for c in flat]
+
+
+def test_batch_fifo_order_and_chunking():
+    c = W.config2(n_parents=2000)
+    offs = O.expand(c.counts, tags=False)
+    child, parent, ordinal, sizes = O.batch(c.queue, c.keep, offs, c.batch_size)
+    kept = np.nonzero(c.keep)[0]
+    # FIFO: kept entries appear once each, in queue order
+    assert np.array_equal(child, c.queue[kept])
+    m = len(kept)
+    B = c.batch_size
+    assert len(sizes) == -(-m // B)
+    assert np.all(sizes[:-1] == B) and 1 <= sizes[-1] <= B
+    assert np.all(offs[parent] + ordinal == child)
+
+
+def test_batch_errors():
+    offs = O.expand(np.array([2, 1], np.int32), tags=False)
+    with pytest.raises(O.OracleError) as e:
+        O.batch(np.array([0, 3], np.uint32), None, offs, 2)
+    assert e.value.code == O.ERANGE
+    # an out-of-range id that is not kept is never looked at
+    child, *_ = O.batch(np.array([0, 3], np.uint32), np.array([1, 0], np.uint8), offs, 2)
+    assert list(child) == [0]
+    child, parent, ordinal, sizes = O.batch(np.zeros(0, np.uint32), None, offs, 4)
+    assert len(child) == 0 and len(sizes) == 0
+
+
+# ---------------------------------------------------------------- gather
+def _random_reports(rng, counts, p_report=1.0, states=(0, 1, 2), max_len=5):
+    reports = []
+    for p, k in enumerate(counts):
+        for o in range(k):
+            if rng.random() >= p_report:
+                continue
+            s = int(rng.choice(states))
+            ln = int(rng.integers(0, max_len + 1))
+            reports.append([p, o, s, bytes(rng.integers(0, 256, ln, dtype=np.uint8))])
+    order = rng.permutation(len(reports))
+    return [reports[i] for i in order]
+
+
+def _run_gather(reports, counts):
+    offsets = O.expand(np.array(counts, np.int32), tags=False)
+    n = len(reports)
+    par = np.array([r[0] for r in reports], np.uint32)
+    ordi = np.array([r[1] for r in reports], np.uint32)
+    st = np.array([r[2] for r in reports], np.uint8)
+    lens = np.array([len(r[3]) for r in reports], np.int64)
+    off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    data = np.frombuffer(b"".join(r[3] for r in reports) or b"\0", np.uint8)
+    return O.gather(par, ordi, st, off, data, offsets)
+
+
+def _compare_brute(g, b):
+    for p, (ns, nf, nk, done, state, slot) in enumerate(b):
+        assert g["n_success"][p] == ns and g["n_failed"][p] == nf and g["n_skipped"][p] == nk
+        assert g["complete"][p] == done and g["parent_state"][p] == state
+        got = bytes(g["out_data"][g["out_off"][p]:g["out_off"][p + 1]])
+        assert got == slot
+
+
+def test_gather_vs_brute_exhaustive_states():
+    rng = np.random.default_rng(7)
+    for counts in [(1, 2), (0, 3), (2, 0, 2), (3,)]:
+        n = sum(counts)
+        for states in itertools.product((0, 1, 2, 3), repeat=n):
+            reports = []
+            i = 0
+            for p, k in enumerate(counts):
+                for o in range(k):
+                    reports.append([p, o, states[i], bytes([p * 16 + o] * (o + 1))])
+                    i += 1
+            order = rng.permutation(n)
+            reports = [reports[j] for j in order]
+            _compare_brute(_run_gather(reports, counts), brute.gather(reports, counts))
+
+
+def test_gather_vs_brute_random():
+    rng = np.random.default_rng(11)
+    for trial in range(300):
+        P = int(rng.integers(0, 7))
+        counts = [int(x) for x in rng.integers(0, 5, P)]
+        reports = _random_reports(rng, counts, p_report=float(rng.choice([1.0, 0.7])),
+                                  states=(0, 0, 1, 2, 3))
+        _compare_brute(_run_gather(reports, counts), brute.gather(reports, counts))
+
+
+def test_gather_round_trip_and_content():
+    """gather(batch(expand(x))) puts every record of parent p back in ordinal
+    order; each record's bytes are the splitmix64 stream of its own key."""
+    c = W.config1()
+    offs, cpar, cord = O.expand(c.counts)
+    child, parent, ordinal, _ = O.batch(c.queue, c.keep, offs, c.batch_size)
+    r = c.reports
+    m = len(child)
+    data = r.data()
+    g = O.gather(parent, ordinal, r.state[:m], r.off[:m + 1], data, offs)
+    # reference slot of each parent from the content definition
+    for p in range(c.n_parents):
+        ords = np.arange(c.counts[p])
+        ok = c.states[offs[p]:offs[p + 1]] == W.SUCCESS
+        seeds = W.content_seed(np.full(ok.sum(), p), ords[ok])
+        want = W.record_bytes(seeds, c.lengths[offs[p]:offs[p + 1]][ok])
+        got = g["out_data"][g["out_off"][p]:g["out_off"][p + 1]]
+        assert np.array_equal(got, want)
+        assert g["n_success"][p] == ok.sum() and g["n_failed"][p] == (~ok).sum()
+        assert g["complete"][p] == 1
+        assert g["parent_state"][p] == (O.FAILED if (~ok).any() else O.SUCCESS)
+
+
+def _full_reports(c, B=None, perm=None):
+    """oracle batch tags for the dispatched + sealed children of a workload."""
+    offs = O.expand(c.counts, tags=False)
+    B = B or c.batch_size
+    ch1, p1, o1, _ = O.batch(c.queue, c.keep, offs, B)
+    ch2, p2, o2, _ = O.batch(c.queue, c.sealed, offs, B)
+    par = np.concatenate([p1, p2])
+    ordi = np.concatenate([o1, o2])
+    return offs, par, ordi
+
+
+def test_gather_schedule_invariance():
+    """Eq. (schedule-invariance): report order and batch size do not change
+    the gathered items."""
+    c = W.config2(n_parents=1500)
+    r = c.reports
+    data = r.data()
+    offs, par, ordi = _full_reports(c)
+    g0 = O.gather(par, ordi, r.state, r.off, data, offs)
+    offs, par_b, ordi_b = _full_reports(c, B=7)
+    assert np.array_equal(par_b, par) and np.array_equal(ordi_b, ordi)   # B never reorders
+    rng = np.random.default_rng(3)
+    perm = rng.permutation(len(par))
+    # permute the reports (their bytes move with them)
+    lens = np.diff(r.off)[perm]
+    off2 = np.concatenate([[0], np.cumsum(lens)])
+    data2 = np.concatenate([data[r.off[i]:r.off[i + 1]] for i in perm])
+    g1 = O.gather(par[perm], ordi[perm], r.state[perm], off2, data2, offs)
+    for k in g0:
+        assert np.array_equal(g0[k], g1[k]), k
+
+
+def test_gather_complete_iff_all_terminal():
+    c = W.config2(n_parents=800)
+    r = c.reports
+    data = r.data()
+    offs, par, ordi = _full_reports(c)
+    rng = np.random.default_rng(5)
+    st = r.state.copy()
+    drop = rng.random(len(st)) < 0.01
+    st[drop] = W.PENDING
+    g = O.gather(par, ordi, st, r.off, data, offs)
+    missing = np.zeros(c.n_parents, np.int64)
+    np.add.at(missing, par[drop], 1)
+    assert np.array_equal(g["complete"] == 1, missing == 0)
+    assert np.all(g["parent_state"][missing > 0] == O.PENDING)
+    # an incomplete parent still packs the SUCCESS bytes it has, in ordinal order
+    p = int(np.nonzero(missing)[0][0])
+    sel = np.nonzero((par == p) & (st == W.SUCCESS))[0]
+    sel = sel[np.argsort(ordi[sel])]
+    want = np.concatenate([data[r.off[i]:r.off[i + 1]] for i in sel]) if len(sel) else np.zeros(0, np.uint8)
+    assert np.array_equal(g["out_data"][g["out_off"][p]:g["out_off"][p + 1]], want)
+
+
+def test_gather_empty_expansion_and_all_skipped():
+    counts = [0, 2, 0, 3, 0]
+    reports = [[1, 0, W.SKIPPED, b"xx"], [1, 1, W.SKIPPED, b""], [3, 2, W.SUCCESS, b"abc"],
+               [3, 0, W.FAILED, b"zz"], [3, 1, W.SUCCESS, b"d"]]
+    g = _run_gather(reports, counts)
+    assert list(g["complete"]) == [1, 1, 1, 1, 1]
+    assert list(g["parent_state"]) == [O.SUCCESS, O.SUCCESS, O.SUCCESS, O.FAILED, O.SUCCESS]
+    assert list(g["out_off"]) == [0, 0, 0, 0, 4, 4]
+    assert bytes(g["out_data"]) == b"dabc"        # failed bytes never copied; ordinal order
+
+
+def test_gather_errors():
+    counts = [2, 1]
+    with pytest.raises(O.OracleError) as e:
+        _run_gather([[0, 0, 0, b"a"], [0, 0, 1, b""]], counts)
+    assert e.value.code == O.EDUP
+    with pytest.raises(O.OracleError) as e:
+        _run_gather([[2, 0, 0, b"a"]], counts)
+    assert e.value.code == O.ERANGE
+    with pytest.raises(O.OracleError) as e:
+        _run_gather([[1, 1, 0, b"a"]], counts)
+    assert e.value.code == O.ERANGE
+    with pytest.raises(O.OracleError) as e:
+        _run_gather([[0, 0, 4, b"a"]], counts)
+    assert e.value.code == O.ESTATE
+    # a PENDING slot is no report: duplicates of it are not conflicts
+    g = _run_gather([[0, 0, 3, b""], [0, 0, 3, b""], [0, 0, 0, b"q"]], counts)
+    assert g["n_success"][0] == 1
+    offsets = O.expand(np.array(counts, np.int32), tags=False)
+    with pytest.raises(O.OracleError) as e:           # decreasing offsets
+        O.gather(np.array([0, 0], np.uint32), np.array([0, 1], np.uint32), np.zeros(2, np.uint8),
+                 np.array([0, 3, 2]), np.zeros(3, np.uint8), offsets)
+    assert e.value.code == O.EINVAL
+
+
+# ---------------------------------------------------------------- nested
+def test_nested_closed_form_documents():
+    """All leaves succeed and the mid level is canonical: each document's
+    slot is the concatenation, over (page ordinal, region ordinal) in
+    lexicographic order, of the region records."""
+    n = W.config3(n_docs=150)
+    r = n.reports
+    data = r.data()
+    res = O.nested(n.counts1, n.queue1, None, n.batch1, n.counts2, n.queue2, None, n.batch2,
+                   r.state, r.off, data)
+    low, up = res["low"], res["up"]
+    off1, off2 = res["offsets1"], res["offsets2"]
+    assert np.array_equal(up["out_data"], low["out_data"])
+    assert np.array_equal(up["out_off"], low["out_off"][off1])
+    assert np.all(up["complete"] == 1) and np.all(up["parent_state"] == O.SUCCESS)
+    # spot-check a document directly from the content definition
+    for d in (0, len(n.counts1) // 2, len(n.counts1) - 1):
+        parts = []
+        for g in range(off1[d], off1[d + 1]):
+            seeds = W.content_seed(np.full(n.counts2[g], g), np.arange(n.counts2[g]))
+            parts.append(W.record_bytes(seeds, n.lengths[off2[g]:off2[g + 1]]))
+        want = np.concatenate(parts)
+        assert np.array_equal(up["out_data"][up["out_off"][d]:up["out_off"][d + 1]], want)
+
+
+def test_nested_failed_frames_drop_clips():
+    """A clip with a failed frame is FAILED; its bytes stay in the clip slot
+    but never reach the video slot, which is then FAILED too."""
+    n = W.config4(n_videos=40)
+    r = n.reports
+    data = r.data()
+    res = O.nested(n.counts1, n.queue1, None, n.batch1, n.counts2, n.queue2, None, n.batch2,
+                   r.state, r.off, data)
+    low, up = res["low"], res["up"]
+    off1 = res["offsets1"]
+    assert np.all(low["complete"] == 1)
+    for v in range(len(n.counts1)):
+        clips = np.arange(off1[v], off1[v + 1])
+        ok = clips[low["parent_state"][clips] == O.SUCCESS]
+        want = np.concatenate([low["out_data"][low["out_off"][g]:low["out_off"][g + 1]] for g in ok]) \
+            if len(ok) else np.zeros(0, np.uint8)
+        assert np.array_equal(up["out_data"][up["out_off"][v]:up["out_off"][v + 1]], want)
+        assert up["parent_state"][v] == (O.FAILED if len(ok) < len(clips) else O.SUCCESS)
+        assert up["n_failed"][v] == len(clips) - len(ok)
+
+
+# ---------------------------------------------------------------- streaming
+def _stream_run(s, with_brute=False):
+    offs = O.expand(s.counts, tags=False)
+    st = O.Stream(offs)
+    arena = np.concatenate([r.data() for r in s.wave_reports])
+    emitted = []
+    for w, (q, r) in enumerate(zip(s.waves, s.wave_reports)):
+        ch, par, ordi, _ = O.batch(q, None, offs, s.batch_size)
+        st.report(par, ordi, r.state, r.off, arena)
+        emitted.append(st.emit())
+    st.close()
+    return offs, arena, emitted
+
+
+def test_stream_emits_each_parent_once_at_its_last_wave():
+    s = W.config5(n_parents=3000, n_children=40000, n_waves=6)
+    offs, arena, emitted = _stream_run(s)
+    wave_of = np.empty(s.n_children, np.int64)
+    for w, q in enumerate(s.waves):
+        wave_of[q] = w
+    last = np.zeros(s.n_parents, np.int64)
+    par_of_child = np.repeat(np.arange(s.n_parents), s.counts)
+    np.maximum.at(last, par_of_child, wave_of)
+    seen = np.zeros(s.n_parents, np.int64)
+    for w, e in enumerate(emitted):
+        assert np.all(np.diff(e["parent"].astype(np.int64)) > 0)      # ascending
+        assert np.all(last[e["parent"]] == w)
+        seen[e["parent"]] += 1
+    assert np.all(seen == 1)
+    # union over waves equals the one-shot gather of all reports
+    allpar, allord, allst, alloff = [], [], [], []
+    for q, r in zip(s.waves, s.wave_reports):
+        _, p, o, _ = O.batch(q, None, offs, s.batch_size)
+        allpar.append(p); allord.append(o); allst.append(r.state); alloff.append(r.off[:-1])
+    alloff.append(s.wave_reports[-1].off[-1:])
+    g = O.gather(np.concatenate(allpar), np.concatenate(allord), np.concatenate(allst),
+                 np.concatenate(alloff), arena, offs)
+    for e in emitted:
+        for j, p in enumerate(e["parent"]):
+            got = e["data"][e["off"][j]:e["off"][j + 1]]
+            assert np.array_equal(got, g["out_data"][g["out_off"][p]:g["out_off"][p + 1]])
+            assert e["n_success"][j] == g["n_success"][p]
+
+
+def test_stream_vs_brute_small():
+    rng = np.random.default_rng(2)
+    for trial in range(60):
+        P = int(rng.integers(1, 6))
+        counts = [int(x) for x in rng.integers(0, 4, P)]
+        reps = _random_reports(rng, counts, states=(0, 1, 2))
+        cuts = sorted(rng.integers(0, len(reps) + 1, 2))
+        waves = [reps[:cuts[0]], reps[cuts[0]:cuts[1]], reps[cuts[1]:]]
+        want = brute.stream(waves, counts)
+        offs = O.expand(np.array(counts, np.int32), tags=False)
+        st = O.Stream(offs)
+        for w, wave in enumerate(waves):
+            lens = [len(x[3]) for x in wave]
+            off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+            data = np.frombuffer(b"".join(x[3] for x in wave) or b"\0", np.uint8).copy()
+            st.report(np.array([x[0] for x in wave], np.uint32), np.array([x[1] for x in wave], np.uint32),
+                      np.array([x[2] for x in wave], np.uint8), off, data)
+            e = st.emit()
+            got = [(int(p), int(e["n_success"][j]), int(e["n_failed"][j]), int(e["n_skipped"][j]),
+                    int(e["parent_state"][j]), bytes(e["data"][e["off"][j]:e["off"][j + 1]]))
+                   for j, p in enumerate(e["parent"])]
+            assert got == want[w]
+        st.close()
+
+
+def test_stream_duplicate_across_waves():
+    offs = O.expand(np.array([2, 1], np.int32), tags=False)
+    st = O.Stream(offs)
+    one = np.array([0, 1], np.int64)
+    st.report(np.array([0], np.uint32), np.array([1], np.uint32), np.zeros(1, np.uint8), one,
+              np.zeros(1, np.uint8))
+    with pytest.raises(O.OracleError) as e:
+        st.report(np.array([0], np.uint32), np.array([1], np.uint32), np.zeros(1, np.uint8), one,
+                  np.zeros(1, np.uint8))
+    assert e.value.code == O.EDUP
+    st.close()

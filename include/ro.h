@@ -1,0 +1,183 @@
+/*
+ * ro.h -- C ABI of the lineage-controlled expand / batch / gather core for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The operations follow RayOrch (arXiv 2609.18703):
+ *   - ro_expand  : F.expand (Table "primitives"; Sec. 4 "Lineage State and
+ *                  Parent Completion"): one Expansion per parent, an ordered
+ *                  child set whose members carry (parent, immutable ordinal).
+ *   - ro_batch   : per-Call FIFO Ready Queue with elastic reservation
+ *                  (Sec. 4 "Scheduling Ready Grains"): at most B entries
+ *                  leave the head of the queue per reservation, parents may mix.
+ *   - ro_gather  : F.reduce and the Reduce rule (Sec. 4): a parent resolves
+ *                  once every member is terminal; dropped members are
+ *                  excluded, failed members suppress the parent, present
+ *                  values are concatenated in ordinal order, zero survivors
+ *                  give an empty list.  Conflicting second reports are
+ *                  rejected (publication rules, same section).
+ *   - ro_stream_*: the same gather fed wave by wave; a parent is emitted as
+ *                  soon as all of its children are terminal (Sec. 1 and 4:
+ *                  completed parents proceed while others still produce),
+ *                  in ascending parent order, exactly once.
+ *
+ * Conventions shared by every entry point:
+ *   * Memory.  Every array argument is DEVICE memory owned by the caller
+ *     (e.g. a torch tensor's data pointer).  The library keeps no caller
+ *     pointer past the call, except a stream's offsets and the report bytes of
+ *     parents not yet emitted (see ro_stream_report).
+ *   * Ordering.  Every call enqueues its kernels on the context's HIP stream
+ *     and returns at once.  Nothing synchronises except ro_ctx_status,
+ *     ro_ctx_reserve (which may allocate) and ro_stream_create/destroy.
+ *   * Errors.  Errors found on the host (NULL where an array is required, a
+ *     negative size, batch_size <= 0, a failing HIP call) are returned
+ *     immediately and nothing is enqueued.  Errors that depend on device data
+ *     are written to the context's error word, first error wins, and are
+ *     returned (and cleared) by ro_ctx_status.  After any error the outputs of
+ *     that call are unspecified; a gather or stream emission that follows a
+ *     recorded error copies no bytes until the error is cleared.
+ *   * Sizes.  Child ids are uint32, so an expansion may hold at most
+ *     2^32 - 1 children (RO_EOVERFLOW otherwise).  Byte offsets are int64.
+ *   * Terminal states are uint8: RO_SUCCESS (Present), RO_FAILED (Failed, or
+ *     Suppressed handed up from a lower level), RO_SKIPPED (Dropped) and
+ *     RO_PENDING (no report yet).
+ *
+ * A context is bound to one stream and is not thread safe.
+ */
+#ifndef RO_H
+#define RO_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    RO_OK = 0,
+    RO_EINVAL = -1,     /* bad argument, negative count, decreasing byte offsets      */
+    RO_ERANGE = -2,     /* parent >= P, ordinal >= k_p, or queued child id >= N        */
+    RO_EDUP = -3,       /* a child reported twice (within a call or across waves)      */
+    RO_ECAP = -4,       /* an output or the reserved workspace is too small            */
+    RO_EOVERFLOW = -5,  /* N >= 2^32 children, or byte totals beyond 2^45              */
+    RO_ESTATE = -6,     /* a state byte > RO_PENDING                                   */
+    RO_EHIP = -7        /* a HIP runtime call failed                                   */
+};
+
+enum { RO_SUCCESS = 0, RO_FAILED = 1, RO_SKIPPED = 2, RO_PENDING = 3 };
+
+typedef struct ro_ctx ro_ctx;
+
+/* Create a context on the current HIP device, bound to `hip_stream`
+ * (a hipStream_t; NULL means the null stream).  Returns RO_OK or RO_EHIP. */
+int ro_ctx_create(ro_ctx **out, void *hip_stream);
+
+/* Re-bind the context to another stream of the same device. */
+int ro_ctx_set_stream(ro_ctx *ctx, void *hip_stream);
+
+/* Pre-size the device workspace for expansions of up to `max_children`
+ * children and `max_parents` parents, and queues of up to `max_queue`
+ * entries, so that later calls never allocate.  Calls whose host-known sizes
+ * (parents, queue length, report count) exceed the reservation grow it
+ * (hipMalloc, which synchronises).  An expansion whose child count, known
+ * only on the device, exceeds the reservation fails with RO_ECAP. */
+int ro_ctx_reserve(ro_ctx *ctx, int64_t max_children, int64_t max_parents, int64_t max_queue);
+
+/* Wait for the context's stream, then return and clear the first error the
+ * device recorded (RO_OK if none). */
+int ro_ctx_status(ro_ctx *ctx);
+
+/* Free the context's workspace.  Waits for its stream first. */
+int ro_ctx_destroy(ro_ctx *ctx);
+
+/* F.expand.  counts[P] (int32, >= 0) -> offsets[P+1] (int64 exclusive scan,
+ * offsets[P] = N): parent p's ordered children are the canonical ids
+ * [offsets[p], offsets[p+1]).  If child_parent / child_ordinal are not NULL,
+ * child c also gets its key (p, c - offsets[p]); both need room for N
+ * entries, N <= child_cap (RO_ECAP otherwise).  A negative count is
+ * RO_EINVAL; N >= 2^32 is RO_EOVERFLOW. */
+int ro_expand(ro_ctx *ctx, const int32_t *counts, int64_t n_parents, int64_t *offsets,
+              uint32_t *child_parent, uint32_t *child_ordinal, int64_t child_cap);
+
+/* FIFO Ready Queue + elastic reservation.  queue[q_len] holds canonical
+ * child ids in enqueue order; entry i is ready iff keep == NULL or
+ * keep[i] != 0.  Ready entries are compacted in queue order into slots
+ * [0, M); reservation j is slots [j*B, min((j+1)*B, M)).  Each slot gets the
+ * child id (out_child), its parent (out_parent) and its ordinal
+ * (out_ordinal); any of the three may be NULL.  M must be <= out_cap
+ * (RO_ECAP).  A ready id >= N (N = offsets[n_parents]) is RO_ERANGE.  M and
+ * ceil(M/B) are written to the device scalars *n_out_dev and *n_batches_dev
+ * (either may be NULL). */
+int ro_batch(ro_ctx *ctx, const uint32_t *queue, const uint8_t *keep, int64_t q_len,
+             const int64_t *offsets, int64_t n_parents, int32_t batch_size,
+             uint32_t *out_child, uint32_t *out_parent, uint32_t *out_ordinal, int64_t out_cap,
+             int64_t *n_out_dev, int64_t *n_batches_dev);
+
+/* One terminal report per child, in any order.  Report i is the child
+ * (parent[i], ordinal[i]) with state[i]; its value is the byte range
+ * data[off[i], off[i+1]) (Arrow-style offsets, off nondecreasing, off[0]
+ * >= 0, RO_EINVAL otherwise).  Only RO_SUCCESS bytes are ever read.  A
+ * report with state RO_PENDING is ignored. */
+typedef struct ro_reports {
+    const uint32_t *parent;
+    const uint32_t *ordinal;
+    const uint8_t *state;
+    const int64_t *off;       /* [n + 1] */
+    const uint8_t *data;
+    int64_t n;
+} ro_reports;
+
+/* Per-parent outputs of a gather ([P] arrays unless noted). */
+typedef struct ro_gather_out {
+    int64_t *out_off;         /* [P + 1] slot p = out_data[out_off[p], out_off[p+1])   */
+    uint8_t *out_data;        /* the packed slots; needs out_off[P] <= out_cap bytes    */
+    int64_t out_cap;
+    int32_t *n_success;       /* reports per state (may be NULL)                         */
+    int32_t *n_failed;
+    int32_t *n_skipped;
+    uint8_t *complete;        /* 1 iff all k_p children have a terminal report (NULL ok) */
+    uint8_t *parent_state;    /* RO_PENDING if incomplete, else RO_FAILED if any member
+                                 failed, else RO_SUCCESS (NULL ok)                        */
+} ro_gather_out;
+
+/* F.reduce: ordered gather of reports into parent slots.  Slot p holds the
+ * bytes of parent p's RO_SUCCESS reports in ordinal order; an incomplete
+ * parent's slot holds the ones received so far; a parent with a failed
+ * member keeps its surviving bytes and is flagged RO_FAILED; a parent with
+ * no children is complete and RO_SUCCESS with an empty slot.  Errors:
+ * RO_ERANGE, RO_ESTATE, RO_EINVAL (offsets), RO_EDUP (two reports for one
+ * child), RO_ECAP (bytes > out_cap, or N above the reservation).
+ * out_data must not overlap the report bytes. */
+int ro_gather(ro_ctx *ctx, const ro_reports *reports, const int64_t *offsets, int64_t n_parents,
+              const ro_gather_out *out);
+
+/* Streaming gather over one expansion (offsets[P+1] on the device, kept by
+ * reference until ro_stream_destroy).  The stream's own state lives in
+ * device memory allocated here (about 20 bytes per child and 24 per parent). */
+typedef struct ro_stream ro_stream;
+int ro_stream_create(ro_ctx *ctx, const int64_t *offsets, int64_t n_parents, int64_t n_children,
+                     ro_stream **out);
+
+/* Record one wave of reports (same validation as ro_gather; a child already
+ * reported in an earlier wave is RO_EDUP).  The report bytes are read when
+ * their parent is emitted, so `data` must stay valid until then. */
+int ro_stream_report(ro_ctx *ctx, ro_stream *s, const ro_reports *wave);
+
+/* Emit every parent that is complete now and was not emitted before, in
+ * ascending parent order: emit_parent[e], its slot
+ * emit_data[emit_off[e], emit_off[e+1]), its counts and its state.  Needs
+ * room for cap_parents parents (emit_off: cap_parents + 1) and cap_bytes
+ * bytes (RO_ECAP).  The number of parents and bytes go to the device
+ * scalars *n_emitted_dev / *n_bytes_dev (either may be NULL).  Parents
+ * without children are emitted by the first call. */
+int ro_stream_emit(ro_ctx *ctx, ro_stream *s, uint32_t *emit_parent, int64_t *emit_off,
+                   uint8_t *emit_data, int64_t cap_parents, int64_t cap_bytes,
+                   int32_t *n_success, int32_t *n_failed, int32_t *n_skipped,
+                   uint8_t *parent_state, int64_t *n_emitted_dev, int64_t *n_bytes_dev);
+
+int ro_stream_destroy(ro_stream *s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RO_H */

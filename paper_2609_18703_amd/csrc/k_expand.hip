@@ -1,0 +1,134 @@
+// F.expand on gfx950: child counts -> Expansion offsets (decoupled look-back
+// scan) and per-child lineage keys (load-balanced over children).
+//
+// RayOrch (arXiv 2609.18703), Sec. 4 "Lineage State and Parent Completion":
+// each parent's Expansion is its ordered child set and every child carries
+// (parent, immutable zero-based ordinal).
+#include "ro_device.h"
+
+namespace ro {
+
+// Counts int32[P] -> offsets int64[P+1].  One tile = 4096 counts, 16 per
+// thread.  Tiles come from the ticket; the exclusive prefix of each tile
+// comes from the look-back.
+__global__ __launch_bounds__(kBlock) void k_expand_scan(const int32_t *__restrict__ counts, int64_t P,
+                                                        int64_t *__restrict__ offsets, int64_t child_cap,
+                                                        int want_tags, Ctl *ctl, uint64_t *desc,
+                                                        int64_t desc_cap, int64_t ntiles)
+{
+    const uint32_t epoch = scan_epoch(ctl);
+    __shared__ int64_t s_wave[kBlock / 64];
+    __shared__ uint64_t s_b;
+    __shared__ int64_t s_t;
+    __shared__ int32_t s_last;
+    for (;;) {
+        const int64_t t = next_ticket(ctl, &s_t);
+        if (t >= ntiles) break;
+        const int64_t i0 = t * kTile + (int64_t)threadIdx.x * kItems;
+        int32_t v[kItems];
+        int64_t sum = 0;
+        bool bad = false;
+#pragma unroll
+        for (int k = 0; k < kItems; ++k) {
+            const int64_t i = i0 + k;
+            int32_t x = i < P ? counts[i] : 0;
+            if (x < 0) { bad = true; x = 0; }
+            v[k] = x;
+            sum += x;
+        }
+        if (bad) raise_err(ctl, RO_EINVAL);
+        int64_t tot;
+        const int64_t ex = block_excl_scan(sum, s_wave, tot);
+        const uint64_t pre = tile_prefix(desc, t, epoch, (uint64_t)tot, &s_b, ctl);
+        int64_t run = (int64_t)pre + ex;
+#pragma unroll
+        for (int k = 0; k < kItems; ++k) {
+            const int64_t i = i0 + k;
+            if (i < P) offsets[i] = run;
+            run += v[k];
+        }
+        if (t == ntiles - 1 && threadIdx.x == 0) {
+            const int64_t n = (int64_t)pre + tot;
+            offsets[P] = n;
+            if (pre >= kSat || n >= ((int64_t)1 << 32)) raise_err(ctl, RO_EOVERFLOW);
+            else if (want_tags && n > child_cap) raise_err(ctl, RO_ECAP);
+        }
+    }
+    ticket_done(ctl, epoch, desc, desc_cap, &s_last);
+}
+
+// Lineage keys: child c -> (p, c - offsets[p]).  Each thread owns 16
+// consecutive children, finds the parent of the first one by binary search
+// and walks forward, so a huge parent is spread over as many threads as it
+// has children/16 and never serialises a wave.
+__global__ __launch_bounds__(kBlock) void k_expand_tags(const int64_t *__restrict__ offsets, int64_t P,
+                                                        uint32_t *__restrict__ child_parent,
+                                                        uint32_t *__restrict__ child_ordinal,
+                                                        int64_t child_cap, int vec_ok)
+{
+    const int64_t N = offsets[P];
+    if (N > child_cap || N >= ((int64_t)1 << 32)) return;     // reported by the scan
+    const int64_t nthreads = (N + kItems - 1) / kItems;
+    for (int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x; g < nthreads;
+         g += (int64_t)gridDim.x * kBlock) {
+        const int64_t c0 = g * kItems;
+        int64_t p = upper_bound_g(offsets, 0, P + 1, c0) - 1;
+        int64_t start = offsets[p];
+        int64_t next = offsets[p + 1];
+        uint32_t par[kItems], ord[kItems];
+#pragma unroll
+        for (int k = 0; k < kItems; ++k) {
+            const int64_t c = c0 + k;
+            if (c < N && c >= next) {
+                p = advance_parent(offsets, P, p, c);
+                start = offsets[p];
+                next = offsets[p + 1];
+            }
+            par[k] = (uint32_t)p;
+            ord[k] = (uint32_t)(c - start);
+        }
+        if (vec_ok && c0 + kItems <= N) {
+            if (child_parent) {
+                uint4 *dp = reinterpret_cast<uint4 *>(child_parent + c0);
+#pragma unroll
+                for (int k = 0; k < kItems / 4; ++k)
+                    dp[k] = make_uint4(par[4 * k], par[4 * k + 1], par[4 * k + 2], par[4 * k + 3]);
+            }
+            if (child_ordinal) {
+                uint4 *dp = reinterpret_cast<uint4 *>(child_ordinal + c0);
+#pragma unroll
+                for (int k = 0; k < kItems / 4; ++k)
+                    dp[k] = make_uint4(ord[4 * k], ord[4 * k + 1], ord[4 * k + 2], ord[4 * k + 3]);
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < kItems; ++k) {
+                if (c0 + k < N) {
+                    if (child_parent) child_parent[c0 + k] = par[k];
+                    if (child_ordinal) child_ordinal[c0 + k] = ord[k];
+                }
+            }
+        }
+    }
+}
+
+hipError_t launch_expand(const Launch &L, const int32_t *counts, int64_t P,
+                         int64_t *offsets, uint32_t *child_parent, uint32_t *child_ordinal,
+                         int64_t child_cap)
+{
+    const int64_t ntiles = P > 0 ? (P + kTile - 1) / kTile : 1;
+    const int want = (child_parent != nullptr || child_ordinal != nullptr);
+    const int64_t grid = ntiles < (int64_t)L.num_cus * 4 ? ntiles : (int64_t)L.num_cus * 4;
+    hipLaunchKernelGGL(k_expand_scan, dim3((unsigned)grid), dim3(kBlock), 0, L.stream, counts, P,
+                       offsets, child_cap, want, L.ctl, L.desc, L.desc_cap, ntiles);
+    if (want) {
+        const bool aligned = ((reinterpret_cast<uintptr_t>(child_parent) |
+                               reinterpret_cast<uintptr_t>(child_ordinal)) & 15u) == 0;
+        const int64_t grid2 = (int64_t)L.num_cus * 8;
+        hipLaunchKernelGGL(k_expand_tags, dim3((unsigned)grid2), dim3(kBlock), 0, L.stream, offsets,
+                           P, child_parent, child_ordinal, child_cap, aligned ? 1 : 0);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace ro

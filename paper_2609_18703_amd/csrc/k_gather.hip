@@ -1,0 +1,388 @@
+// F.reduce on gfx950: ordered gather of variable-length child reports into
+// parent slots, with per-parent counts and completion.
+//
+// RayOrch (arXiv 2609.18703), Sec. 4, Reduce rule: a parent resolves once its
+// Expansion and every member outcome are terminal; dropped members are left
+// out, failed members suppress the parent, present values appear in immutable
+// ordinal order, and zero survivors give an empty list.  The publication
+// rules of the same section reject a second, conflicting report.
+//
+// Four kernels:
+//   scatter  : report i -> canonical slot c = offsets[p] + o (validation, one
+//              16-byte store per report; the only random-access pass).
+//   scan     : canonical order, decoupled look-back over the surviving byte
+//              lengths -> every parent's slot offset, per-parent counts (LDS
+//              aggregated), per-sub-tile output bases.
+//   finalize : per parent: complete / state, trailing slot offsets, duplicate
+//              and capacity checks.
+//   copy     : per sub-tile of 1024 canonical children, a workgroup rebuilds
+//              the destination offsets in LDS and writes its contiguous output
+//              window as aligned 16-byte stores; sources are byte-aligned
+//              records read as aligned 16-byte pairs and realigned in registers.
+#include "ro_device.h"
+
+namespace ro {
+
+// ---------------------------------------------------------------- scatter
+__global__ __launch_bounds__(kBlock) void k_gather_scatter(
+    const uint32_t *__restrict__ rp, const uint32_t *__restrict__ ro_, const uint8_t *__restrict__ rs,
+    const int64_t *__restrict__ roff, const uint8_t *data, int64_t n,
+    const int64_t *__restrict__ offsets, int64_t P, Canon *__restrict__ canon, int64_t canon_cap,
+    int32_t *__restrict__ ns, int32_t *__restrict__ nf, int32_t *__restrict__ nk, Ctl *ctl)
+{
+    __shared__ int64_t s_wave[kBlock / 64];
+    const uint32_t epoch = ctl->canon_epoch;
+    const int64_t N = offsets[P];
+    const bool cap_ok = N <= canon_cap;
+    const int64_t gtid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    const int64_t gstride = (int64_t)gridDim.x * kBlock;
+    if (gtid == 0) {
+        if (!cap_ok) raise_err(ctl, RO_ECAP);
+        if (n > 0 && roff[0] < 0) raise_err(ctl, RO_EINVAL);
+    }
+    int err = 0;
+    // the Expansion must be an exclusive scan: offsets[0] = 0, nondecreasing
+    if (gtid == 0 && offsets[0] != 0) err = RO_EINVAL;
+    for (int64_t p = gtid; p < P; p += gstride) {
+        if (ns) ns[p] = 0;
+        if (nf) nf[p] = 0;
+        if (nk) nk[p] = 0;
+        if (offsets[p + 1] < offsets[p]) err = RO_EINVAL;
+    }
+    int64_t cnt = 0;
+    for (int64_t i = gtid; i < n; i += gstride) {
+        const uint32_t s = rs[i];
+        const int64_t o0 = roff[i], o1 = roff[i + 1];
+        if (o1 < o0) { err = RO_EINVAL; continue; }
+        if (s > RO_PENDING) { err = RO_ESTATE; continue; }
+        if (s == RO_PENDING) continue;
+        const uint32_t p = rp[i];
+        if ((int64_t)p >= P) { err = RO_ERANGE; continue; }
+        const int64_t st = offsets[p];
+        const uint32_t o = ro_[i];
+        if ((int64_t)o >= offsets[p + 1] - st) { err = RO_ERANGE; continue; }
+        const int64_t c = st + (int64_t)o;
+        if (st < 0 || c >= N) { err = RO_EINVAL; continue; }     // offsets not an Expansion
+        const int64_t len = s == RO_SUCCESS ? o1 - o0 : 0;
+        if (len >= ((int64_t)1 << 32)) { err = RO_EOVERFLOW; continue; }
+        ++cnt;
+        if (cap_ok) {
+            Canon e;
+            e.src = reinterpret_cast<uint64_t>(data) + (uint64_t)o0;
+            e.len = (uint32_t)len;
+            e.tag = (epoch << 2) | s;
+            canon[c] = e;
+        }
+    }
+    if (err) raise_err(ctl, err);
+    const int64_t tot = block_sum(cnt, s_wave);
+    if (threadIdx.x == 0 && tot)
+        __hip_atomic_fetch_add(&ctl->n_valid, tot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ---------------------------------------------------------------- scan
+// One tile = 4096 canonical children, 16 consecutive per thread; a wave
+// covers exactly one copy sub-tile (1024 children).
+__global__ __launch_bounds__(kBlock) void k_gather_scan(
+    const int64_t *__restrict__ offsets, int64_t P, const Canon *__restrict__ canon, int64_t canon_cap,
+    int64_t *__restrict__ out_off, int32_t *__restrict__ ns, int32_t *__restrict__ nf,
+    int32_t *__restrict__ nk, int64_t *__restrict__ sub_base, Ctl *ctl, uint64_t *desc,
+    int64_t desc_cap)
+{
+    const uint32_t epoch = ctl->canon_epoch;
+    const uint32_t sepoch = scan_epoch(ctl);
+    __shared__ int64_t s_wave[kBlock / 64];
+    __shared__ uint64_t s_b;
+    __shared__ int64_t s_t;
+    __shared__ int32_t s_last;
+    __shared__ int64_t s_p[2];
+    __shared__ int32_t s_cnt[3][kCntLds];
+    const int64_t N0 = offsets[P];
+    // over capacity, or an invalid Expansion found by the scatter: no tiles
+    const int64_t N = (N0 <= canon_cap && read_err(ctl) == 0) ? N0 : 0;
+    const int64_t ntiles = (N + kTile - 1) / kTile;
+    int32_t *cnt_out[3] = {ns, nf, nk};
+    int64_t filled_total = 0;
+    // a workgroup that sees no tiles draws no ticket, so every drawn ticket
+    // is processed even if workgroups disagree about an error raised meanwhile
+    while (ntiles > 0) {
+        const int64_t t = next_ticket(ctl, &s_t);
+        if (t >= ntiles) break;
+        const int64_t ct0 = t * kTile;
+        const int64_t ct1 = min64(ct0 + kTile, N);
+        if (threadIdx.x == 0) {
+            s_p[0] = upper_bound_g(offsets, 0, P + 1, ct0) - 1;
+            s_p[1] = upper_bound_g(offsets, s_p[0], P + 1, ct1 - 1) - 1;
+        }
+        __syncthreads();
+        const int64_t pf = s_p[0], pl = s_p[1];
+        const int64_t R = min64(pl - pf + 1, kCntLds);
+        for (int j = threadIdx.x; j < 3 * kCntLds; j += kBlock) (&s_cnt[0][0])[j] = 0;
+
+        // pass 1: surviving lengths and filled slots
+        const int64_t c0 = ct0 + (int64_t)threadIdx.x * kItems;
+        uint32_t len[kItems];
+        uint32_t stv[kItems];          // state, or 4 = not reported in this call
+        int64_t sum = 0, filled = 0;
+#pragma unroll
+        for (int k = 0; k < kItems; ++k) {
+            const int64_t c = c0 + k;
+            len[k] = 0;
+            stv[k] = 4;
+            if (c < ct1) {
+                const Canon e = canon[c];
+                if ((e.tag >> 2) == epoch) {
+                    stv[k] = e.tag & 3u;
+                    len[k] = stv[k] == RO_SUCCESS ? e.len : 0;
+                    ++filled;
+                }
+            }
+            sum += len[k];
+        }
+        filled_total += filled;
+        int64_t tot;
+        const int64_t ex = block_excl_scan(sum, s_wave, tot);
+        const uint64_t pre = tile_prefix(desc, t, sepoch, (uint64_t)tot, &s_b, ctl);
+        const int64_t base = (int64_t)pre + ex;
+        if ((threadIdx.x & 63) == 0) {
+            const int64_t sb = t * (kTile / kSub) + (threadIdx.x >> 6);
+            sub_base[sb] = base;                    // lane 0 of each wave starts a sub-tile
+        }
+
+        // pass 2: parents -- slot offsets and run-length counts
+        if (c0 < ct1) {
+            int64_t p = upper_bound_g(offsets, pf, pl + 1, c0) - 1;
+            int64_t pos = base;
+            if (offsets[p] == c0) {
+                // every parent whose first child is c0 (empty ones included)
+                const int64_t q0 = lower_bound_g(offsets, 0, p + 1, c0);
+                if (out_off)
+                    for (int64_t q = q0; q <= p; ++q) out_off[q] = pos;
+            }
+            int64_t next = offsets[p + 1];
+            int32_t run[3] = {0, 0, 0};
+            for (int k = 0; k < kItems; ++k) {
+                const int64_t c = c0 + k;
+                if (c >= ct1) break;
+                if (c >= next) {
+#pragma unroll
+                    for (int s = 0; s < 3; ++s) {
+                        if (run[s]) {
+                            if (p - pf < R) atomicAdd(&s_cnt[s][p - pf], run[s]);
+                            else if (cnt_out[s]) atomicAdd(&cnt_out[s][p], run[s]);
+                            run[s] = 0;
+                        }
+                    }
+                    const int64_t pn = advance_parent(offsets, P, p, c);
+                    if (out_off)
+                        for (int64_t q = p + 1; q <= pn; ++q) out_off[q] = pos;
+                    p = pn;
+                    next = offsets[p + 1];
+                }
+                if (stv[k] < 3) run[stv[k]] += 1;
+                pos += len[k];
+            }
+#pragma unroll
+            for (int s = 0; s < 3; ++s) {
+                if (run[s]) {
+                    if (p - pf < R) atomicAdd(&s_cnt[s][p - pf], run[s]);
+                    else if (cnt_out[s]) atomicAdd(&cnt_out[s][p], run[s]);
+                }
+            }
+        }
+        __syncthreads();
+        for (int64_t j = threadIdx.x; j < R; j += kBlock) {
+#pragma unroll
+            for (int s = 0; s < 3; ++s) {
+                const int32_t v = s_cnt[s][j];
+                if (v && cnt_out[s]) atomicAdd(&cnt_out[s][pf + j], v);
+            }
+        }
+        if (t == ntiles - 1 && threadIdx.x == 0) {
+            const int64_t total = (int64_t)pre + tot;
+            ctl->total = total;
+            if (pre >= kSat) raise_err(ctl, RO_EOVERFLOW);
+        }
+        __syncthreads();
+    }
+    const int64_t f = block_sum(filled_total, s_wave);
+    if (threadIdx.x == 0 && f)
+        __hip_atomic_fetch_add(&ctl->n_filled, f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    ticket_done(ctl, sepoch, desc, desc_cap, &s_last);
+}
+
+// ---------------------------------------------------------------- finalize
+__global__ __launch_bounds__(kBlock) void k_gather_finalize(
+    const int64_t *__restrict__ offsets, int64_t P, int64_t canon_cap, int64_t *__restrict__ out_off,
+    int64_t out_cap, int has_data, const int32_t *__restrict__ ns, const int32_t *__restrict__ nf,
+    const int32_t *__restrict__ nk, uint8_t *__restrict__ complete, uint8_t *__restrict__ pstate,
+    Ctl *ctl)
+{
+    const int64_t N0 = offsets[P];
+    const int64_t N = N0 <= canon_cap ? N0 : 0;
+    const int64_t total = N > 0 ? ctl->total : 0;
+    const int64_t gtid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (gtid == 0) {
+        if (out_off) out_off[P] = total;
+        if (ctl->n_filled != ctl->n_valid) raise_err(ctl, RO_EDUP);
+        if (has_data && total > out_cap) raise_err(ctl, RO_ECAP);
+    }
+    for (int64_t p = gtid; p < P; p += (int64_t)gridDim.x * kBlock) {
+        const int64_t st = offsets[p];
+        const int64_t k = offsets[p + 1] - st;
+        if (st >= N && out_off) out_off[p] = total;       // no child at or after its start
+        const int64_t a = ns ? ns[p] : 0, b = nf ? nf[p] : 0, c = nk ? nk[p] : 0;
+        const bool done = (a + b + c) == k;
+        if (complete) complete[p] = done ? 1 : 0;
+        if (pstate) pstate[p] = !done ? RO_PENDING : (b > 0 ? RO_FAILED : RO_SUCCESS);
+    }
+}
+
+// finalize needs all three counters even if the caller wants none of them;
+// the runtime passes workspace arrays in that case.
+
+// End of a gather: clear the per-call counters and advance the canonical epoch.
+__global__ void k_gather_reset(Ctl *ctl)
+{
+    if (threadIdx.x == 0) {
+        ctl->n_valid = 0;
+        ctl->n_filled = 0;
+        ctl->total = 0;
+        ctl->canon_epoch = ctl->canon_epoch + 1;
+    }
+}
+
+// ---------------------------------------------------------------- copy
+// 16 bytes starting at an arbitrary byte address, read as one or two aligned
+// 16-byte loads and shifted in registers.  Every aligned load covers at least
+// one byte of [p, p+16), so it never leaves a page that the record touches.
+__device__ __forceinline__ uint4 load16_any(uint64_t addr)
+{
+    const uint64_t a = addr & ~(uint64_t)15;
+    const uint32_t sh = (uint32_t)(addr & 15);
+    const uint4 lo = *reinterpret_cast<const uint4 *>(a);
+    if (sh == 0) return lo;
+    const uint4 hi = *reinterpret_cast<const uint4 *>(a + 16);
+    const uint32_t dw = sh >> 2, bs = sh & 3;
+    // pick w[dw .. dw+4] from (lo, hi)
+    uint32_t w0, w1, w2, w3, w4;
+    if (dw == 0)      { w0 = lo.x; w1 = lo.y; w2 = lo.z; w3 = lo.w; w4 = hi.x; }
+    else if (dw == 1) { w0 = lo.y; w1 = lo.z; w2 = lo.w; w3 = hi.x; w4 = hi.y; }
+    else if (dw == 2) { w0 = lo.z; w1 = lo.w; w2 = hi.x; w3 = hi.y; w4 = hi.z; }
+    else              { w0 = lo.w; w1 = hi.x; w2 = hi.y; w3 = hi.z; w4 = hi.w; }
+    uint4 r;
+    r.x = __builtin_amdgcn_alignbyte(w1, w0, bs);
+    r.y = __builtin_amdgcn_alignbyte(w2, w1, bs);
+    r.z = __builtin_amdgcn_alignbyte(w3, w2, bs);
+    r.w = __builtin_amdgcn_alignbyte(w4, w3, bs);
+    return r;
+}
+
+constexpr int kCopyPer = kSub / kBlock;   // 4 children per thread in the copy prologue
+
+__global__ __launch_bounds__(kBlock) void k_gather_copy(
+    const int64_t *__restrict__ offsets, int64_t P, const Canon *__restrict__ canon, int64_t canon_cap,
+    const int64_t *__restrict__ sub_base, uint8_t *__restrict__ out, Ctl *ctl)
+{
+    const uint32_t epoch = ctl->canon_epoch;
+    __shared__ int64_t s_dst[kSub + 1];     // destination offset of each record, relative
+    __shared__ uint64_t s_src[kSub];
+    __shared__ int64_t s_wave[kBlock / 64];
+    if (read_err(ctl) != 0) return;          // any recorded error: copy nothing
+    const int64_t N0 = offsets[P];
+    const int64_t N = N0 <= canon_cap ? N0 : 0;
+    const int64_t nsub = (N + kSub - 1) / kSub;
+    const uint64_t outa = reinterpret_cast<uint64_t>(out);
+    for (int64_t sb = blockIdx.x; sb < nsub; sb += gridDim.x) {
+        const int64_t c0 = sb * kSub;
+        const int64_t cnt = min64(kSub, N - c0);
+        // prologue: surviving lengths -> relative destination offsets
+        int64_t lsum = 0;
+        uint32_t l[kCopyPer];
+        uint64_t s[kCopyPer];
+#pragma unroll
+        for (int k = 0; k < kCopyPer; ++k) {
+            const int64_t r = (int64_t)threadIdx.x * kCopyPer + k;
+            l[k] = 0;
+            s[k] = 0;
+            if (r < cnt) {
+                const Canon e = canon[c0 + r];
+                if (e.tag == ((epoch << 2) | RO_SUCCESS)) {
+                    l[k] = e.len;
+                    s[k] = e.src;
+                }
+            }
+            lsum += l[k];
+        }
+        int64_t tot;
+        int64_t run = block_excl_scan(lsum, s_wave, tot);
+#pragma unroll
+        for (int k = 0; k < kCopyPer; ++k) {
+            const int r = threadIdx.x * kCopyPer + k;
+            s_dst[r] = run;
+            s_src[r] = s[k];
+            run += l[k];
+        }
+        if (threadIdx.x == 0) s_dst[kSub] = tot;
+        __syncthreads();
+        if (tot > 0) {
+            const int64_t D0 = sub_base[sb];
+            const int64_t D1 = D0 + tot;
+            const uint64_t a0 = (outa + (uint64_t)D0) & ~(uint64_t)15;
+            const uint64_t a1 = (outa + (uint64_t)D1 - 1) & ~(uint64_t)15;
+            const int64_t nchunks = (int64_t)((a1 - a0) >> 4) + 1;
+            for (int64_t ch = threadIdx.x; ch < nchunks; ch += kBlock) {
+                const uint64_t A = a0 + ((uint64_t)ch << 4);
+                const int64_t x = (int64_t)(A - outa) - D0;      // chunk start, relative to D0
+                const int64_t lo = x > 0 ? x : 0;
+                const int64_t hi = min64(x + 16, tot);
+                // record holding byte lo: largest r with s_dst[r] <= lo
+                int rl = 0, rh = kSub + 1;
+                while (rh - rl > 1) {
+                    const int mid = (rl + rh) >> 1;
+                    if (s_dst[mid] <= lo) rl = mid; else rh = mid;
+                }
+                int r = rl;
+                if (lo == x && hi == x + 16 && x + 16 <= s_dst[r + 1]) {
+                    const uint4 v = load16_any(s_src[r] + (uint64_t)(x - s_dst[r]));
+                    *reinterpret_cast<uint4 *>(A) = v;
+                } else {
+                    // chunk straddles records or the window edge: byte by byte
+                    uint8_t *dst = reinterpret_cast<uint8_t *>(A);
+                    for (int64_t y = lo; y < hi; ++y) {
+                        while (y >= s_dst[r + 1]) ++r;
+                        const uint8_t *sp = reinterpret_cast<const uint8_t *>(s_src[r]);
+                        dst[y - x] = sp[y - s_dst[r]];
+                    }
+                }
+            }
+        }
+        __syncthreads();
+    }
+}
+
+hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w)
+{
+    const int64_t grid_r = (int64_t)L.num_cus * 8;
+    hipLaunchKernelGGL(k_gather_scatter, dim3((unsigned)grid_r), dim3(kBlock), 0, L.stream, a.rp, a.ro,
+                       a.rs, a.roff, a.data, a.n, a.offsets, a.P, w.canon, w.canon_cap, a.ns, a.nf,
+                       a.nk, L.ctl);
+    const int64_t grid_s = (int64_t)L.num_cus * 4;
+    hipLaunchKernelGGL(k_gather_scan, dim3((unsigned)grid_s), dim3(kBlock), 0, L.stream, a.offsets, a.P,
+                       w.canon, w.canon_cap, a.out_off, a.ns, a.nf, a.nk, w.sub_base, L.ctl, L.desc,
+                       L.desc_cap);
+    int64_t grid_f = (a.P + kBlock - 1) / kBlock;
+    grid_f = grid_f < 1 ? 1 : (grid_f > (int64_t)L.num_cus * 8 ? (int64_t)L.num_cus * 8 : grid_f);
+    hipLaunchKernelGGL(k_gather_finalize, dim3((unsigned)grid_f), dim3(kBlock), 0, L.stream, a.offsets,
+                       a.P, w.canon_cap, a.out_off, a.out_cap, a.out_data != nullptr ? 1 : 0, a.ns, a.nf,
+                       a.nk, a.complete, a.pstate, L.ctl);
+    if (a.out_data != nullptr) {
+        const int64_t grid_c = (int64_t)L.num_cus * 8;
+        hipLaunchKernelGGL(k_gather_copy, dim3((unsigned)grid_c), dim3(kBlock), 0, L.stream, a.offsets,
+                           a.P, w.canon, w.canon_cap, w.sub_base, a.out_data, L.ctl);
+    }
+    hipLaunchKernelGGL(k_gather_reset, dim3(1), dim3(64), 0, L.stream, L.ctl);
+    return hipGetLastError();
+}
+
+}  // namespace ro

@@ -1,0 +1,50 @@
+// Context bookkeeping kernels: control-word initialisation and epoch resets.
+#include "ro_device.h"
+
+namespace ro {
+
+__global__ void k_ctl_init(Ctl *ctl)
+{
+    if (threadIdx.x == 0) {
+        ctl->scan_epoch = 1;
+        ctl->canon_epoch = 1;
+    }
+}
+
+// Clears every look-back descriptor and restarts the descriptor epoch at 1.
+__global__ void k_reset_scan_epoch(Ctl *ctl, uint64_t *desc, int64_t n)
+{
+    const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    for (int64_t i = g; i < n; i += (int64_t)gridDim.x * blockDim.x) desc[i] = 0;
+    if (g == 0) ctl->scan_epoch = 1;
+}
+
+// Clears every canonical slot's tag and restarts the canonical epoch at 1.
+__global__ void k_reset_canon(Ctl *ctl, Canon *canon, int64_t n)
+{
+    const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    for (int64_t i = g; i < n; i += (int64_t)gridDim.x * blockDim.x) canon[i].tag = 0;
+    if (g == 0) ctl->canon_epoch = 1;
+}
+
+hipError_t launch_ctl_init(const Launch &L)
+{
+    hipLaunchKernelGGL(k_ctl_init, dim3(1), dim3(64), 0, L.stream, L.ctl);
+    return hipGetLastError();
+}
+
+hipError_t launch_reset_scan_epoch(const Launch &L)
+{
+    hipLaunchKernelGGL(k_reset_scan_epoch, dim3((unsigned)L.num_cus), dim3(256), 0, L.stream, L.ctl,
+                       L.desc, L.desc_cap);
+    return hipGetLastError();
+}
+
+hipError_t launch_reset_canon(const Launch &L, Canon *canon, int64_t n)
+{
+    hipLaunchKernelGGL(k_reset_canon, dim3((unsigned)L.num_cus * 4), dim3(256), 0, L.stream, L.ctl,
+                       canon, n);
+    return hipGetLastError();
+}
+
+}  // namespace ro

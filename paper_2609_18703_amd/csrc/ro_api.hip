@@ -1,0 +1,309 @@
+// Host side of the C ABI: contexts, workspace, argument checks, launches.
+#include <stdlib.h>
+#include <string.h>
+
+#include "ro_internal.h"
+
+using namespace ro;
+
+struct ro_ctx {
+    hipStream_t stream;
+    int device;
+    int num_cus;
+    Ctl *ctl;
+    uint64_t *desc;
+    int64_t desc_cap;
+    Canon *canon;
+    int64_t canon_cap;
+    int64_t *sub_base;
+    int64_t sub_cap;
+    int64_t *samples;
+    int32_t *cnt;             // [3 * cnt_cap] counters used when the caller passes none
+    int64_t cnt_cap;
+    int64_t scan_launches;    // host shadow of the device scan epoch
+    int64_t gathers;          // host shadow of the device canonical epoch
+};
+
+struct ro_stream {
+    ro_ctx *ctx;
+    StreamState st;
+    void *block;              // one device allocation for all stream state
+};
+
+namespace {
+
+int hip_fail(hipError_t e) { return e == hipSuccess ? RO_OK : RO_EHIP; }
+
+Launch launch_of(ro_ctx *c)
+{
+    Launch L;
+    L.stream = c->stream;
+    L.num_cus = c->num_cus;
+    L.ctl = c->ctl;
+    L.desc = c->desc;
+    L.desc_cap = c->desc_cap;
+    return L;
+}
+
+template <typename T>
+hipError_t dev_alloc(T **p, int64_t n)
+{
+    *p = nullptr;
+    if (n <= 0) n = 1;
+    return hipMalloc(reinterpret_cast<void **>(p), (size_t)n * sizeof(T));
+}
+
+int64_t tiles_for(int64_t n) { return (n + kTile - 1) / kTile + 1; }
+
+// Make sure the look-back descriptors cover `tiles` tiles.
+int ensure_desc(ro_ctx *c, int64_t tiles)
+{
+    if (tiles <= c->desc_cap) return RO_OK;
+    if (hipStreamSynchronize(c->stream) != hipSuccess) return RO_EHIP;
+    (void)hipFree(c->desc);
+    c->desc = nullptr;
+    c->desc_cap = 0;
+    if (dev_alloc(&c->desc, tiles) != hipSuccess) return RO_EHIP;
+    if (hipMemset(c->desc, 0, (size_t)tiles * sizeof(uint64_t)) != hipSuccess) return RO_EHIP;
+    c->desc_cap = tiles;
+    return RO_OK;
+}
+
+int ensure_canon(ro_ctx *c, int64_t children)
+{
+    if (children <= c->canon_cap && c->canon) return RO_OK;
+    if (hipStreamSynchronize(c->stream) != hipSuccess) return RO_EHIP;
+    (void)hipFree(c->canon);
+    (void)hipFree(c->sub_base);
+    c->canon = nullptr;
+    c->sub_base = nullptr;
+    c->canon_cap = 0;
+    c->sub_cap = 0;
+    const int64_t n = children > 0 ? children : 1;
+    if (dev_alloc(&c->canon, n) != hipSuccess) return RO_EHIP;
+    if (hipMemset(c->canon, 0, (size_t)n * sizeof(Canon)) != hipSuccess) return RO_EHIP;
+    const int64_t subs = (n / kTile + 2) * (kTile / kSub);
+    if (dev_alloc(&c->sub_base, subs) != hipSuccess) return RO_EHIP;
+    c->canon_cap = n;
+    c->sub_cap = subs;
+    return ensure_desc(c, tiles_for(n));
+}
+
+int ensure_cnt(ro_ctx *c, int64_t parents)
+{
+    if (parents <= c->cnt_cap && c->cnt) return RO_OK;
+    if (hipStreamSynchronize(c->stream) != hipSuccess) return RO_EHIP;
+    (void)hipFree(c->cnt);
+    c->cnt = nullptr;
+    c->cnt_cap = 0;
+    const int64_t n = parents > 0 ? parents : 1;
+    if (dev_alloc(&c->cnt, 3 * n) != hipSuccess) return RO_EHIP;
+    c->cnt_cap = n;
+    return RO_OK;
+}
+
+// Called before every ticketed launch: if the 16-bit descriptor epoch is about
+// to wrap, clear the descriptors and restart the epoch at 1 first.
+int before_scan(ro_ctx *c, int launches)
+{
+    if (c->scan_launches + launches > (int64_t)kMaxScanEpoch) {
+        if (launch_reset_scan_epoch(launch_of(c)) != hipSuccess) return RO_EHIP;
+        c->scan_launches = 1;
+    }
+    c->scan_launches += launches;
+    return RO_OK;
+}
+
+int before_gather(ro_ctx *c)
+{
+    if (c->gathers + 1 > (int64_t)kMaxCanonEpoch) {
+        if (launch_reset_canon(launch_of(c), c->canon, c->canon_cap) != hipSuccess) return RO_EHIP;
+        c->gathers = 1;
+    }
+    c->gathers += 1;
+    return RO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ro_ctx_create(ro_ctx **out, void *hip_stream)
+{
+    if (out == nullptr) return RO_EINVAL;
+    *out = nullptr;
+    ro_ctx *c = (ro_ctx *)calloc(1, sizeof(ro_ctx));
+    if (!c) return RO_EINVAL;
+    c->stream = (hipStream_t)hip_stream;
+    if (hipGetDevice(&c->device) != hipSuccess ||
+        hipDeviceGetAttribute(&c->num_cus, hipDeviceAttributeMultiprocessorCount, c->device) != hipSuccess ||
+        dev_alloc(&c->ctl, 1) != hipSuccess || dev_alloc(&c->samples, kMaxSamples) != hipSuccess) {
+        ro_ctx_destroy(c);
+        return RO_EHIP;
+    }
+    if (c->num_cus <= 0) c->num_cus = 1;
+    if (hipMemset(c->ctl, 0, sizeof(Ctl)) != hipSuccess ||
+        launch_ctl_init(launch_of(c)) != hipSuccess || hipDeviceSynchronize() != hipSuccess ||
+        ensure_desc(c, 64) != RO_OK) {
+        ro_ctx_destroy(c);
+        return RO_EHIP;
+    }
+    c->scan_launches = 1;     // device scan epoch starts at 1
+    c->gathers = 1;           // device canonical epoch starts at 1
+    *out = c;
+    return RO_OK;
+}
+
+int ro_ctx_set_stream(ro_ctx *c, void *hip_stream)
+{
+    if (!c) return RO_EINVAL;
+    if (hipStreamSynchronize(c->stream) != hipSuccess) return RO_EHIP;
+    c->stream = (hipStream_t)hip_stream;
+    return RO_OK;
+}
+
+int ro_ctx_reserve(ro_ctx *c, int64_t max_children, int64_t max_parents, int64_t max_queue)
+{
+    if (!c || max_children < 0 || max_parents < 0 || max_queue < 0) return RO_EINVAL;
+    int rc = ensure_canon(c, max_children);
+    if (rc) return rc;
+    rc = ensure_cnt(c, max_parents);
+    if (rc) return rc;
+    int64_t m = max_children > max_parents ? max_children : max_parents;
+    m = m > max_queue ? m : max_queue;
+    return ensure_desc(c, tiles_for(m));
+}
+
+int ro_ctx_status(ro_ctx *c)
+{
+    if (!c) return RO_EINVAL;
+    if (hipStreamSynchronize(c->stream) != hipSuccess) return RO_EHIP;
+    int32_t err = 0;
+    if (hipMemcpy(&err, &c->ctl->err, sizeof(err), hipMemcpyDeviceToHost) != hipSuccess) return RO_EHIP;
+    if (err != 0) {
+        const int32_t zero = 0;
+        if (hipMemcpy(&c->ctl->err, &zero, sizeof(zero), hipMemcpyHostToDevice) != hipSuccess)
+            return RO_EHIP;
+    }
+    return err;
+}
+
+int ro_ctx_destroy(ro_ctx *c)
+{
+    if (!c) return RO_EINVAL;
+    if (c->stream || c->ctl) (void)hipStreamSynchronize(c->stream);
+    (void)hipFree(c->ctl);
+    (void)hipFree(c->desc);
+    (void)hipFree(c->canon);
+    (void)hipFree(c->sub_base);
+    (void)hipFree(c->samples);
+    (void)hipFree(c->cnt);
+    free(c);
+    return RO_OK;
+}
+
+int ro_expand(ro_ctx *c, const int32_t *counts, int64_t n_parents, int64_t *offsets,
+              uint32_t *child_parent, uint32_t *child_ordinal, int64_t child_cap)
+{
+    if (!c || !offsets || n_parents < 0 || child_cap < 0 || (n_parents > 0 && !counts)) return RO_EINVAL;
+    int rc = ensure_desc(c, tiles_for(n_parents));
+    if (rc) return rc;
+    if ((rc = before_scan(c, 1))) return rc;
+    return hip_fail(launch_expand(launch_of(c), counts, n_parents, offsets, child_parent, child_ordinal,
+                                  child_cap));
+}
+
+int ro_batch(ro_ctx *c, const uint32_t *queue, const uint8_t *keep, int64_t q_len,
+             const int64_t *offsets, int64_t n_parents, int32_t batch_size,
+             uint32_t *out_child, uint32_t *out_parent, uint32_t *out_ordinal, int64_t out_cap,
+             int64_t *n_out_dev, int64_t *n_batches_dev)
+{
+    if (!c || !offsets || q_len < 0 || n_parents < 0 || batch_size <= 0 || out_cap < 0 ||
+        (q_len > 0 && !queue))
+        return RO_EINVAL;
+    int rc = ensure_desc(c, tiles_for(q_len));
+    if (rc) return rc;
+    if ((rc = before_scan(c, 1))) return rc;
+    return hip_fail(launch_batch(launch_of(c), queue, keep, q_len, offsets, n_parents, batch_size,
+                                 out_child, out_parent, out_ordinal, out_cap, n_out_dev, n_batches_dev,
+                                 c->samples));
+}
+
+int ro_gather(ro_ctx *c, const ro_reports *r, const int64_t *offsets, int64_t n_parents,
+              const ro_gather_out *o)
+{
+    if (!c || !r || !o || !offsets || n_parents < 0 || r->n < 0 || !o->out_off || o->out_cap < 0)
+        return RO_EINVAL;
+    if (r->n > 0 && (!r->parent || !r->ordinal || !r->state || !r->off)) return RO_EINVAL;
+    if (o->out_data != nullptr && r->n > 0 && !r->data) return RO_EINVAL;
+    // the canonical workspace must cover the expansion; its size is on the
+    // device, so the report count is the host's best lower bound
+    int rc = ensure_canon(c, c->canon_cap > r->n ? c->canon_cap : r->n);
+    if (rc) return rc;
+    rc = ensure_desc(c, tiles_for(c->canon_cap));
+    if (rc) return rc;
+    GatherArgs a;
+    a.rp = r->parent;
+    a.ro = r->ordinal;
+    a.rs = r->state;
+    a.roff = r->off;
+    a.data = r->data;
+    a.n = r->n;
+    a.offsets = offsets;
+    a.P = n_parents;
+    a.out_off = o->out_off;
+    a.out_data = o->out_data;
+    a.out_cap = o->out_cap;
+    a.ns = o->n_success;
+    a.nf = o->n_failed;
+    a.nk = o->n_skipped;
+    a.complete = o->complete;
+    a.pstate = o->parent_state;
+    if (!a.ns || !a.nf || !a.nk) {
+        if ((rc = ensure_cnt(c, n_parents))) return rc;
+        if (!a.ns) a.ns = c->cnt;
+        if (!a.nf) a.nf = c->cnt + c->cnt_cap;
+        if (!a.nk) a.nk = c->cnt + 2 * c->cnt_cap;
+    }
+    GatherWs w;
+    w.canon = c->canon;
+    w.canon_cap = c->canon_cap;
+    w.sub_base = c->sub_base;
+    w.sub_cap = c->sub_cap;
+    if ((rc = before_scan(c, 1))) return rc;
+    if ((rc = before_gather(c))) return rc;
+    return hip_fail(launch_gather(launch_of(c), a, w));
+}
+
+int ro_stream_create(ro_ctx *c, const int64_t *offsets, int64_t n_parents, int64_t n_children,
+                     ro_stream **out)
+{
+    (void)c; (void)offsets; (void)n_parents; (void)n_children;
+    if (out) *out = nullptr;
+    return RO_EINVAL;
+}
+
+int ro_stream_report(ro_ctx *c, ro_stream *s, const ro_reports *wave)
+{
+    (void)c; (void)s; (void)wave;
+    return RO_EINVAL;
+}
+
+int ro_stream_emit(ro_ctx *c, ro_stream *s, uint32_t *emit_parent, int64_t *emit_off,
+                   uint8_t *emit_data, int64_t cap_parents, int64_t cap_bytes,
+                   int32_t *n_success, int32_t *n_failed, int32_t *n_skipped,
+                   uint8_t *parent_state, int64_t *n_emitted_dev, int64_t *n_bytes_dev)
+{
+    (void)c; (void)s; (void)emit_parent; (void)emit_off; (void)emit_data; (void)cap_parents;
+    (void)cap_bytes; (void)n_success; (void)n_failed; (void)n_skipped; (void)parent_state;
+    (void)n_emitted_dev; (void)n_bytes_dev;
+    return RO_EINVAL;
+}
+
+int ro_stream_destroy(ro_stream *s)
+{
+    (void)s;
+    return RO_EINVAL;
+}
+
+}  // extern "C"

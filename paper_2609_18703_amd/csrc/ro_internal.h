@@ -1,0 +1,117 @@
+// Internal declarations shared by the host runtime and the kernel sources.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "ro.h"
+
+namespace ro {
+
+constexpr int kBlock = 256;                 // threads per workgroup (4 waves of 64)
+constexpr int kItems = 16;                  // items per thread in scan tiles
+constexpr int kTile = kBlock * kItems;      // 4096 entries per scan tile
+constexpr int kSub = 1024;                  // children per copy sub-tile (one wave's share of a tile)
+constexpr int kMaxSamples = 2048;           // LDS-resident samples of the offsets array
+constexpr int kCntLds = 1024;               // parents aggregated in LDS per tile
+
+// Canonical per-child record written by the report scatter.  `tag` holds the
+// call epoch (bits 31..2) and the terminal state (bits 1..0): an entry is
+// valid for the current call only if its epoch matches, so the array never
+// needs clearing between calls.
+struct alignas(16) Canon {
+    uint64_t src;     // device address of the record's first byte
+    uint32_t len;     // bytes copied (0 unless SUCCESS)
+    uint32_t tag;     // epoch << 2 | state
+};
+static_assert(sizeof(Canon) == 16, "Canon must be 16 bytes");
+
+// Device-resident control words of one context.
+struct Ctl {
+    int32_t err;             // first error (0 = none)
+    uint32_t done;           // workgroups finished (ticketed kernels)
+    uint64_t ticket;         // next tile ticket (ticketed kernels)
+    int64_t n_valid;         // gather: accepted (non-pending) reports of this call
+    int64_t n_filled;        // gather: canonical slots holding this call's epoch
+    int64_t total;           // gather / emit: total bytes
+    int64_t n_items;         // emit: emitted parents
+    int64_t n_virtual;       // emit: children of emitted parents
+    uint32_t scan_epoch;     // look-back descriptor epoch of the next ticketed launch (1..65535)
+    uint32_t canon_epoch;    // canonical-slot epoch of the next gather (1..2^30-1)
+    int64_t pad[8];
+};
+
+struct Launch {
+    hipStream_t stream;
+    int num_cus;
+    Ctl *ctl;
+    uint64_t *desc;          // look-back descriptors
+    int64_t desc_cap;        // tiles
+};
+
+constexpr uint32_t kMaxScanEpoch = 65535;
+constexpr uint32_t kMaxCanonEpoch = (1u << 30) - 1;
+
+// Reset kernels the host enqueues when a device epoch is about to wrap.
+hipError_t launch_reset_scan_epoch(const Launch &L);
+hipError_t launch_reset_canon(const Launch &L, Canon *canon, int64_t n);
+hipError_t launch_ctl_init(const Launch &L);
+
+// ---- launchers (defined in the kernel sources) ----------------------------
+hipError_t launch_expand(const Launch &L, const int32_t *counts, int64_t P,
+                         int64_t *offsets, uint32_t *child_parent, uint32_t *child_ordinal,
+                         int64_t child_cap);
+
+hipError_t launch_batch(const Launch &L, const uint32_t *queue, const uint8_t *keep,
+                        int64_t Q, const int64_t *offsets, int64_t P, int32_t B,
+                        uint32_t *out_child, uint32_t *out_parent, uint32_t *out_ordinal,
+                        int64_t out_cap, int64_t *n_out, int64_t *n_batches, int64_t *samples);
+
+struct GatherArgs {
+    const uint32_t *rp, *ro;
+    const uint8_t *rs;
+    const int64_t *roff;
+    const uint8_t *data;
+    int64_t n;
+    const int64_t *offsets;
+    int64_t P;
+    int64_t *out_off;
+    uint8_t *out_data;
+    int64_t out_cap;
+    int32_t *ns, *nf, *nk;
+    uint8_t *complete, *pstate;
+};
+
+struct GatherWs {
+    Canon *canon;
+    int64_t canon_cap;
+    int64_t *sub_base;       // per copy sub-tile: first output byte
+    int64_t sub_cap;
+};
+
+hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w);
+
+// streaming
+struct StreamState {
+    const int64_t *offsets;
+    int64_t P, N;
+    Canon *canon;            // [N] accepted reports (tag epoch 1 = accepted)
+    uint32_t *seen;          // [N/32] duplicate detection bitmap
+    int32_t *cnt;            // [3*P] per-parent SUCCESS / FAILED / SKIPPED counts
+    uint8_t *emitted;        // [P]
+    uint32_t *elist;         // [P] emitted parents of the current emission
+    int64_t *evoff;          // [P+1] child offsets of the emitted parents (virtual children)
+    int64_t *sub_base;       // per sub-tile of virtual children
+    int64_t sub_cap;
+};
+
+hipError_t launch_stream_init(const Launch &L, StreamState &s);
+hipError_t launch_stream_report(const Launch &L, StreamState &s, const uint32_t *rp,
+                                const uint32_t *ro, const uint8_t *rs, const int64_t *roff,
+                                const uint8_t *data, int64_t n);
+hipError_t launch_stream_emit(const Launch &L, StreamState &s,
+                              uint32_t *emit_parent, int64_t *emit_off, uint8_t *emit_data,
+                              int64_t cap_parents, int64_t cap_bytes, int32_t *ns, int32_t *nf,
+                              int32_t *nk, uint8_t *pstate, int64_t *n_emitted, int64_t *n_bytes);
+
+}  // namespace ro

@@ -1,0 +1,121 @@
+"""Chains of ro calls for one expansion level and for two nested levels.
+
+These functions only sequence C-ABI calls on device tensors the caller owns;
+every step runs in the HIP library.
+
+Single level (a batch of one Call over the children of one expansion):
+  1. ro_expand  counts -> offsets, per-child (parent, ordinal)
+  2. ro_batch   ready queue with the dispatch mask -> report tags of the
+                dispatched children, in FIFO order, slots [0, M)
+  3. ro_batch   same queue with the sealed mask -> report tags of the children
+                that turned terminal without dispatch, slots [M, N)
+  4. ro_gather  reports -> parent slots, counts, completion
+
+Nested (two expansions, RayOrch's multi-grain program shape): the lower
+gather's slots and derived states are the upper level's child reports, keyed
+by the level-1 children's own lineage (parent, ordinal).
+"""
+from __future__ import annotations
+
+import torch
+
+__all__ = ["SingleLevelBuffers", "single_level", "NestedBuffers", "nested"]
+
+
+def _empty(n, dtype):
+    return torch.empty(max(int(n), 1), dtype=dtype, device="cuda")
+
+
+class SingleLevelBuffers:
+    """Device inputs and outputs of one single-level pipeline."""
+
+    def __init__(self, counts, queue, keep, sealed, rep_state, rep_off, data, n_children,
+                 n_dispatched, batch_size, out_cap=None, want_data=True):
+        P = counts.numel()
+        N = int(n_children)
+        self.counts, self.queue, self.keep, self.sealed = counts, queue, keep, sealed
+        self.rep_state, self.rep_off, self.data = rep_state, rep_off, data
+        self.N, self.M, self.B = N, int(n_dispatched), int(batch_size)
+        self.offsets = _empty(P + 1, torch.int64)
+        self.child_parent = _empty(N, torch.int32)
+        self.child_ordinal = _empty(N, torch.int32)
+        self.rep_parent = _empty(N, torch.int32)
+        self.rep_ordinal = _empty(N, torch.int32)
+        self.scalars = torch.zeros(4, dtype=torch.int64, device="cuda")   # M, nb, N-M, nb'
+        self.out_off = _empty(P + 1, torch.int64)
+        if out_cap is None:
+            out_cap = int(rep_off[-1].item() - rep_off[0].item()) if N else 0
+        self.out_cap = int(out_cap)
+        self.out_data = _empty(self.out_cap, torch.uint8) if want_data else None
+        self.n_success = _empty(P, torch.int32)
+        self.n_failed = _empty(P, torch.int32)
+        self.n_skipped = _empty(P, torch.int32)
+        self.complete = _empty(P, torch.uint8)
+        self.parent_state = _empty(P, torch.uint8)
+
+
+def single_level(ctx, b: SingleLevelBuffers):
+    """Enqueue the four calls of one level on ctx's stream."""
+    N, M = b.N, b.M
+    ctx.expand(b.counts, b.offsets, b.child_parent, b.child_ordinal)
+    ctx.batch(b.queue, b.keep, b.offsets, b.B, None, b.rep_parent, b.rep_ordinal,
+              b.scalars[0:1], b.scalars[1:2], out_cap=M)
+    if N > M:
+        ctx.batch(b.queue, b.sealed, b.offsets, b.B, None, b.rep_parent[M:], b.rep_ordinal[M:],
+                  b.scalars[2:3], b.scalars[3:4], out_cap=N - M)
+    ctx.gather(b.rep_parent, b.rep_ordinal, b.rep_state, b.rep_off, b.data, b.offsets, b.out_off,
+               b.out_data, b.n_success, b.n_failed, b.n_skipped, b.complete, b.parent_state, n=N,
+               out_cap=b.out_cap)
+
+
+class NestedBuffers:
+    """Device inputs and outputs of a two-level pipeline (top -> mid -> leaf)."""
+
+    def __init__(self, counts1, queue1, batch1, counts2, queue2, batch2, leaf_state, leaf_off,
+                 leaf_data, n_mid, n_leaf, want_data=True):
+        P1 = counts1.numel()
+        self.P1, self.N1, self.N2 = P1, int(n_mid), int(n_leaf)
+        self.counts1, self.queue1, self.B1 = counts1, queue1, int(batch1)
+        self.counts2, self.queue2, self.B2 = counts2, queue2, int(batch2)
+        self.leaf_state, self.leaf_off, self.leaf_data = leaf_state, leaf_off, leaf_data
+        N1, N2 = self.N1, self.N2
+        self.offsets1 = _empty(P1 + 1, torch.int64)
+        self.mid_parent = _empty(N1, torch.int32)
+        self.mid_ordinal = _empty(N1, torch.int32)
+        self.b1_parent = _empty(N1, torch.int32)
+        self.b1_ordinal = _empty(N1, torch.int32)
+        self.offsets2 = _empty(N1 + 1, torch.int64)
+        self.leaf_parent = _empty(N2, torch.int32)
+        self.leaf_ordinal = _empty(N2, torch.int32)
+        self.b2_parent = _empty(N2, torch.int32)
+        self.b2_ordinal = _empty(N2, torch.int32)
+        self.scalars = torch.zeros(4, dtype=torch.int64, device="cuda")
+        cap = int(leaf_off[-1].item() - leaf_off[0].item()) if N2 else 0
+        self.mid_off = _empty(N1 + 1, torch.int64)
+        self.mid_data = _empty(cap, torch.uint8) if want_data else None
+        self.mid_cnt = _empty(3 * N1, torch.int32)
+        self.mid_complete = _empty(N1, torch.uint8)
+        self.mid_state = _empty(N1, torch.uint8)
+        self.top_off = _empty(P1 + 1, torch.int64)
+        self.top_data = _empty(cap, torch.uint8) if want_data else None
+        self.top_cnt = _empty(3 * P1, torch.int32)
+        self.top_complete = _empty(P1, torch.uint8)
+        self.top_state = _empty(P1, torch.uint8)
+        self.cap = cap
+
+
+def nested(ctx, b: NestedBuffers):
+    """expand(top) -> batch(mid) -> expand(mid) -> batch(leaf) -> gather(leaf->mid) -> gather(mid->top)."""
+    N1, N2 = b.N1, b.N2
+    ctx.expand(b.counts1, b.offsets1, b.mid_parent, b.mid_ordinal)
+    ctx.batch(b.queue1, None, b.offsets1, b.B1, None, b.b1_parent, b.b1_ordinal,
+              b.scalars[0:1], b.scalars[1:2], out_cap=N1)
+    ctx.expand(b.counts2, b.offsets2, b.leaf_parent, b.leaf_ordinal)
+    ctx.batch(b.queue2, None, b.offsets2, b.B2, None, b.b2_parent, b.b2_ordinal,
+              b.scalars[2:3], b.scalars[3:4], out_cap=N2)
+    ctx.gather(b.b2_parent, b.b2_ordinal, b.leaf_state, b.leaf_off, b.leaf_data, b.offsets2,
+               b.mid_off, b.mid_data, b.mid_cnt[:N1], b.mid_cnt[N1:2 * N1], b.mid_cnt[2 * N1:],
+               b.mid_complete, b.mid_state, n=N2, out_cap=b.cap)
+    ctx.gather(b.mid_parent, b.mid_ordinal, b.mid_state, b.mid_off, b.mid_data, b.offsets1,
+               b.top_off, b.top_data, b.top_cnt[:b.P1], b.top_cnt[b.P1:2 * b.P1], b.top_cnt[2 * b.P1:],
+               b.top_complete, b.top_state, n=N1, out_cap=b.cap)

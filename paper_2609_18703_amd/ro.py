@@ -1,0 +1,197 @@
+"""Python binding of the ``ro`` C ABI (argument marshalling only).
+
+Every array argument is a torch tensor on the GPU; the binding passes its
+data pointer and size to ``libro.so`` and the torch current stream to the
+context.  Nothing here computes any step of the path.  If the library is
+missing, loading fails loudly: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+__all__ = ["RoError", "load", "Context", "Stream", "OK", "EINVAL", "ERANGE", "EDUP", "ECAP",
+           "EOVERFLOW", "ESTATE", "EHIP", "SUCCESS", "FAILED", "SKIPPED", "PENDING", "LIB_PATH"]
+
+OK, EINVAL, ERANGE, EDUP, ECAP, EOVERFLOW, ESTATE, EHIP = 0, -1, -2, -3, -4, -5, -6, -7
+SUCCESS, FAILED, SKIPPED, PENDING = 0, 1, 2, 3
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libro.so")
+
+
+class RoError(RuntimeError):
+    def __init__(self, code, what):
+        super().__init__(f"{what}: ro error {code}")
+        self.code = code
+
+
+class ReportsT(C.Structure):
+    _fields_ = [("parent", C.c_void_p), ("ordinal", C.c_void_p), ("state", C.c_void_p),
+                ("off", C.c_void_p), ("data", C.c_void_p), ("n", C.c_int64)]
+
+
+class GatherOutT(C.Structure):
+    _fields_ = [("out_off", C.c_void_p), ("out_data", C.c_void_p), ("out_cap", C.c_int64),
+                ("n_success", C.c_void_p), ("n_failed", C.c_void_p), ("n_skipped", C.c_void_p),
+                ("complete", C.c_void_p), ("parent_state", C.c_void_p)]
+
+
+_lib = None
+
+
+def load(path=None):
+    """Load libro.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    path = path or LIB_PATH
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with paper_2609_18703_amd/build.py")
+    L = C.CDLL(path)
+    P, i64, i32 = C.c_void_p, C.c_int64, C.c_int32
+    pp = C.POINTER(C.c_void_p)
+    L.ro_ctx_create.argtypes = [pp, P]
+    L.ro_ctx_set_stream.argtypes = [P, P]
+    L.ro_ctx_reserve.argtypes = [P, i64, i64, i64]
+    L.ro_ctx_status.argtypes = [P]
+    L.ro_ctx_destroy.argtypes = [P]
+    L.ro_expand.argtypes = [P, P, i64, P, P, P, i64]
+    L.ro_batch.argtypes = [P, P, P, i64, P, i64, i32, P, P, P, i64, P, P]
+    L.ro_gather.argtypes = [P, C.POINTER(ReportsT), P, i64, C.POINTER(GatherOutT)]
+    L.ro_stream_create.argtypes = [P, P, i64, i64, pp]
+    L.ro_stream_report.argtypes = [P, P, C.POINTER(ReportsT)]
+    L.ro_stream_emit.argtypes = [P, P, P, P, P, i64, i64, P, P, P, P, P, P]
+    L.ro_stream_destroy.argtypes = [P]
+    for name in ("ro_ctx_create", "ro_ctx_set_stream", "ro_ctx_reserve", "ro_ctx_status",
+                 "ro_ctx_destroy", "ro_expand", "ro_batch", "ro_gather", "ro_stream_create",
+                 "ro_stream_report", "ro_stream_emit", "ro_stream_destroy"):
+        getattr(L, name).restype = C.c_int
+    if path == LIB_PATH:
+        _lib = L
+    return L
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("ro arrays must live in GPU memory")
+    if not t.is_contiguous():
+        raise ValueError("ro arrays must be contiguous")
+    return C.c_void_p(t.data_ptr())
+
+
+def _check(rc, what):
+    if rc != OK:
+        raise RoError(rc, what)
+
+
+def _reports(parent, ordinal, state, off, data, n=None):
+    n = parent.numel() if n is None else n
+    return ReportsT(_ptr(parent), _ptr(ordinal), _ptr(state), _ptr(off), _ptr(data), n)
+
+
+class Context:
+    """An ro context bound to a HIP stream (torch's current stream by default)."""
+
+    def __init__(self, stream=None):
+        import torch
+        self.L = load()
+        if stream is None:
+            stream = torch.cuda.current_stream()
+        self._stream = stream
+        h = C.c_void_p()
+        _check(self.L.ro_ctx_create(C.byref(h), C.c_void_p(stream.cuda_stream)), "ro_ctx_create")
+        self.h = h
+
+    def reserve(self, max_children, max_parents, max_queue=0):
+        _check(self.L.ro_ctx_reserve(self.h, int(max_children), int(max_parents), int(max_queue)),
+               "ro_ctx_reserve")
+
+    def status(self):
+        return self.L.ro_ctx_status(self.h)
+
+    def check(self, what="device"):
+        _check(self.status(), what)
+
+    def expand(self, counts, offsets, child_parent=None, child_ordinal=None):
+        cap = 0
+        if child_parent is not None or child_ordinal is not None:
+            cap = min(t.numel() for t in (child_parent, child_ordinal) if t is not None)
+        _check(self.L.ro_expand(self.h, _ptr(counts), counts.numel(), _ptr(offsets),
+                                _ptr(child_parent), _ptr(child_ordinal), cap), "ro_expand")
+
+    def batch(self, queue, keep, offsets, batch_size, out_child=None, out_parent=None,
+              out_ordinal=None, n_out=None, n_batches=None, q_len=None, out_cap=None):
+        q_len = queue.numel() if q_len is None else q_len
+        if out_cap is None:
+            outs = [t.numel() for t in (out_child, out_parent, out_ordinal) if t is not None]
+            out_cap = min(outs) if outs else q_len
+        _check(self.L.ro_batch(self.h, _ptr(queue), _ptr(keep), q_len, _ptr(offsets),
+                               offsets.numel() - 1, int(batch_size), _ptr(out_child), _ptr(out_parent),
+                               _ptr(out_ordinal), int(out_cap), _ptr(n_out), _ptr(n_batches)),
+               "ro_batch")
+
+    def gather(self, parent, ordinal, state, off, data, offsets, out_off, out_data=None,
+               n_success=None, n_failed=None, n_skipped=None, complete=None, parent_state=None,
+               n=None, out_cap=None):
+        rep = _reports(parent, ordinal, state, off, data, n)
+        if out_cap is None:
+            out_cap = out_data.numel() if out_data is not None else 0
+        out = GatherOutT(_ptr(out_off), _ptr(out_data), int(out_cap), _ptr(n_success), _ptr(n_failed),
+                         _ptr(n_skipped), _ptr(complete), _ptr(parent_state))
+        _check(self.L.ro_gather(self.h, C.byref(rep), _ptr(offsets), offsets.numel() - 1, C.byref(out)),
+               "ro_gather")
+
+    def stream(self, offsets, n_children):
+        return Stream(self, offsets, n_children)
+
+    def close(self):
+        if getattr(self, "h", None):
+            self.L.ro_ctx_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Stream:
+    """Streaming gather over one expansion."""
+
+    def __init__(self, ctx, offsets, n_children):
+        self.ctx = ctx
+        self.offsets = offsets
+        h = C.c_void_p()
+        _check(ctx.L.ro_stream_create(ctx.h, _ptr(offsets), offsets.numel() - 1, int(n_children),
+                                      C.byref(h)), "ro_stream_create")
+        self.h = h
+
+    def report(self, parent, ordinal, state, off, data, n=None):
+        rep = _reports(parent, ordinal, state, off, data, n)
+        _check(self.ctx.L.ro_stream_report(self.ctx.h, self.h, C.byref(rep)), "ro_stream_report")
+
+    def emit(self, emit_parent, emit_off, emit_data, n_success=None, n_failed=None, n_skipped=None,
+             parent_state=None, n_emitted=None, n_bytes=None, cap_parents=None, cap_bytes=None):
+        if cap_parents is None:
+            cap_parents = emit_off.numel() - 1
+        if cap_bytes is None:
+            cap_bytes = emit_data.numel() if emit_data is not None else 0
+        _check(self.ctx.L.ro_stream_emit(self.ctx.h, self.h, _ptr(emit_parent), _ptr(emit_off),
+                                         _ptr(emit_data), int(cap_parents), int(cap_bytes),
+                                         _ptr(n_success), _ptr(n_failed), _ptr(n_skipped),
+                                         _ptr(parent_state), _ptr(n_emitted), _ptr(n_bytes)),
+               "ro_stream_emit")
+
+    def close(self):
+        if getattr(self, "h", None):
+            self.ctx.L.ro_stream_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

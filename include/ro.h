@@ -89,6 +89,20 @@ int ro_ctx_status(ro_ctx *ctx);
 /* Free the context's workspace.  Waits for its stream first. */
 int ro_ctx_destroy(ro_ctx *ctx);
 
+/* Per-kernel timing (measurement aid).  While enabled, every kernel the
+ * context launches is bracketed by two HIP events on the context's stream.
+ * ro_ctx_trace_read waits for the stream, adds up the elapsed time per
+ * kernel kind since the last read into launches[k] / total_ms[k] for
+ * k < n (indices below), and clears the record. */
+enum {
+    RO_K_EXPAND_SCAN = 0, RO_K_EXPAND_TAGS, RO_K_BATCH_SAMPLES, RO_K_BATCH,
+    RO_K_GATHER_SCATTER, RO_K_GATHER_SCAN, RO_K_GATHER_FINALIZE, RO_K_GATHER_COPY,
+    RO_K_GATHER_RESET, RO_K_STREAM_REPORT, RO_K_STREAM_SELECT, RO_K_STREAM_SCAN,
+    RO_K_STREAM_COPY, RO_K_STREAM_FINISH, RO_K_MISC, RO_K_COUNT
+};
+int ro_ctx_trace(ro_ctx *ctx, int enable);
+int ro_ctx_trace_read(ro_ctx *ctx, int64_t *launches, double *total_ms, int32_t n);
+
 /* F.expand.  counts[P] (int32, >= 0) -> offsets[P+1] (int64 exclusive scan,
  * offsets[P] = N): parent p's ordered children are the canonical ids
  * [offsets[p], offsets[p+1]).  If child_parent / child_ordinal are not NULL,

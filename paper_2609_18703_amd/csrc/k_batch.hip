@@ -135,13 +135,13 @@ hipError_t launch_batch(const Launch &L, const uint32_t *queue, const uint8_t *k
     int shift = 0;
     while ((((P + 1) + ((int64_t)1 << shift) - 1) >> shift) > kMaxSamples) ++shift;
     const int64_t nsamp = ((P + 1) + ((int64_t)1 << shift) - 1) >> shift;
-    hipLaunchKernelGGL(k_batch_samples, dim3((unsigned)((nsamp + 255) / 256)), dim3(256), 0, L.stream,
+    RO_LAUNCH(L, RO_K_BATCH_SAMPLES, k_batch_samples, dim3((unsigned)((nsamp + 255) / 256)), dim3(256), 0, L.stream,
                        offsets, P, shift, nsamp, samples);
     const int64_t ntiles = Q > 0 ? (Q + kTile - 1) / kTile : 1;
     const int64_t cap_grid = (int64_t)L.num_cus * 4;
     const int64_t grid = ntiles < cap_grid ? ntiles : cap_grid;
     const bool aligned = ((reinterpret_cast<uintptr_t>(queue) | reinterpret_cast<uintptr_t>(keep)) & 15u) == 0;
-    hipLaunchKernelGGL(k_batch, dim3((unsigned)grid), dim3(kBlock), 0, L.stream, queue, keep, Q, offsets,
+    RO_LAUNCH(L, RO_K_BATCH, k_batch, dim3((unsigned)grid), dim3(kBlock), 0, L.stream, queue, keep, Q, offsets,
                        P, samples, nsamp, shift, B, out_child, out_parent, out_ordinal, out_cap, n_out,
                        n_batches, L.ctl, L.desc, L.desc_cap, ntiles, aligned ? 1 : 0);
     return hipGetLastError();

@@ -119,13 +119,13 @@ hipError_t launch_expand(const Launch &L, const int32_t *counts, int64_t P,
     const int64_t ntiles = P > 0 ? (P + kTile - 1) / kTile : 1;
     const int want = (child_parent != nullptr || child_ordinal != nullptr);
     const int64_t grid = ntiles < (int64_t)L.num_cus * 4 ? ntiles : (int64_t)L.num_cus * 4;
-    hipLaunchKernelGGL(k_expand_scan, dim3((unsigned)grid), dim3(kBlock), 0, L.stream, counts, P,
+    RO_LAUNCH(L, RO_K_EXPAND_SCAN, k_expand_scan, dim3((unsigned)grid), dim3(kBlock), 0, L.stream, counts, P,
                        offsets, child_cap, want, L.ctl, L.desc, L.desc_cap, ntiles);
     if (want) {
         const bool aligned = ((reinterpret_cast<uintptr_t>(child_parent) |
                                reinterpret_cast<uintptr_t>(child_ordinal)) & 15u) == 0;
         const int64_t grid2 = (int64_t)L.num_cus * 8;
-        hipLaunchKernelGGL(k_expand_tags, dim3((unsigned)grid2), dim3(kBlock), 0, L.stream, offsets,
+        RO_LAUNCH(L, RO_K_EXPAND_TAGS, k_expand_tags, dim3((unsigned)grid2), dim3(kBlock), 0, L.stream, offsets,
                            P, child_parent, child_ordinal, child_cap, aligned ? 1 : 0);
     }
     return hipGetLastError();

@@ -253,18 +253,30 @@ __global__ void k_gather_reset(Ctl *ctl)
 }
 
 // ---------------------------------------------------------------- copy
-// 16 bytes starting at an arbitrary byte address, read as one or two aligned
-// 16-byte loads and shifted in registers.  Every aligned load covers at least
-// one byte of [p, p+16), so it never leaves a page that the record touches.
-__device__ __forceinline__ uint4 load16_any(uint64_t addr)
+// Payload accesses use explicit global-address-space pointers so they compile
+// to global_load/global_store (flat accesses would also hold up every LDS
+// read of the record search behind outstanding memory traffic).
+#define RO_GLOBAL __attribute__((address_space(1)))
+
+typedef uint32_t v4u32 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint4 ld16(uint64_t a)
 {
-    const uint64_t a = addr & ~(uint64_t)15;
-    const uint32_t sh = (uint32_t)(addr & 15);
-    const uint4 lo = *reinterpret_cast<const uint4 *>(a);
-    if (sh == 0) return lo;
-    const uint4 hi = *reinterpret_cast<const uint4 *>(a + 16);
+    const v4u32 t = *(const RO_GLOBAL v4u32 *)a;
+    return make_uint4(t.x, t.y, t.z, t.w);
+}
+__device__ __forceinline__ void st16(uint64_t a, uint4 v)
+{
+    const v4u32 t = {v.x, v.y, v.z, v.w};
+    *(RO_GLOBAL v4u32 *)a = t;
+}
+__device__ __forceinline__ uint8_t ld8(uint64_t a) { return *(const RO_GLOBAL uint8_t *)a; }
+__device__ __forceinline__ void st8(uint64_t a, uint8_t v) { *(RO_GLOBAL uint8_t *)a = v; }
+
+// Bytes sh..sh+15 of the 32-byte pair (lo, hi).
+__device__ __forceinline__ uint4 shift16(const uint4 &lo, const uint4 &hi, uint32_t sh)
+{
     const uint32_t dw = sh >> 2, bs = sh & 3;
-    // pick w[dw .. dw+4] from (lo, hi)
     uint32_t w0, w1, w2, w3, w4;
     if (dw == 0)      { w0 = lo.x; w1 = lo.y; w2 = lo.z; w3 = lo.w; w4 = hi.x; }
     else if (dw == 1) { w0 = lo.y; w1 = lo.z; w2 = lo.w; w3 = hi.x; w4 = hi.y; }
@@ -278,14 +290,170 @@ __device__ __forceinline__ uint4 load16_any(uint64_t addr)
     return r;
 }
 
+// One record's share of an output chunk: output bytes fv..lv (0..15) come
+// from source addresses S+fv .. S+lv.  Only the aligned 16-byte source
+// chunks holding some of those bytes are read, so no load leaves a page the
+// record occupies.
+struct Piece {
+    uint4 lo, hi;
+    uint32_t sh;
+    int fv, lv;
+};
+
+__device__ __forceinline__ void piece_load(Piece &p, uint64_t S, int fv, int lv)
+{
+    const uint64_t c0 = S & ~(uint64_t)15;
+    p.sh = (uint32_t)(S & 15);
+    p.fv = fv;
+    p.lv = lv;
+    const bool need0 = S + (uint64_t)fv < c0 + 16;
+    const bool need1 = S + (uint64_t)lv >= c0 + 16;
+    // Both loads are unconditional (a conditional load makes the compiler
+    // zero its destination first, which waits for every outstanding memory
+    // operation); a half that is not needed re-reads the one that is, and
+    // its bytes are masked off by piece_merge.
+    p.lo = ld16(need0 ? c0 : c0 + 16);
+    p.hi = ld16(need1 ? c0 + 16 : c0);
+}
+
+// Byte mask of output bytes fv..lv that fall in dword j.
+__device__ __forceinline__ uint32_t byte_mask(int j, int fv, int lv)
+{
+    const int a = fv - 4 * j > 0 ? fv - 4 * j : 0;
+    const int b = lv - 4 * j < 3 ? lv - 4 * j : 3;
+    if (a > b) return 0u;
+    return (0xffffffffu >> (8 * (3 - b))) & (0xffffffffu << (8 * a));
+}
+
+__device__ __forceinline__ void piece_merge(uint4 &acc, const Piece &p)
+{
+    const uint4 v = shift16(p.lo, p.hi, p.sh);
+    uint32_t m;
+    m = byte_mask(0, p.fv, p.lv); acc.x = (acc.x & ~m) | (v.x & m);
+    m = byte_mask(1, p.fv, p.lv); acc.y = (acc.y & ~m) | (v.y & m);
+    m = byte_mask(2, p.fv, p.lv); acc.z = (acc.z & ~m) | (v.z & m);
+    m = byte_mask(3, p.fv, p.lv); acc.w = (acc.w & ~m) | (v.w & m);
+}
+
+__device__ __forceinline__ uint32_t dword_of(const uint4 &v, int j)
+{
+    return j == 0 ? v.x : (j == 1 ? v.y : (j == 2 ? v.z : v.w));
+}
+
 constexpr int kCopyPer = kSub / kBlock;   // 4 children per thread in the copy prologue
 
-__global__ __launch_bounds__(kBlock) void k_gather_copy(
+// Largest r in [r, kSub] with s_dst[r] <= pos, given s_dst[r] <= pos: a few
+// linear steps (the usual distance between neighbouring chunks), then a
+// binary search.  Zero-length records are stepped over.
+__device__ __forceinline__ int advance_record(const int32_t *s_dst, int r, int pos)
+{
+#pragma unroll 1
+    for (int step = 0; step < 6; ++step) {
+        if (s_dst[r + 1] > pos) return r;
+        ++r;
+    }
+    int rl = r, rh = kSub + 1;
+    while (rh - rl > 1) {
+        const int mid = (rl + rh) >> 1;
+        if (s_dst[mid] <= pos) rl = mid; else rh = mid;
+    }
+    return rl;
+}
+
+// Store the bytes [b0, b1) (0..16) of a 16-byte chunk value at A.
+__device__ __forceinline__ void store_partial(uint64_t A, const uint4 &v, int b0, int b1)
+{
+    for (int b = b0; b < b1; ++b) st8(A + (uint64_t)b, (uint8_t)(dword_of(v, b >> 2) >> (8 * (b & 3))));
+}
+
+// A sub-tile whose output window is under 2 GiB: positions relative to the
+// window start fit in 32 bits.  Each wave owns a contiguous run of 64-chunk
+// groups and lane `lane` takes chunk 64*g + lane of every group g, so the
+// record it reads from only moves forward.  Every chunk strictly inside the
+// window is written with one aligned 16-byte store; chunks that straddle
+// records are assembled from their pieces first.
+__device__ __forceinline__ void copy_window32(const int32_t *s_dst, const uint64_t *s_src, int tot,
+                                              uint64_t outa, int64_t D0, int wave, int lane)
+{
+    const uint64_t a0 = (outa + (uint64_t)D0) & ~(uint64_t)15;
+    const uint64_t a1 = (outa + (uint64_t)(D0 + tot) - 1) & ~(uint64_t)15;
+    const int nchunks = (int)((a1 - a0) >> 4) + 1;
+    const int xbase = (int)((int64_t)(a0 - outa) - D0);     // -15..0
+    const int ngroups = (nchunks + 63) >> 6;
+    const int per = (ngroups + 3) >> 2;
+    const int g0 = min(wave * per, ngroups);
+    const int g1 = min(g0 + per, ngroups);
+    int r = 0;
+    for (int g = g0; g < g1; ++g) {
+        const int ch = g * 64 + lane;
+        if (ch >= nchunks) continue;
+        const int x = xbase + ch * 16;
+        const int lo = x > 0 ? x : 0;
+        const int hi = x + 16 < tot ? x + 16 : tot;
+        r = advance_record(s_dst, r, lo);
+        const int d1 = s_dst[r + 1];
+        const int e1 = hi < d1 ? hi : d1;
+        Piece p;
+        piece_load(p, s_src[r] + (uint64_t)(int64_t)(x - s_dst[r]), lo - x, e1 - 1 - x);
+        uint4 acc = make_uint4(0u, 0u, 0u, 0u);
+        if (e1 < hi) {
+            // the chunk also holds the start of the next record(s)
+            int q = advance_record(s_dst, r, e1);
+            int e = e1;
+            while (e < hi) {
+                const int dq = s_dst[q + 1];
+                const int e2 = hi < dq ? hi : dq;
+                Piece pq;
+                piece_load(pq, s_src[q] + (uint64_t)(int64_t)(x - s_dst[q]), e - x, e2 - 1 - x);
+                piece_merge(acc, pq);
+                e = e2;
+                if (e < hi) q = advance_record(s_dst, q, e);
+            }
+            r = q;
+        }
+        piece_merge(acc, p);
+        const uint64_t A = outa + (uint64_t)(D0 + x);
+        if (lo == x && hi == x + 16) st16(A, acc);
+        else store_partial(A, acc, lo - x, hi - x);     // first or last chunk of the window
+    }
+}
+
+// A sub-tile with an output window of 2 GiB or more (records of megabytes):
+// one wave per record, 64-bit positions, record edges written bytewise.
+__device__ __forceinline__ void copy_records64(const int64_t *s_dst, const uint64_t *s_src, uint64_t outa,
+                                            int64_t D0, int wave, int lane)
+{
+    for (int r = wave; r < kSub; r += kBlock / 64) {
+        const int64_t L = s_dst[r + 1] - s_dst[r];
+        if (L <= 0) continue;
+        const uint64_t D = outa + (uint64_t)(D0 + s_dst[r]);
+        const uint64_t a0 = D & ~(uint64_t)15, a1 = (D + (uint64_t)L - 1) & ~(uint64_t)15;
+        const int64_t nch = (int64_t)((a1 - a0) >> 4) + 1;
+        for (int64_t k = lane; k < nch; k += 64) {
+            const uint64_t A = a0 + ((uint64_t)k << 4);
+            const int64_t x = (int64_t)(A - D);               // chunk start, relative to the record
+            const int64_t lo = x > 0 ? x : 0;
+            const int64_t hi = min64(x + 16, L);
+            Piece p;
+            piece_load(p, s_src[r] + (uint64_t)x, (int)(lo - x), (int)(hi - 1 - x));
+            uint4 acc = make_uint4(0u, 0u, 0u, 0u);
+            piece_merge(acc, p);
+            if (lo == x && hi == x + 16) st16(A, acc);
+            else store_partial(A, acc, (int)(lo - x), (int)(hi - x));
+        }
+    }
+}
+
+#ifndef RO_COPY_WAVES
+#define RO_COPY_WAVES 6
+#endif
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_WAVES))) void k_gather_copy(
     const int64_t *__restrict__ offsets, int64_t P, const Canon *__restrict__ canon, int64_t canon_cap,
     const int64_t *__restrict__ sub_base, uint8_t *__restrict__ out, Ctl *ctl)
 {
     const uint32_t epoch = ctl->canon_epoch;
     __shared__ int64_t s_dst[kSub + 1];     // destination offset of each record, relative
+    __shared__ int32_t s_dst32[kSub + 1];   // the same, when the window is under 2 GiB
     __shared__ uint64_t s_src[kSub];
     __shared__ int64_t s_wave[kBlock / 64];
     if (read_err(ctl) != 0) return;          // any recorded error: copy nothing
@@ -293,6 +461,7 @@ __global__ __launch_bounds__(kBlock) void k_gather_copy(
     const int64_t N = N0 <= canon_cap ? N0 : 0;
     const int64_t nsub = (N + kSub - 1) / kSub;
     const uint64_t outa = reinterpret_cast<uint64_t>(out);
+    const int wave = (int)(threadIdx.x >> 6), lane = lane_id();
     for (int64_t sb = blockIdx.x; sb < nsub; sb += gridDim.x) {
         const int64_t c0 = sb * kSub;
         const int64_t cnt = min64(kSub, N - c0);
@@ -320,42 +489,19 @@ __global__ __launch_bounds__(kBlock) void k_gather_copy(
         for (int k = 0; k < kCopyPer; ++k) {
             const int r = threadIdx.x * kCopyPer + k;
             s_dst[r] = run;
+            s_dst32[r] = (int32_t)run;
             s_src[r] = s[k];
             run += l[k];
         }
-        if (threadIdx.x == 0) s_dst[kSub] = tot;
+        if (threadIdx.x == 0) {
+            s_dst[kSub] = tot;
+            s_dst32[kSub] = (int32_t)tot;
+        }
         __syncthreads();
         if (tot > 0) {
             const int64_t D0 = sub_base[sb];
-            const int64_t D1 = D0 + tot;
-            const uint64_t a0 = (outa + (uint64_t)D0) & ~(uint64_t)15;
-            const uint64_t a1 = (outa + (uint64_t)D1 - 1) & ~(uint64_t)15;
-            const int64_t nchunks = (int64_t)((a1 - a0) >> 4) + 1;
-            for (int64_t ch = threadIdx.x; ch < nchunks; ch += kBlock) {
-                const uint64_t A = a0 + ((uint64_t)ch << 4);
-                const int64_t x = (int64_t)(A - outa) - D0;      // chunk start, relative to D0
-                const int64_t lo = x > 0 ? x : 0;
-                const int64_t hi = min64(x + 16, tot);
-                // record holding byte lo: largest r with s_dst[r] <= lo
-                int rl = 0, rh = kSub + 1;
-                while (rh - rl > 1) {
-                    const int mid = (rl + rh) >> 1;
-                    if (s_dst[mid] <= lo) rl = mid; else rh = mid;
-                }
-                int r = rl;
-                if (lo == x && hi == x + 16 && x + 16 <= s_dst[r + 1]) {
-                    const uint4 v = load16_any(s_src[r] + (uint64_t)(x - s_dst[r]));
-                    *reinterpret_cast<uint4 *>(A) = v;
-                } else {
-                    // chunk straddles records or the window edge: byte by byte
-                    uint8_t *dst = reinterpret_cast<uint8_t *>(A);
-                    for (int64_t y = lo; y < hi; ++y) {
-                        while (y >= s_dst[r + 1]) ++r;
-                        const uint8_t *sp = reinterpret_cast<const uint8_t *>(s_src[r]);
-                        dst[y - x] = sp[y - s_dst[r]];
-                    }
-                }
-            }
+            if (tot < ((int64_t)1 << 31)) copy_window32(s_dst32, s_src, (int)tot, outa, D0, wave, lane);
+            else copy_records64(s_dst, s_src, outa, D0, wave, lane);
         }
         __syncthreads();
     }
@@ -364,24 +510,24 @@ __global__ __launch_bounds__(kBlock) void k_gather_copy(
 hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w)
 {
     const int64_t grid_r = (int64_t)L.num_cus * 8;
-    hipLaunchKernelGGL(k_gather_scatter, dim3((unsigned)grid_r), dim3(kBlock), 0, L.stream, a.rp, a.ro,
+    RO_LAUNCH(L, RO_K_GATHER_SCATTER, k_gather_scatter, dim3((unsigned)grid_r), dim3(kBlock), 0, L.stream, a.rp, a.ro,
                        a.rs, a.roff, a.data, a.n, a.offsets, a.P, w.canon, w.canon_cap, a.ns, a.nf,
                        a.nk, L.ctl);
     const int64_t grid_s = (int64_t)L.num_cus * 4;
-    hipLaunchKernelGGL(k_gather_scan, dim3((unsigned)grid_s), dim3(kBlock), 0, L.stream, a.offsets, a.P,
+    RO_LAUNCH(L, RO_K_GATHER_SCAN, k_gather_scan, dim3((unsigned)grid_s), dim3(kBlock), 0, L.stream, a.offsets, a.P,
                        w.canon, w.canon_cap, a.out_off, a.ns, a.nf, a.nk, w.sub_base, L.ctl, L.desc,
                        L.desc_cap);
     int64_t grid_f = (a.P + kBlock - 1) / kBlock;
     grid_f = grid_f < 1 ? 1 : (grid_f > (int64_t)L.num_cus * 8 ? (int64_t)L.num_cus * 8 : grid_f);
-    hipLaunchKernelGGL(k_gather_finalize, dim3((unsigned)grid_f), dim3(kBlock), 0, L.stream, a.offsets,
+    RO_LAUNCH(L, RO_K_GATHER_FINALIZE, k_gather_finalize, dim3((unsigned)grid_f), dim3(kBlock), 0, L.stream, a.offsets,
                        a.P, w.canon_cap, a.out_off, a.out_cap, a.out_data != nullptr ? 1 : 0, a.ns, a.nf,
                        a.nk, a.complete, a.pstate, L.ctl);
     if (a.out_data != nullptr) {
         const int64_t grid_c = (int64_t)L.num_cus * 8;
-        hipLaunchKernelGGL(k_gather_copy, dim3((unsigned)grid_c), dim3(kBlock), 0, L.stream, a.offsets,
+        RO_LAUNCH(L, RO_K_GATHER_COPY, k_gather_copy, dim3((unsigned)grid_c), dim3(kBlock), 0, L.stream, a.offsets,
                            a.P, w.canon, w.canon_cap, w.sub_base, a.out_data, L.ctl);
     }
-    hipLaunchKernelGGL(k_gather_reset, dim3(1), dim3(64), 0, L.stream, L.ctl);
+    RO_LAUNCH(L, RO_K_GATHER_RESET, k_gather_reset, dim3(1), dim3(64), 0, L.stream, L.ctl);
     return hipGetLastError();
 }
 

@@ -29,20 +29,20 @@ __global__ void k_reset_canon(Ctl *ctl, Canon *canon, int64_t n)
 
 hipError_t launch_ctl_init(const Launch &L)
 {
-    hipLaunchKernelGGL(k_ctl_init, dim3(1), dim3(64), 0, L.stream, L.ctl);
+    RO_LAUNCH(L, RO_K_MISC, k_ctl_init, dim3(1), dim3(64), 0, L.stream, L.ctl);
     return hipGetLastError();
 }
 
 hipError_t launch_reset_scan_epoch(const Launch &L)
 {
-    hipLaunchKernelGGL(k_reset_scan_epoch, dim3((unsigned)L.num_cus), dim3(256), 0, L.stream, L.ctl,
+    RO_LAUNCH(L, RO_K_MISC, k_reset_scan_epoch, dim3((unsigned)L.num_cus), dim3(256), 0, L.stream, L.ctl,
                        L.desc, L.desc_cap);
     return hipGetLastError();
 }
 
 hipError_t launch_reset_canon(const Launch &L, Canon *canon, int64_t n)
 {
-    hipLaunchKernelGGL(k_reset_canon, dim3((unsigned)L.num_cus * 4), dim3(256), 0, L.stream, L.ctl,
+    RO_LAUNCH(L, RO_K_MISC, k_reset_canon, dim3((unsigned)L.num_cus * 4), dim3(256), 0, L.stream, L.ctl,
                        canon, n);
     return hipGetLastError();
 }

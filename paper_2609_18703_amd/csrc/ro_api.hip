@@ -2,9 +2,55 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <vector>
+
 #include "ro_internal.h"
 
 using namespace ro;
+
+namespace ro {
+
+// Events bracketing every traced launch; recycled after each read.
+struct Tracer {
+    struct Rec {
+        int kind;
+        hipEvent_t e0, e1;
+    };
+    bool on = false;
+    std::vector<hipEvent_t> pool;   // all events ever created
+    size_t used = 0;                // events handed out since the last read
+    std::vector<Rec> recs;
+    hipEvent_t next_event()
+    {
+        if (used == pool.size()) {
+            hipEvent_t e = nullptr;
+            if (hipEventCreate(&e) != hipSuccess) return nullptr;
+            pool.push_back(e);
+        }
+        return pool[used++];
+    }
+};
+
+void trace_begin(const Launch &L, int kernel)
+{
+    Tracer *t = L.tracer;
+    if (!t || !t->on) return;
+    hipEvent_t e = t->next_event();
+    if (e && hipEventRecord(e, L.stream) != hipSuccess) e = nullptr;
+    t->recs.push_back({kernel, e, nullptr});
+}
+
+void trace_end(const Launch &L, int kernel)
+{
+    (void)kernel;
+    Tracer *t = L.tracer;
+    if (!t || !t->on || t->recs.empty()) return;
+    hipEvent_t e = t->next_event();
+    if (e && hipEventRecord(e, L.stream) != hipSuccess) e = nullptr;
+    t->recs.back().e1 = e;
+}
+
+}  // namespace ro
 
 struct ro_ctx {
     hipStream_t stream;
@@ -20,8 +66,8 @@ struct ro_ctx {
     int64_t *samples;
     int32_t *cnt;             // [3 * cnt_cap] counters used when the caller passes none
     int64_t cnt_cap;
-    int64_t scan_launches;    // host shadow of the device scan epoch
     int64_t gathers;          // host shadow of the device canonical epoch
+    Tracer *tracer;
 };
 
 struct ro_stream {
@@ -42,6 +88,7 @@ Launch launch_of(ro_ctx *c)
     L.ctl = c->ctl;
     L.desc = c->desc;
     L.desc_cap = c->desc_cap;
+    L.tracer = c->tracer;
     return L;
 }
 
@@ -102,18 +149,6 @@ int ensure_cnt(ro_ctx *c, int64_t parents)
     return RO_OK;
 }
 
-// Called before every ticketed launch: if the 16-bit descriptor epoch is about
-// to wrap, clear the descriptors and restart the epoch at 1 first.
-int before_scan(ro_ctx *c, int launches)
-{
-    if (c->scan_launches + launches > (int64_t)kMaxScanEpoch) {
-        if (launch_reset_scan_epoch(launch_of(c)) != hipSuccess) return RO_EHIP;
-        c->scan_launches = 1;
-    }
-    c->scan_launches += launches;
-    return RO_OK;
-}
-
 int before_gather(ro_ctx *c)
 {
     if (c->gathers + 1 > (int64_t)kMaxCanonEpoch) {
@@ -134,6 +169,7 @@ int ro_ctx_create(ro_ctx **out, void *hip_stream)
     *out = nullptr;
     ro_ctx *c = (ro_ctx *)calloc(1, sizeof(ro_ctx));
     if (!c) return RO_EINVAL;
+    c->tracer = new Tracer();
     c->stream = (hipStream_t)hip_stream;
     if (hipGetDevice(&c->device) != hipSuccess ||
         hipDeviceGetAttribute(&c->num_cus, hipDeviceAttributeMultiprocessorCount, c->device) != hipSuccess ||
@@ -148,7 +184,6 @@ int ro_ctx_create(ro_ctx **out, void *hip_stream)
         ro_ctx_destroy(c);
         return RO_EHIP;
     }
-    c->scan_launches = 1;     // device scan epoch starts at 1
     c->gathers = 1;           // device canonical epoch starts at 1
     *out = c;
     return RO_OK;
@@ -198,7 +233,35 @@ int ro_ctx_destroy(ro_ctx *c)
     (void)hipFree(c->sub_base);
     (void)hipFree(c->samples);
     (void)hipFree(c->cnt);
+    if (c->tracer) {
+        for (hipEvent_t e : c->tracer->pool) (void)hipEventDestroy(e);
+        delete c->tracer;
+    }
     free(c);
+    return RO_OK;
+}
+
+int ro_ctx_trace(ro_ctx *c, int enable)
+{
+    if (!c || !c->tracer) return RO_EINVAL;
+    c->tracer->on = enable != 0;
+    return RO_OK;
+}
+
+int ro_ctx_trace_read(ro_ctx *c, int64_t *launches, double *total_ms, int32_t n)
+{
+    if (!c || !c->tracer || n < 0 || (n > 0 && (!launches || !total_ms))) return RO_EINVAL;
+    Tracer *t = c->tracer;
+    if (hipStreamSynchronize(c->stream) != hipSuccess) return RO_EHIP;
+    for (const Tracer::Rec &r : t->recs) {
+        if (r.kind < 0 || r.kind >= n || !r.e0 || !r.e1) continue;
+        float ms = 0.f;
+        if (hipEventElapsedTime(&ms, r.e0, r.e1) != hipSuccess) continue;
+        launches[r.kind] += 1;
+        total_ms[r.kind] += (double)ms;
+    }
+    t->recs.clear();
+    t->used = 0;
     return RO_OK;
 }
 
@@ -208,7 +271,6 @@ int ro_expand(ro_ctx *c, const int32_t *counts, int64_t n_parents, int64_t *offs
     if (!c || !offsets || n_parents < 0 || child_cap < 0 || (n_parents > 0 && !counts)) return RO_EINVAL;
     int rc = ensure_desc(c, tiles_for(n_parents));
     if (rc) return rc;
-    if ((rc = before_scan(c, 1))) return rc;
     return hip_fail(launch_expand(launch_of(c), counts, n_parents, offsets, child_parent, child_ordinal,
                                   child_cap));
 }
@@ -223,7 +285,6 @@ int ro_batch(ro_ctx *c, const uint32_t *queue, const uint8_t *keep, int64_t q_le
         return RO_EINVAL;
     int rc = ensure_desc(c, tiles_for(q_len));
     if (rc) return rc;
-    if ((rc = before_scan(c, 1))) return rc;
     return hip_fail(launch_batch(launch_of(c), queue, keep, q_len, offsets, n_parents, batch_size,
                                  out_child, out_parent, out_ordinal, out_cap, n_out_dev, n_batches_dev,
                                  c->samples));
@@ -270,7 +331,6 @@ int ro_gather(ro_ctx *c, const ro_reports *r, const int64_t *offsets, int64_t n_
     w.canon_cap = c->canon_cap;
     w.sub_base = c->sub_base;
     w.sub_cap = c->sub_cap;
-    if ((rc = before_scan(c, 1))) return rc;
     if ((rc = before_gather(c))) return rc;
     return hip_fail(launch_gather(launch_of(c), a, w));
 }

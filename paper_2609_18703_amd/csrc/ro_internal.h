@@ -41,13 +41,27 @@ struct Ctl {
     int64_t pad[8];
 };
 
+struct Tracer;
+
 struct Launch {
     hipStream_t stream;
     int num_cus;
     Ctl *ctl;
     uint64_t *desc;          // look-back descriptors
     int64_t desc_cap;        // tiles
+    Tracer *tracer;          // per-kernel events, or null
 };
+
+// Bracket one kernel launch with trace events when tracing is on.
+void trace_begin(const Launch &L, int kernel);
+void trace_end(const Launch &L, int kernel);
+
+#define RO_LAUNCH(L, kid, ...)               \
+    do {                                     \
+        ::ro::trace_begin((L), (kid));       \
+        hipLaunchKernelGGL(__VA_ARGS__);     \
+        ::ro::trace_end((L), (kid));         \
+    } while (0)
 
 constexpr uint32_t kMaxScanEpoch = 65535;
 constexpr uint32_t kMaxCanonEpoch = (1u << 30) - 1;

@@ -10,11 +10,16 @@ from __future__ import annotations
 import ctypes as C
 import os
 
-__all__ = ["RoError", "load", "Context", "Stream", "OK", "EINVAL", "ERANGE", "EDUP", "ECAP",
+__all__ = ["RoError", "load", "Context", "Stream", "KERNELS", "OK", "EINVAL", "ERANGE", "EDUP", "ECAP",
            "EOVERFLOW", "ESTATE", "EHIP", "SUCCESS", "FAILED", "SKIPPED", "PENDING", "LIB_PATH"]
 
 OK, EINVAL, ERANGE, EDUP, ECAP, EOVERFLOW, ESTATE, EHIP = 0, -1, -2, -3, -4, -5, -6, -7
 SUCCESS, FAILED, SKIPPED, PENDING = 0, 1, 2, 3
+
+# kernel kinds reported by Context.trace_read, in the C enum's order
+KERNELS = ["expand_scan", "expand_tags", "batch_samples", "batch", "gather_scatter", "gather_scan",
+           "gather_finalize", "gather_copy", "gather_reset", "stream_report", "stream_select",
+           "stream_scan", "stream_copy", "stream_finish", "misc"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libro.so")
 
@@ -62,7 +67,9 @@ def load(path=None):
     L.ro_stream_report.argtypes = [P, P, C.POINTER(ReportsT)]
     L.ro_stream_emit.argtypes = [P, P, P, P, P, i64, i64, P, P, P, P, P, P]
     L.ro_stream_destroy.argtypes = [P]
-    for name in ("ro_ctx_create", "ro_ctx_set_stream", "ro_ctx_reserve", "ro_ctx_status",
+    L.ro_ctx_trace.argtypes = [P, C.c_int]
+    L.ro_ctx_trace_read.argtypes = [P, P, P, i32]
+    for name in ("ro_ctx_trace", "ro_ctx_trace_read", "ro_ctx_create", "ro_ctx_set_stream", "ro_ctx_reserve", "ro_ctx_status",
                  "ro_ctx_destroy", "ro_expand", "ro_batch", "ro_gather", "ro_stream_create",
                  "ro_stream_report", "ro_stream_emit", "ro_stream_destroy"):
         getattr(L, name).restype = C.c_int
@@ -113,6 +120,19 @@ class Context:
 
     def check(self, what="device"):
         _check(self.status(), what)
+
+    def trace(self, enable=True):
+        """Bracket every kernel this context launches with HIP events."""
+        _check(self.L.ro_ctx_trace(self.h, 1 if enable else 0), "ro_ctx_trace")
+
+    def trace_read(self):
+        """{kernel: (launches, total_ms)} since the last read (waits for the stream)."""
+        n = len(KERNELS)
+        launches = (C.c_int64 * n)()
+        ms = (C.c_double * n)()
+        _check(self.L.ro_ctx_trace_read(self.h, C.cast(launches, C.c_void_p), C.cast(ms, C.c_void_p), n),
+               "ro_ctx_trace_read")
+        return {k: (int(launches[i]), float(ms[i])) for i, k in enumerate(KERNELS) if launches[i]}
 
     def expand(self, counts, offsets, child_parent=None, child_ordinal=None):
         cap = 0

@@ -66,20 +66,30 @@ def record_bytes(seeds, lengths, chunk_words=1 << 22):
     nw = (lengths + 7) // 8
     r0, pos = 0, 0
     n = len(lengths)
+    cum_all = np.cumsum(nw)
     while r0 < n:
         # records [r0, r1) hold at most ~chunk_words words (at least one record)
-        cum = np.cumsum(nw[r0:])
-        r1 = r0 + max(1, int(np.searchsorted(cum, chunk_words, side="right")))
+        base = int(cum_all[r0 - 1]) if r0 else 0
+        r1 = r0 + max(1, int(np.searchsorted(cum_all[r0:] - base, chunk_words, side="right")))
         w = nw[r0:r1]
         W = int(w.sum())
         if W:
-            rec = np.repeat(np.arange(r0, r1), w)
             first = np.cumsum(w) - w
             k = np.arange(W, dtype=np.int64) - np.repeat(first, w)
-            words = splitmix64_words(seeds[rec], k).astype("<u8")
-            b = words.view(np.uint8).reshape(W, 8)
-            keep = (k[:, None] * 8 + np.arange(8)[None, :]) < lengths[rec][:, None]
-            seg = b[keep]
+            words = splitmix64_words(np.repeat(seeds[r0:r1], w), k).astype("<u8")
+            b = words.view(np.uint8)
+            # drop the 0..7 bytes past each record's length in its last word
+            pad = 8 * w - lengths[r0:r1]
+            npad = int(pad.sum())
+            if npad:
+                wend = np.cumsum(w)
+                rp = np.repeat(np.arange(r1 - r0), pad)
+                t = np.arange(npad, dtype=np.int64) - np.repeat(np.cumsum(pad) - pad, pad)
+                keep = np.ones(b.size, dtype=bool)
+                keep[8 * wend[rp] - pad[rp] + t] = False
+                seg = b[keep]
+            else:
+                seg = b
             out[pos:pos + seg.size] = seg
             pos += seg.size
         r0 = r1

@@ -3,8 +3,8 @@
 
 One step = the whole path over one batch of the synthetic workload: ro_expand
 (counts -> offsets and lineage keys), ro_batch over the ready queue for the
-dispatched children, ro_batch over the same queue for the children sealed
-before dispatch, and ro_gather of all reports into parent slots.  Inputs
+dispatched children, ro_batch over the list of children sealed before
+dispatch, and ro_gather of all reports into parent slots.  Inputs
 (counts, ready queue, masks, report states, report offsets and record bytes)
 are resident in HBM before the timed region; record bytes are generated
 untimed by the generator's device fill.
@@ -95,7 +95,7 @@ def main():
     data = torch.empty(max(S, 1), dtype=torch.uint8, device="cuda")
     D.fill_records_dev(D.to_dev(r.seed), D.to_dev(r.off), data)
     b = PL.SingleLevelBuffers(
-        D.to_dev(c.counts), D.to_dev(c.queue.view(np.int32)), D.to_dev(c.keep), D.to_dev(c.sealed),
+        D.to_dev(c.counts), D.to_dev(c.queue.view(np.int32)), D.to_dev(c.keep), D.to_dev(c.sealed_ids.view(np.int32)),
         D.to_dev(r.state), D.to_dev(r.off), data, N, M, c.batch_size, out_cap=S)
     torch.cuda.synchronize()
     log(f"[bench] staged in HBM ({time.time() - t0:.1f}s)")
@@ -134,8 +134,9 @@ def main():
     total_alg = 0
     for k, (n_launch, ms) in kern.items():
         if k == "batch":
-            # two launches per step: dispatched (M tags out) and sealed (N-M tags out)
-            per_step = 5 * N * 2 + 8 * N
+            # two launches per step: the ready queue (N entries in, M tags out) and
+            # the sealed list (N-M entries in, N-M tags out)
+            per_step = 5 * N + 4 * (N - M) + 8 * N
             ab = per_step / 2
         else:
             ab = alg_bytes(k, P, N, M, S)
@@ -221,7 +222,7 @@ def cpu_baseline(n_parents):
     t = time.perf_counter()
     offs, cp, co = O.expand(c.counts, L=L)
     b1 = O.batch(c.queue, c.keep, offs, c.batch_size, L=L)
-    b2 = O.batch(c.queue, c.sealed, offs, c.batch_size, L=L)
+    b2 = O.batch(c.sealed_ids, None, offs, c.batch_size, L=L)
     par = np.concatenate([b1[1], b2[1]])
     ordi = np.concatenate([b1[2], b2[2]])
     g = O.gather(par, ordi, r.state, r.off, data, offs, L=L)

@@ -5,56 +5,55 @@
 // most B entries from the head and may mix parents.  Taking the reservations
 // one after another until the queue is empty is a stable compaction of the
 // ready entries cut into consecutive chunks of B, which is what this kernel
-// computes in one pass: ballot ranks inside a wave, a workgroup scan, and a
-// decoupled look-back across tiles keep every ready entry in queue order.
+// computes in one pass: a workgroup scan of the ready flags and a decoupled
+// look-back across tiles give every ready entry its FIFO slot.
 #include "ro_device.h"
 
 namespace ro {
 
-// Samples of the offsets array: samp[j] = offsets[min(j << shift, P)].
-__global__ void k_batch_samples(const int64_t *__restrict__ offsets, int64_t P, int shift,
-                                int64_t nsamp, int64_t *__restrict__ samp)
+// Coarse child -> parent map: cmap[j] = parent of child j << kCmapShift.  A
+// child's parent then lies between cmap[j] and cmap[j+1], a handful of
+// offsets that sit in L2.
+constexpr int kCmapShift = 6;
+
+__global__ void k_batch_cmap(const int64_t *__restrict__ offsets, int64_t P, uint32_t *__restrict__ cmap,
+                             int64_t cmap_cap)
 {
-    const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (j < nsamp) {
-        const int64_t i = j << shift;
-        samp[j] = offsets[i < P ? i : P];
-    }
+    const int64_t N = offsets[P];
+    int64_t nmap = (N + (1 << kCmapShift) - 1) >> kCmapShift;
+    nmap = nmap < cmap_cap ? nmap : cmap_cap;
+    for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < nmap;
+         j += (int64_t)gridDim.x * blockDim.x)
+        cmap[j] = (uint32_t)(upper_bound_g(offsets, 0, P + 1, j << kCmapShift) - 1);
 }
 
-// Parent of child c: the LDS samples narrow the search to 2^shift offsets,
-// a short global binary search finishes it.
-__device__ __forceinline__ int64_t find_parent(const int64_t *s_samp, int64_t nsamp, int shift,
-                                               const int64_t *offsets, int64_t P, int64_t c)
+// Parent of child c < N.
+__device__ __forceinline__ int64_t parent_of(const uint32_t *__restrict__ cmap, int64_t nmap,
+                                             const int64_t *__restrict__ offsets, int64_t P, int64_t c)
 {
-    int64_t lo = 0, hi = nsamp;
-    while (lo < hi) {
-        int64_t mid = (lo + hi) >> 1;
-        if (s_samp[mid] <= c) lo = mid + 1; else hi = mid;
-    }
-    const int64_t j = lo - 1;                    // s_samp[0] = 0 <= c
-    const int64_t b = j << shift;
-    int64_t e = b + ((int64_t)1 << shift);
-    e = e < P + 1 ? e : P + 1;
-    return upper_bound_g(offsets, b, e, c) - 1;
+    const int64_t j = c >> kCmapShift;
+    if (j >= nmap) return upper_bound_g(offsets, 0, P + 1, c) - 1;
+    const int64_t lo = cmap[j];
+    const int64_t hi = j + 1 < nmap ? (int64_t)cmap[j + 1] : P - 1;
+    return upper_bound_g(offsets, lo, hi + 1, c) - 1;
 }
 
 __global__ __launch_bounds__(kBlock) void k_batch(
     const uint32_t *__restrict__ queue, const uint8_t *__restrict__ keep, int64_t Q,
-    const int64_t *__restrict__ offsets, int64_t P, const int64_t *__restrict__ samp, int64_t nsamp,
-    int shift, int32_t B, uint32_t *__restrict__ out_child, uint32_t *__restrict__ out_parent,
+    const int64_t *__restrict__ offsets, int64_t P, const uint32_t *__restrict__ cmap, int64_t cmap_cap,
+    int32_t B, uint32_t *__restrict__ out_child, uint32_t *__restrict__ out_parent,
     uint32_t *__restrict__ out_ordinal, int64_t out_cap, int64_t *n_out, int64_t *n_batches,
     Ctl *ctl, uint64_t *desc, int64_t desc_cap, int64_t ntiles, int vec_ok)
 {
     const uint32_t epoch = scan_epoch(ctl);
-    __shared__ int64_t s_samp[kMaxSamples];
+    __shared__ uint32_t s_out[kTile];          // one output array of a tile, in slot order
     __shared__ int64_t s_wave[kBlock / 64];
     __shared__ uint64_t s_b;
     __shared__ int64_t s_t;
     __shared__ int32_t s_last;
-    for (int64_t j = threadIdx.x; j < nsamp; j += kBlock) s_samp[j] = samp[j];
-    __syncthreads();
     const int64_t N = offsets[P];
+    int64_t nmap = (N + (1 << kCmapShift) - 1) >> kCmapShift;
+    nmap = nmap < cmap_cap ? nmap : cmap_cap;
     const bool want_tags = out_parent != nullptr || out_ordinal != nullptr;
     for (;;) {
         const int64_t t = next_ticket(ctl, &s_t);
@@ -89,35 +88,50 @@ __global__ __launch_bounds__(kBlock) void k_batch(
                 }
             }
         }
-        const int64_t cnt = __popc(kmask);
+        // lineage tags of the ready entries (independent lookups, all in flight)
+        uint32_t par[kItems], ord[kItems];
+        bool bad_range = false;
+#pragma unroll
+        for (int k = 0; k < kItems; ++k) {
+            par[k] = 0xffffffffu;
+            ord[k] = 0xffffffffu;
+            if (kmask & (1u << k)) {
+                const int64_t c = q[k];
+                if (c >= N) {
+                    bad_range = true;
+                } else if (want_tags) {
+                    const int64_t p = parent_of(cmap, nmap, offsets, P, c);
+                    par[k] = (uint32_t)p;
+                    ord[k] = (uint32_t)(c - offsets[p]);
+                }
+            }
+        }
+        if (bad_range) raise_err(ctl, RO_ERANGE);
+        const int cnt = __popc(kmask);
         int64_t tot;
         const int64_t ex = block_excl_scan(cnt, s_wave, tot);
         const uint64_t pre = tile_prefix(desc, t, epoch, (uint64_t)tot, &s_b, ctl);
-        int64_t slot = (int64_t)pre + ex;
-        bool bad_range = false, bad_cap = false;
+        const int64_t base = (int64_t)pre;
+        if (base + tot > out_cap && threadIdx.x == 0) raise_err(ctl, RO_ECAP);
+        const int64_t lim = out_cap - base < tot ? (out_cap - base > 0 ? out_cap - base : 0) : tot;
+        // stage each requested output array in LDS in slot order, then write
+        // the tile's contiguous slot range with coalesced stores
+#pragma unroll 1
+        for (int which = 0; which < 3; ++which) {
+            uint32_t *dst = which == 0 ? out_child : (which == 1 ? out_parent : out_ordinal);
+            if (dst == nullptr) continue;
+            int slot = (int)ex;
 #pragma unroll
-        for (int k = 0; k < kItems; ++k) {
-            if (!(kmask & (1u << k))) continue;
-            const int64_t c = q[k];
-            uint32_t p = 0xffffffffu, o = 0xffffffffu;
-            if (c >= N) {
-                bad_range = true;
-            } else if (want_tags) {
-                const int64_t pp = find_parent(s_samp, nsamp, shift, offsets, P, c);
-                p = (uint32_t)pp;
-                o = (uint32_t)(c - offsets[pp]);
+            for (int k = 0; k < kItems; ++k) {
+                if (kmask & (1u << k)) {
+                    s_out[slot] = which == 0 ? q[k] : (which == 1 ? par[k] : ord[k]);
+                    ++slot;
+                }
             }
-            if (slot < out_cap) {
-                if (out_child) out_child[slot] = (uint32_t)c;
-                if (out_parent) out_parent[slot] = p;
-                if (out_ordinal) out_ordinal[slot] = o;
-            } else {
-                bad_cap = true;
-            }
-            ++slot;
+            __syncthreads();
+            for (int64_t j = threadIdx.x; j < lim; j += kBlock) dst[base + j] = s_out[j];
+            __syncthreads();
         }
-        if (bad_range) raise_err(ctl, RO_ERANGE);
-        if (bad_cap) raise_err(ctl, RO_ECAP);
         if (t == ntiles - 1 && threadIdx.x == 0) {
             const int64_t m = (int64_t)pre + tot;
             if (n_out) *n_out = m;
@@ -130,20 +144,21 @@ __global__ __launch_bounds__(kBlock) void k_batch(
 hipError_t launch_batch(const Launch &L, const uint32_t *queue, const uint8_t *keep,
                         int64_t Q, const int64_t *offsets, int64_t P, int32_t B,
                         uint32_t *out_child, uint32_t *out_parent, uint32_t *out_ordinal,
-                        int64_t out_cap, int64_t *n_out, int64_t *n_batches, int64_t *samples)
+                        int64_t out_cap, int64_t *n_out, int64_t *n_batches, uint32_t *cmap,
+                        int64_t cmap_cap)
 {
-    int shift = 0;
-    while ((((P + 1) + ((int64_t)1 << shift) - 1) >> shift) > kMaxSamples) ++shift;
-    const int64_t nsamp = ((P + 1) + ((int64_t)1 << shift) - 1) >> shift;
-    RO_LAUNCH(L, RO_K_BATCH_SAMPLES, k_batch_samples, dim3((unsigned)((nsamp + 255) / 256)), dim3(256), 0, L.stream,
-                       offsets, P, shift, nsamp, samples);
+    if (out_parent != nullptr || out_ordinal != nullptr) {
+        const int64_t grid_m = (int64_t)L.num_cus * 4;
+        RO_LAUNCH(L, RO_K_BATCH_SAMPLES, k_batch_cmap, dim3((unsigned)grid_m), dim3(256), 0, L.stream,
+                  offsets, P, cmap, cmap_cap);
+    }
     const int64_t ntiles = Q > 0 ? (Q + kTile - 1) / kTile : 1;
     const int64_t cap_grid = (int64_t)L.num_cus * 4;
     const int64_t grid = ntiles < cap_grid ? ntiles : cap_grid;
     const bool aligned = ((reinterpret_cast<uintptr_t>(queue) | reinterpret_cast<uintptr_t>(keep)) & 15u) == 0;
-    RO_LAUNCH(L, RO_K_BATCH, k_batch, dim3((unsigned)grid), dim3(kBlock), 0, L.stream, queue, keep, Q, offsets,
-                       P, samples, nsamp, shift, B, out_child, out_parent, out_ordinal, out_cap, n_out,
-                       n_batches, L.ctl, L.desc, L.desc_cap, ntiles, aligned ? 1 : 0);
+    RO_LAUNCH(L, RO_K_BATCH, k_batch, dim3((unsigned)grid), dim3(kBlock), 0, L.stream, queue, keep, Q,
+              offsets, P, cmap, cmap_cap, B, out_child, out_parent, out_ordinal, out_cap, n_out, n_batches,
+              L.ctl, L.desc, L.desc_cap, ntiles, aligned ? 1 : 0);
     return hipGetLastError();
 }
 

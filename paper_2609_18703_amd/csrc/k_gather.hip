@@ -144,9 +144,9 @@ __global__ __launch_bounds__(kBlock) void k_gather_scan(
         const int64_t ex = block_excl_scan(sum, s_wave, tot);
         const uint64_t pre = tile_prefix(desc, t, sepoch, (uint64_t)tot, &s_b, ctl);
         const int64_t base = (int64_t)pre + ex;
-        if ((threadIdx.x & 63) == 0) {
-            const int64_t sb = t * (kTile / kSub) + (threadIdx.x >> 6);
-            sub_base[sb] = base;                    // lane 0 of each wave starts a sub-tile
+        if ((threadIdx.x % (kSub / kItems)) == 0) {
+            const int64_t sb = t * (kTile / kSub) + threadIdx.x / (kSub / kItems);
+            sub_base[sb] = base;                    // first byte of each copy sub-tile
         }
 
         // pass 2: parents -- slot offsets and run-length counts
@@ -340,7 +340,7 @@ __device__ __forceinline__ uint32_t dword_of(const uint4 &v, int j)
     return j == 0 ? v.x : (j == 1 ? v.y : (j == 2 ? v.z : v.w));
 }
 
-constexpr int kCopyPer = kSub / kBlock;   // 4 children per thread in the copy prologue
+constexpr int kCopyPer = kSub / 64;       // records per lane in a wave's copy prologue
 
 // Largest r in [r, kSub] with s_dst[r] <= pos, given s_dst[r] <= pos: a few
 // linear steps (the usual distance between neighbouring chunks), then a
@@ -367,26 +367,20 @@ __device__ __forceinline__ void store_partial(uint64_t A, const uint4 &v, int b0
 }
 
 // A sub-tile whose output window is under 2 GiB: positions relative to the
-// window start fit in 32 bits.  Each wave owns a contiguous run of 64-chunk
-// groups and lane `lane` takes chunk 64*g + lane of every group g, so the
-// record it reads from only moves forward.  Every chunk strictly inside the
-// window is written with one aligned 16-byte store; chunks that straddle
-// records are assembled from their pieces first.
+// window start fit in 32 bits.  The wave sweeps its window 1 KiB at a time,
+// lane `lane` taking chunk 64*g + lane, so the record each lane reads from
+// only moves forward.  Every chunk strictly inside the window is written with
+// one aligned 16-byte store; chunks that straddle records are assembled from
+// their pieces first, with all of their loads in flight together.
 __device__ __forceinline__ void copy_window32(const int32_t *s_dst, const uint64_t *s_src, int tot,
-                                              uint64_t outa, int64_t D0, int wave, int lane)
+                                              uint64_t outa, int64_t D0, int lane)
 {
     const uint64_t a0 = (outa + (uint64_t)D0) & ~(uint64_t)15;
     const uint64_t a1 = (outa + (uint64_t)(D0 + tot) - 1) & ~(uint64_t)15;
     const int nchunks = (int)((a1 - a0) >> 4) + 1;
     const int xbase = (int)((int64_t)(a0 - outa) - D0);     // -15..0
-    const int ngroups = (nchunks + 63) >> 6;
-    const int per = (ngroups + 3) >> 2;
-    const int g0 = min(wave * per, ngroups);
-    const int g1 = min(g0 + per, ngroups);
     int r = 0;
-    for (int g = g0; g < g1; ++g) {
-        const int ch = g * 64 + lane;
-        if (ch >= nchunks) continue;
+    for (int ch = lane; ch < nchunks; ch += 64) {
         const int x = xbase + ch * 16;
         const int lo = x > 0 ? x : 0;
         const int hi = x + 16 < tot ? x + 16 : tot;
@@ -419,11 +413,11 @@ __device__ __forceinline__ void copy_window32(const int32_t *s_dst, const uint64
 }
 
 // A sub-tile with an output window of 2 GiB or more (records of megabytes):
-// one wave per record, 64-bit positions, record edges written bytewise.
+// one record at a time across the wave, 64-bit positions, edges bytewise.
 __device__ __forceinline__ void copy_records64(const int64_t *s_dst, const uint64_t *s_src, uint64_t outa,
-                                            int64_t D0, int wave, int lane)
+                                               int64_t D0, int lane)
 {
-    for (int r = wave; r < kSub; r += kBlock / 64) {
+    for (int r = 0; r < kSub; ++r) {
         const int64_t L = s_dst[r + 1] - s_dst[r];
         if (L <= 0) continue;
         const uint64_t D = outa + (uint64_t)(D0 + s_dst[r]);
@@ -444,25 +438,32 @@ __device__ __forceinline__ void copy_records64(const int64_t *s_dst, const uint6
     }
 }
 
+// Each wave works alone on one sub-tile of kSub canonical children at a time:
+// it rebuilds the sub-tile's destination offsets with a wave scan into its own
+// LDS slice, then writes the sub-tile's contiguous output window.  No
+// workgroup barrier is involved, so waves never wait for one another.
 #ifndef RO_COPY_WAVES
-#define RO_COPY_WAVES 6
+#define RO_COPY_WAVES 4
 #endif
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_WAVES))) void k_gather_copy(
     const int64_t *__restrict__ offsets, int64_t P, const Canon *__restrict__ canon, int64_t canon_cap,
     const int64_t *__restrict__ sub_base, uint8_t *__restrict__ out, Ctl *ctl)
 {
+    constexpr int kWaves = kBlock / 64;
     const uint32_t epoch = ctl->canon_epoch;
-    __shared__ int64_t s_dst[kSub + 1];     // destination offset of each record, relative
-    __shared__ int32_t s_dst32[kSub + 1];   // the same, when the window is under 2 GiB
-    __shared__ uint64_t s_src[kSub];
-    __shared__ int64_t s_wave[kBlock / 64];
-    if (read_err(ctl) != 0) return;          // any recorded error: copy nothing
+    __shared__ int64_t s_dst_all[kWaves][kSub + 1];     // destination offset of each record, relative
+    __shared__ int32_t s_dst32_all[kWaves][kSub + 1];   // the same, when the window is under 2 GiB
+    __shared__ uint64_t s_src_all[kWaves][kSub];
+    if (read_err(ctl) != 0) return;                      // any recorded error: copy nothing
     const int64_t N0 = offsets[P];
     const int64_t N = N0 <= canon_cap ? N0 : 0;
     const int64_t nsub = (N + kSub - 1) / kSub;
     const uint64_t outa = reinterpret_cast<uint64_t>(out);
     const int wave = (int)(threadIdx.x >> 6), lane = lane_id();
-    for (int64_t sb = blockIdx.x; sb < nsub; sb += gridDim.x) {
+    int64_t *s_dst = s_dst_all[wave];
+    int32_t *s_dst32 = s_dst32_all[wave];
+    uint64_t *s_src = s_src_all[wave];
+    for (int64_t sb = (int64_t)blockIdx.x * kWaves + wave; sb < nsub; sb += (int64_t)gridDim.x * kWaves) {
         const int64_t c0 = sb * kSub;
         const int64_t cnt = min64(kSub, N - c0);
         // prologue: surviving lengths -> relative destination offsets
@@ -471,7 +472,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_
         uint64_t s[kCopyPer];
 #pragma unroll
         for (int k = 0; k < kCopyPer; ++k) {
-            const int64_t r = (int64_t)threadIdx.x * kCopyPer + k;
+            const int64_t r = (int64_t)lane * kCopyPer + k;
             l[k] = 0;
             s[k] = 0;
             if (r < cnt) {
@@ -483,36 +484,37 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_
             }
             lsum += l[k];
         }
-        int64_t tot;
-        int64_t run = block_excl_scan(lsum, s_wave, tot);
+        const int64_t inc = wave_incl_sum(lsum);
+        const int64_t tot = __shfl(inc, 63, 64);
+        int64_t run = inc - lsum;
 #pragma unroll
         for (int k = 0; k < kCopyPer; ++k) {
-            const int r = threadIdx.x * kCopyPer + k;
+            const int r = lane * kCopyPer + k;
             s_dst[r] = run;
             s_dst32[r] = (int32_t)run;
             s_src[r] = s[k];
             run += l[k];
         }
-        if (threadIdx.x == 0) {
+        if (lane == 0) {
             s_dst[kSub] = tot;
             s_dst32[kSub] = (int32_t)tot;
         }
-        __syncthreads();
+        __builtin_amdgcn_wave_barrier();
         if (tot > 0) {
             const int64_t D0 = sub_base[sb];
-            if (tot < ((int64_t)1 << 31)) copy_window32(s_dst32, s_src, (int)tot, outa, D0, wave, lane);
-            else copy_records64(s_dst, s_src, outa, D0, wave, lane);
+            if (tot < ((int64_t)1 << 31)) copy_window32(s_dst32, s_src, (int)tot, outa, D0, lane);
+            else copy_records64(s_dst, s_src, outa, D0, lane);
         }
-        __syncthreads();
+        __builtin_amdgcn_wave_barrier();
     }
 }
 
 hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w)
 {
     const int64_t grid_r = (int64_t)L.num_cus * 8;
-    RO_LAUNCH(L, RO_K_GATHER_SCATTER, k_gather_scatter, dim3((unsigned)grid_r), dim3(kBlock), 0, L.stream, a.rp, a.ro,
-                       a.rs, a.roff, a.data, a.n, a.offsets, a.P, w.canon, w.canon_cap, a.ns, a.nf,
-                       a.nk, L.ctl);
+    RO_LAUNCH(L, RO_K_GATHER_SCATTER, k_gather_scatter, dim3((unsigned)grid_r), dim3(kBlock), 0, L.stream,
+              a.rp, a.ro, a.rs, a.roff, a.data, a.n, a.offsets, a.P, w.canon, w.canon_cap, a.ns, a.nf,
+              a.nk, L.ctl);
     const int64_t grid_s = (int64_t)L.num_cus * 4;
     RO_LAUNCH(L, RO_K_GATHER_SCAN, k_gather_scan, dim3((unsigned)grid_s), dim3(kBlock), 0, L.stream, a.offsets, a.P,
                        w.canon, w.canon_cap, a.out_off, a.ns, a.nf, a.nk, w.sub_base, L.ctl, L.desc,

@@ -63,7 +63,8 @@ struct ro_ctx {
     int64_t canon_cap;
     int64_t *sub_base;
     int64_t sub_cap;
-    int64_t *samples;
+    uint32_t *cmap;           // coarse child -> parent map used by ro_batch
+    int64_t cmap_cap;
     int32_t *cnt;             // [3 * cnt_cap] counters used when the caller passes none
     int64_t cnt_cap;
     int64_t gathers;          // host shadow of the device canonical epoch
@@ -122,17 +123,23 @@ int ensure_canon(ro_ctx *c, int64_t children)
     if (hipStreamSynchronize(c->stream) != hipSuccess) return RO_EHIP;
     (void)hipFree(c->canon);
     (void)hipFree(c->sub_base);
+    (void)hipFree(c->cmap);
     c->canon = nullptr;
     c->sub_base = nullptr;
+    c->cmap = nullptr;
     c->canon_cap = 0;
     c->sub_cap = 0;
+    c->cmap_cap = 0;
     const int64_t n = children > 0 ? children : 1;
     if (dev_alloc(&c->canon, n) != hipSuccess) return RO_EHIP;
     if (hipMemset(c->canon, 0, (size_t)n * sizeof(Canon)) != hipSuccess) return RO_EHIP;
     const int64_t subs = (n / kTile + 2) * (kTile / kSub);
     if (dev_alloc(&c->sub_base, subs) != hipSuccess) return RO_EHIP;
+    const int64_t maps = (n >> 6) + 2;
+    if (dev_alloc(&c->cmap, maps) != hipSuccess) return RO_EHIP;
     c->canon_cap = n;
     c->sub_cap = subs;
+    c->cmap_cap = maps;
     return ensure_desc(c, tiles_for(n));
 }
 
@@ -173,7 +180,7 @@ int ro_ctx_create(ro_ctx **out, void *hip_stream)
     c->stream = (hipStream_t)hip_stream;
     if (hipGetDevice(&c->device) != hipSuccess ||
         hipDeviceGetAttribute(&c->num_cus, hipDeviceAttributeMultiprocessorCount, c->device) != hipSuccess ||
-        dev_alloc(&c->ctl, 1) != hipSuccess || dev_alloc(&c->samples, kMaxSamples) != hipSuccess) {
+        dev_alloc(&c->ctl, 1) != hipSuccess) {
         ro_ctx_destroy(c);
         return RO_EHIP;
     }
@@ -231,7 +238,7 @@ int ro_ctx_destroy(ro_ctx *c)
     (void)hipFree(c->desc);
     (void)hipFree(c->canon);
     (void)hipFree(c->sub_base);
-    (void)hipFree(c->samples);
+    (void)hipFree(c->cmap);
     (void)hipFree(c->cnt);
     if (c->tracer) {
         for (hipEvent_t e : c->tracer->pool) (void)hipEventDestroy(e);
@@ -287,7 +294,7 @@ int ro_batch(ro_ctx *c, const uint32_t *queue, const uint8_t *keep, int64_t q_le
     if (rc) return rc;
     return hip_fail(launch_batch(launch_of(c), queue, keep, q_len, offsets, n_parents, batch_size,
                                  out_child, out_parent, out_ordinal, out_cap, n_out_dev, n_batches_dev,
-                                 c->samples));
+                                 c->cmap, c->cmap_cap));
 }
 
 int ro_gather(ro_ctx *c, const ro_reports *r, const int64_t *offsets, int64_t n_parents,

@@ -11,8 +11,7 @@ namespace ro {
 constexpr int kBlock = 256;                 // threads per workgroup (4 waves of 64)
 constexpr int kItems = 16;                  // items per thread in scan tiles
 constexpr int kTile = kBlock * kItems;      // 4096 entries per scan tile
-constexpr int kSub = 1024;                  // children per copy sub-tile (one wave's share of a tile)
-constexpr int kMaxSamples = 2048;           // LDS-resident samples of the offsets array
+constexpr int kSub = 256;                   // children per copy sub-tile (one wave's unit of work)
 constexpr int kCntLds = 1024;               // parents aggregated in LDS per tile
 
 // Canonical per-child record written by the report scatter.  `tag` holds the
@@ -79,7 +78,8 @@ hipError_t launch_expand(const Launch &L, const int32_t *counts, int64_t P,
 hipError_t launch_batch(const Launch &L, const uint32_t *queue, const uint8_t *keep,
                         int64_t Q, const int64_t *offsets, int64_t P, int32_t B,
                         uint32_t *out_child, uint32_t *out_parent, uint32_t *out_ordinal,
-                        int64_t out_cap, int64_t *n_out, int64_t *n_batches, int64_t *samples);
+                        int64_t out_cap, int64_t *n_out, int64_t *n_batches, uint32_t *cmap,
+                        int64_t cmap_cap);
 
 struct GatherArgs {
     const uint32_t *rp, *ro;

@@ -7,8 +7,9 @@ Single level (a batch of one Call over the children of one expansion):
   1. ro_expand  counts -> offsets, per-child (parent, ordinal)
   2. ro_batch   ready queue with the dispatch mask -> report tags of the
                 dispatched children, in FIFO order, slots [0, M)
-  3. ro_batch   same queue with the sealed mask -> report tags of the children
-                that turned terminal without dispatch, slots [M, N)
+  3. ro_batch   the list of children that turned terminal without dispatch
+                (sealed before reaching the queue head) -> their report tags,
+                slots [M, N)
   4. ro_gather  reports -> parent slots, counts, completion
 
 Nested (two expansions, RayOrch's multi-grain program shape): the lower
@@ -29,11 +30,11 @@ def _empty(n, dtype):
 class SingleLevelBuffers:
     """Device inputs and outputs of one single-level pipeline."""
 
-    def __init__(self, counts, queue, keep, sealed, rep_state, rep_off, data, n_children,
+    def __init__(self, counts, queue, keep, sealed_ids, rep_state, rep_off, data, n_children,
                  n_dispatched, batch_size, out_cap=None, want_data=True):
         P = counts.numel()
         N = int(n_children)
-        self.counts, self.queue, self.keep, self.sealed = counts, queue, keep, sealed
+        self.counts, self.queue, self.keep, self.sealed_ids = counts, queue, keep, sealed_ids
         self.rep_state, self.rep_off, self.data = rep_state, rep_off, data
         self.N, self.M, self.B = N, int(n_dispatched), int(batch_size)
         self.offsets = _empty(P + 1, torch.int64)
@@ -61,8 +62,8 @@ def single_level(ctx, b: SingleLevelBuffers):
     ctx.batch(b.queue, b.keep, b.offsets, b.B, None, b.rep_parent, b.rep_ordinal,
               b.scalars[0:1], b.scalars[1:2], out_cap=M)
     if N > M:
-        ctx.batch(b.queue, b.sealed, b.offsets, b.B, None, b.rep_parent[M:], b.rep_ordinal[M:],
-                  b.scalars[2:3], b.scalars[3:4], out_cap=N - M)
+        ctx.batch(b.sealed_ids, None, b.offsets, b.B, None, b.rep_parent[M:], b.rep_ordinal[M:],
+                  b.scalars[2:3], b.scalars[3:4], q_len=N - M, out_cap=N - M)
     ctx.gather(b.rep_parent, b.rep_ordinal, b.rep_state, b.rep_off, b.data, b.offsets, b.out_off,
                b.out_data, b.n_success, b.n_failed, b.n_skipped, b.complete, b.parent_state, n=N,
                out_cap=b.out_cap)

@@ -22,7 +22,7 @@ def stage_single(c, want_data=True):
     r = c.reports
     data = D.reports_data_dev(r) if want_data else torch.zeros(1, dtype=torch.uint8, device="cuda")
     b = PL.SingleLevelBuffers(
-        D.to_dev(c.counts), D.to_dev(c.queue.view(np.int32)), D.to_dev(c.keep), D.to_dev(c.sealed),
+        D.to_dev(c.counts), D.to_dev(c.queue.view(np.int32)), D.to_dev(c.keep), D.to_dev(c.sealed_ids.view(np.int32)),
         D.to_dev(r.state), D.to_dev(r.off), data, c.n_children, c.n_dispatched, c.batch_size,
         want_data=want_data)
     return b
@@ -33,7 +33,7 @@ def oracle_single(c, data=None, with_data=True):
     r = c.reports
     offs, cp, co = O.expand(c.counts)
     b1 = O.batch(c.queue, c.keep, offs, c.batch_size)
-    b2 = O.batch(c.queue, c.sealed, offs, c.batch_size)
+    b2 = O.batch(c.sealed_ids, None, offs, c.batch_size)
     par = np.concatenate([b1[1], b2[1]])
     ordi = np.concatenate([b1[2], b2[2]])
     if with_data and data is None:

@@ -212,6 +212,11 @@ class SingleLevel:
         return (1 - self.keep).astype(np.uint8)
 
     @property
+    def sealed_ids(self):
+        """Children that turned terminal without dispatch, in queue order."""
+        return np.ascontiguousarray(self.queue[self.keep == 0])
+
+    @property
     def n_dispatched(self):
         return int(self.keep.sum())
 

@@ -83,13 +83,21 @@ __global__ __launch_bounds__(kBlock) void k_gather_scatter(
 // ---------------------------------------------------------------- scan
 // One tile = 4096 canonical children, 16 consecutive per thread; a wave
 // covers exactly one copy sub-tile (1024 children).
+//
+// The same kernel serves the streaming emission: there the "parents" are the
+// parents emitted by this call (their count P only known on the device, read
+// from *P_dev), `offsets` is the exclusive scan of their child counts, child
+// v lives in canonical slot vmap[v], the slot epoch is fixed, and no
+// per-parent counts are produced (ns = nf = nk = null).
 __global__ __launch_bounds__(kBlock) void k_gather_scan(
-    const int64_t *__restrict__ offsets, int64_t P, const Canon *__restrict__ canon, int64_t canon_cap,
+    const int64_t *__restrict__ offsets, int64_t P_arg, const int64_t *__restrict__ P_dev,
+    const uint32_t *__restrict__ vmap, uint32_t epoch_arg, const Canon *__restrict__ canon, int64_t canon_cap,
     int64_t *__restrict__ out_off, int32_t *__restrict__ ns, int32_t *__restrict__ nf,
     int32_t *__restrict__ nk, int64_t *__restrict__ sub_base, Ctl *ctl, uint64_t *desc,
     int64_t desc_cap)
 {
-    const uint32_t epoch = ctl->canon_epoch;
+    const int64_t P = P_dev ? *P_dev : P_arg;
+    const uint32_t epoch = epoch_arg ? epoch_arg : ctl->canon_epoch;
     const uint32_t sepoch = scan_epoch(ctl);
     __shared__ int64_t s_wave[kBlock / 64];
     __shared__ uint64_t s_b;
@@ -130,7 +138,7 @@ __global__ __launch_bounds__(kBlock) void k_gather_scan(
             len[k] = 0;
             stv[k] = 4;
             if (c < ct1) {
-                const Canon e = canon[c];
+                const Canon e = canon[vmap ? (int64_t)vmap[c] : c];
                 if ((e.tag >> 2) == epoch) {
                     stv[k] = e.tag & 3u;
                     len[k] = stv[k] == RO_SUCCESS ? e.len : 0;
@@ -446,11 +454,13 @@ __device__ __forceinline__ void copy_records64(const int64_t *s_dst, const uint6
 #define RO_COPY_WAVES 4
 #endif
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_WAVES))) void k_gather_copy(
-    const int64_t *__restrict__ offsets, int64_t P, const Canon *__restrict__ canon, int64_t canon_cap,
+    const int64_t *__restrict__ offsets, int64_t P_arg, const int64_t *__restrict__ P_dev,
+    const uint32_t *__restrict__ vmap, uint32_t epoch_arg, const Canon *__restrict__ canon, int64_t canon_cap,
     const int64_t *__restrict__ sub_base, uint8_t *__restrict__ out, Ctl *ctl)
 {
     constexpr int kWaves = kBlock / 64;
-    const uint32_t epoch = ctl->canon_epoch;
+    const int64_t P = P_dev ? *P_dev : P_arg;
+    const uint32_t epoch = epoch_arg ? epoch_arg : ctl->canon_epoch;
     __shared__ int64_t s_dst_all[kWaves][kSub + 1];     // destination offset of each record, relative
     __shared__ int32_t s_dst32_all[kWaves][kSub + 1];   // the same, when the window is under 2 GiB
     __shared__ uint64_t s_src_all[kWaves][kSub];
@@ -476,7 +486,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_
             l[k] = 0;
             s[k] = 0;
             if (r < cnt) {
-                const Canon e = canon[c0 + r];
+                const Canon e = canon[vmap ? (int64_t)vmap[c0 + r] : c0 + r];
                 if (e.tag == ((epoch << 2) | RO_SUCCESS)) {
                     l[k] = e.len;
                     s[k] = e.src;
@@ -517,8 +527,8 @@ hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w
               a.nk, L.ctl);
     const int64_t grid_s = (int64_t)L.num_cus * 4;
     RO_LAUNCH(L, RO_K_GATHER_SCAN, k_gather_scan, dim3((unsigned)grid_s), dim3(kBlock), 0, L.stream, a.offsets, a.P,
-                       w.canon, w.canon_cap, a.out_off, a.ns, a.nf, a.nk, w.sub_base, L.ctl, L.desc,
-                       L.desc_cap);
+              (const int64_t *)nullptr, (const uint32_t *)nullptr, 0u, w.canon, w.canon_cap, a.out_off, a.ns,
+              a.nf, a.nk, w.sub_base, L.ctl, L.desc, L.desc_cap);
     int64_t grid_f = (a.P + kBlock - 1) / kBlock;
     grid_f = grid_f < 1 ? 1 : (grid_f > (int64_t)L.num_cus * 8 ? (int64_t)L.num_cus * 8 : grid_f);
     RO_LAUNCH(L, RO_K_GATHER_FINALIZE, k_gather_finalize, dim3((unsigned)grid_f), dim3(kBlock), 0, L.stream, a.offsets,
@@ -527,9 +537,31 @@ hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w
     if (a.out_data != nullptr) {
         const int64_t grid_c = (int64_t)L.num_cus * 8;
         RO_LAUNCH(L, RO_K_GATHER_COPY, k_gather_copy, dim3((unsigned)grid_c), dim3(kBlock), 0, L.stream, a.offsets,
-                           a.P, w.canon, w.canon_cap, w.sub_base, a.out_data, L.ctl);
+                  a.P, (const int64_t *)nullptr, (const uint32_t *)nullptr, 0u, w.canon, w.canon_cap, w.sub_base,
+                  a.out_data, L.ctl);
     }
     RO_LAUNCH(L, RO_K_GATHER_RESET, k_gather_reset, dim3(1), dim3(64), 0, L.stream, L.ctl);
+    return hipGetLastError();
+}
+
+// The streaming emission's pass over its virtual expansion (emitted parents'
+// children): byte scan into emitted slot offsets, then the ordered copy.
+hipError_t launch_virtual_scan(const Launch &L, const int64_t *voff, const int64_t *E_dev, const uint32_t *vmap,
+                               const Canon *canon, int64_t canon_cap, int64_t *emit_off, int64_t *sub_base)
+{
+    const int64_t grid_s = (int64_t)L.num_cus * 4;
+    RO_LAUNCH(L, RO_K_STREAM_SCAN, k_gather_scan, dim3((unsigned)grid_s), dim3(kBlock), 0, L.stream, voff,
+              (int64_t)0, E_dev, vmap, 1u, canon, canon_cap, emit_off, (int32_t *)nullptr, (int32_t *)nullptr,
+              (int32_t *)nullptr, sub_base, L.ctl, L.desc, L.desc_cap);
+    return hipGetLastError();
+}
+
+hipError_t launch_virtual_copy(const Launch &L, const int64_t *voff, const int64_t *E_dev, const uint32_t *vmap,
+                               const Canon *canon, int64_t canon_cap, const int64_t *sub_base, uint8_t *out)
+{
+    const int64_t grid_c = (int64_t)L.num_cus * 8;
+    RO_LAUNCH(L, RO_K_STREAM_COPY, k_gather_copy, dim3((unsigned)grid_c), dim3(kBlock), 0, L.stream, voff,
+              (int64_t)0, E_dev, vmap, 1u, canon, canon_cap, sub_base, out, L.ctl);
     return hipGetLastError();
 }
 

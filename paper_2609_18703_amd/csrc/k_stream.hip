@@ -1,0 +1,280 @@
+// Streaming completion on gfx950: reports arrive wave by wave; after each
+// wave, every parent whose children are now all terminal is emitted once, in
+// ascending parent order, with its ordered bytes, counts and state.
+//
+// RayOrch (arXiv 2609.18703): a parent can finalise and proceed as soon as all
+// of its required child results are terminal (Sec. 1; Sec. 4 Reduce rule);
+// facts are published once and conflicting repeats are rejected (Sec. 4,
+// publication rules).
+//
+// Per wave:   report  -> canonical slots + seen bits + per-parent counts.
+// Per emit:   select  -> ascending list of newly complete parents (look-back
+//                        compaction over all parents), their counts/state;
+//             vscan   -> exclusive scan of their child counts: a "virtual"
+//                        expansion whose children are the emitted parents'
+//                        children, in order;
+//             vmap    -> canonical slot of every virtual child;
+//             then the gather's canonical scan and copy kernels run over the
+//             virtual expansion, and finish closes the call.
+#include "ro_device.h"
+
+namespace ro {
+
+constexpr uint32_t kStreamEpoch = 1;      // slot tag epoch of an accepted stream report
+
+// Validates the expansion once: offsets[0] = 0, nondecreasing, offsets[P] = N.
+__global__ void k_stream_check(const int64_t *__restrict__ offsets, int64_t P, int64_t N, Ctl *ctl)
+{
+    const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    bool bad = (g == 0) && (offsets[0] != 0 || offsets[P] != N);
+    for (int64_t p = g; p < P; p += (int64_t)gridDim.x * blockDim.x)
+        if (offsets[p + 1] < offsets[p]) bad = true;
+    if (bad) raise_err(ctl, RO_EINVAL);
+}
+
+__global__ __launch_bounds__(kBlock) void k_stream_report(
+    const uint32_t *__restrict__ rp, const uint32_t *__restrict__ ro_, const uint8_t *__restrict__ rs,
+    const int64_t *__restrict__ roff, const uint8_t *data, int64_t n, const int64_t *__restrict__ offsets,
+    int64_t P, int64_t N, Canon *__restrict__ canon, uint32_t *__restrict__ seen, int32_t *__restrict__ cnt,
+    Ctl *ctl)
+{
+    const int64_t gtid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    const int64_t gstride = (int64_t)gridDim.x * kBlock;
+    int err = 0;
+    if (gtid == 0 && n > 0 && roff[0] < 0) err = RO_EINVAL;
+    for (int64_t i = gtid; i < n; i += gstride) {
+        const uint32_t s = rs[i];
+        const int64_t o0 = roff[i], o1 = roff[i + 1];
+        if (o1 < o0) { err = RO_EINVAL; continue; }
+        if (s > RO_PENDING) { err = RO_ESTATE; continue; }
+        if (s == RO_PENDING) continue;
+        const uint32_t p = rp[i];
+        if ((int64_t)p >= P) { err = RO_ERANGE; continue; }
+        const int64_t st = offsets[p];
+        const uint32_t o = ro_[i];
+        if ((int64_t)o >= offsets[p + 1] - st) { err = RO_ERANGE; continue; }
+        const int64_t c = st + (int64_t)o;
+        if (st < 0 || c >= N) { err = RO_EINVAL; continue; }
+        const int64_t len = s == RO_SUCCESS ? o1 - o0 : 0;
+        if (len >= ((int64_t)1 << 32)) { err = RO_EOVERFLOW; continue; }
+        // first report of this child, in this wave or any earlier one
+        const uint32_t bit = 1u << (c & 31);
+        const uint32_t old = atomicOr(&seen[c >> 5], bit);
+        if (old & bit) { err = RO_EDUP; continue; }
+        Canon e;
+        e.src = reinterpret_cast<uint64_t>(data) + (uint64_t)o0;
+        e.len = (uint32_t)len;
+        e.tag = (kStreamEpoch << 2) | s;
+        canon[c] = e;
+        atomicAdd(&cnt[(int64_t)s * P + p], 1);
+    }
+    if (err) raise_err(ctl, err);
+}
+
+// Newly complete parents, compacted in ascending order (one tile = 4096 parents).
+__global__ __launch_bounds__(kBlock) void k_stream_select(
+    const int64_t *__restrict__ offsets, int64_t P, const int32_t *__restrict__ cnt,
+    uint8_t *__restrict__ emitted, uint32_t *__restrict__ elist, int64_t *__restrict__ ekids,
+    uint32_t *__restrict__ emit_parent, int32_t *__restrict__ ns, int32_t *__restrict__ nf,
+    int32_t *__restrict__ nk, uint8_t *__restrict__ pstate, int64_t cap_parents, int64_t *n_emitted,
+    Ctl *ctl, uint64_t *desc, int64_t desc_cap, int64_t ntiles)
+{
+    const uint32_t epoch = scan_epoch(ctl);
+    __shared__ int64_t s_wave[kBlock / 64];
+    __shared__ uint64_t s_b;
+    __shared__ int64_t s_t;
+    __shared__ int32_t s_last;
+    for (;;) {
+        const int64_t t = next_ticket(ctl, &s_t);
+        if (t >= ntiles) break;
+        const int64_t p0 = t * kTile + (int64_t)threadIdx.x * kItems;
+        uint32_t fmask = 0;
+#pragma unroll
+        for (int k = 0; k < kItems; ++k) {
+            const int64_t p = p0 + k;
+            if (p < P && !emitted[p]) {
+                const int64_t got = (int64_t)cnt[p] + cnt[P + p] + cnt[2 * P + p];
+                if (got == offsets[p + 1] - offsets[p]) fmask |= 1u << k;
+            }
+        }
+        int64_t tot;
+        const int64_t ex = block_excl_scan(__popc(fmask), s_wave, tot);
+        const uint64_t pre = tile_prefix(desc, t, epoch, (uint64_t)tot, &s_b, ctl);
+        int64_t e = (int64_t)pre + ex;
+        bool over = false;
+#pragma unroll
+        for (int k = 0; k < kItems; ++k) {
+            if (!(fmask & (1u << k))) continue;
+            const int64_t p = p0 + k;
+            if (e < cap_parents) {
+                const int32_t a = cnt[p], f = cnt[P + p], s = cnt[2 * P + p];
+                elist[e] = (uint32_t)p;
+                ekids[e] = offsets[p + 1] - offsets[p];
+                if (emit_parent) emit_parent[e] = (uint32_t)p;
+                if (ns) ns[e] = a;
+                if (nf) nf[e] = f;
+                if (nk) nk[e] = s;
+                if (pstate) pstate[e] = f > 0 ? RO_FAILED : RO_SUCCESS;
+                emitted[p] = 1;
+            } else {
+                over = true;
+            }
+            ++e;
+        }
+        if (over) raise_err(ctl, RO_ECAP);
+        if (t == ntiles - 1 && threadIdx.x == 0) {
+            int64_t E = (int64_t)pre + tot;
+            if (n_emitted) *n_emitted = E;
+            ctl->n_items = E < cap_parents ? E : cap_parents;
+        }
+    }
+    ticket_done(ctl, epoch, desc, desc_cap, &s_last);
+}
+
+// evoff = exclusive scan of ekids[0..E); evoff[E] = total virtual children.
+__global__ __launch_bounds__(kBlock) void k_stream_vscan(const int64_t *__restrict__ ekids,
+                                                         int64_t *__restrict__ evoff, Ctl *ctl,
+                                                         uint64_t *desc, int64_t desc_cap)
+{
+    const uint32_t epoch = scan_epoch(ctl);
+    __shared__ int64_t s_wave[kBlock / 64];
+    __shared__ uint64_t s_b;
+    __shared__ int64_t s_t;
+    __shared__ int32_t s_last;
+    const int64_t E = ctl->n_items;
+    const int64_t ntiles = E > 0 ? (E + kTile - 1) / kTile : 1;
+    for (;;) {
+        const int64_t t = next_ticket(ctl, &s_t);
+        if (t >= ntiles) break;
+        const int64_t e0 = t * kTile + (int64_t)threadIdx.x * kItems;
+        int64_t v[kItems];
+        int64_t sum = 0;
+#pragma unroll
+        for (int k = 0; k < kItems; ++k) {
+            v[k] = e0 + k < E ? ekids[e0 + k] : 0;
+            sum += v[k];
+        }
+        int64_t tot;
+        const int64_t ex = block_excl_scan(sum, s_wave, tot);
+        const uint64_t pre = tile_prefix(desc, t, epoch, (uint64_t)tot, &s_b, ctl);
+        int64_t run = (int64_t)pre + ex;
+#pragma unroll
+        for (int k = 0; k < kItems; ++k) {
+            if (e0 + k < E) evoff[e0 + k] = run;
+            run += v[k];
+        }
+        if (t == ntiles - 1 && threadIdx.x == 0) {
+            evoff[E] = (int64_t)pre + tot;
+            ctl->n_virtual = (int64_t)pre + tot;
+        }
+    }
+    ticket_done(ctl, epoch, desc, desc_cap, &s_last);
+}
+
+// vmap[v] = canonical slot of virtual child v: the (v - evoff[e])-th child of
+// emitted parent elist[e].  16 consecutive virtual children per thread.
+__global__ __launch_bounds__(kBlock) void k_stream_vmap(const int64_t *__restrict__ evoff,
+                                                        const uint32_t *__restrict__ elist,
+                                                        const int64_t *__restrict__ offsets,
+                                                        uint32_t *__restrict__ vmap, Ctl *ctl)
+{
+    const int64_t E = ctl->n_items;
+    const int64_t V = ctl->n_virtual;
+    const int64_t nthreads = (V + kItems - 1) / kItems;
+    for (int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x; g < nthreads;
+         g += (int64_t)gridDim.x * kBlock) {
+        const int64_t v0 = g * kItems;
+        int64_t e = upper_bound_g(evoff, 0, E + 1, v0) - 1;
+        int64_t start = evoff[e];
+        int64_t base = offsets[elist[e]];
+        for (int k = 0; k < kItems; ++k) {
+            const int64_t v = v0 + k;
+            if (v >= V) break;
+            if (v >= evoff[e + 1]) {
+                e = advance_parent(evoff, E, e, v);
+                start = evoff[e];
+                base = offsets[elist[e]];
+            }
+            vmap[v] = (uint32_t)(base + (v - start));
+        }
+    }
+}
+
+// Before the copy: trailing slot offsets, capacity check.
+__global__ void k_stream_emit_check(int64_t *__restrict__ emit_off, const int64_t *__restrict__ evoff,
+                                    int64_t cap_bytes, int has_data, int64_t *n_bytes, Ctl *ctl)
+{
+    const int64_t E = ctl->n_items;
+    const int64_t V = ctl->n_virtual;
+    const int64_t total = V > 0 ? ctl->total : 0;
+    const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (g == 0) {
+        emit_off[E] = total;
+        if (n_bytes) *n_bytes = total;
+        if (has_data && total > cap_bytes) raise_err(ctl, RO_ECAP);
+    }
+    // emitted parents without children at the very end get the total
+    for (int64_t e = g; e < E; e += (int64_t)gridDim.x * blockDim.x)
+        if (evoff[e] >= V) emit_off[e] = total;
+}
+
+__global__ void k_stream_finish(Ctl *ctl)
+{
+    if (threadIdx.x == 0) {
+        ctl->n_items = 0;
+        ctl->n_virtual = 0;
+        ctl->total = 0;
+        ctl->n_filled = 0;    // counted by the canonical scan, unused here
+    }
+}
+
+hipError_t launch_stream_init(const Launch &L, StreamState &s)
+{
+    RO_LAUNCH(L, RO_K_MISC, k_stream_check, dim3((unsigned)L.num_cus), dim3(256), 0, L.stream, s.offsets, s.P,
+              s.N, L.ctl);
+    return hipGetLastError();
+}
+
+hipError_t launch_stream_report(const Launch &L, StreamState &s, const uint32_t *rp, const uint32_t *ro,
+                                const uint8_t *rs, const int64_t *roff, const uint8_t *data, int64_t n)
+{
+    int64_t grid = (n + kBlock - 1) / kBlock;
+    grid = grid < 1 ? 1 : (grid > (int64_t)L.num_cus * 8 ? (int64_t)L.num_cus * 8 : grid);
+    RO_LAUNCH(L, RO_K_STREAM_REPORT, k_stream_report, dim3((unsigned)grid), dim3(kBlock), 0, L.stream, rp, ro,
+              rs, roff, data, n, s.offsets, s.P, s.N, s.canon, s.seen, s.cnt, L.ctl);
+    return hipGetLastError();
+}
+
+hipError_t launch_virtual_scan(const Launch &L, const int64_t *voff, const int64_t *E_dev, const uint32_t *vmap,
+                               const Canon *canon, int64_t canon_cap, int64_t *emit_off, int64_t *sub_base);
+hipError_t launch_virtual_copy(const Launch &L, const int64_t *voff, const int64_t *E_dev, const uint32_t *vmap,
+                               const Canon *canon, int64_t canon_cap, const int64_t *sub_base, uint8_t *out);
+
+hipError_t launch_stream_emit(const Launch &L, StreamState &s, uint32_t *emit_parent, int64_t *emit_off,
+                              uint8_t *emit_data, int64_t cap_parents, int64_t cap_bytes, int32_t *ns,
+                              int32_t *nf, int32_t *nk, uint8_t *pstate, int64_t *n_emitted,
+                              int64_t *n_bytes)
+{
+    const int64_t ntiles = s.P > 0 ? (s.P + kTile - 1) / kTile : 1;
+    const int64_t grid = ntiles < (int64_t)L.num_cus * 4 ? ntiles : (int64_t)L.num_cus * 4;
+    RO_LAUNCH(L, RO_K_STREAM_SELECT, k_stream_select, dim3((unsigned)grid), dim3(kBlock), 0, L.stream,
+              s.offsets, s.P, s.cnt, s.emitted, s.elist, s.ekids, emit_parent, ns, nf, nk, pstate, cap_parents,
+              n_emitted, L.ctl, L.desc, L.desc_cap, ntiles);
+    const int64_t grid_v = (int64_t)L.num_cus * 2;
+    RO_LAUNCH(L, RO_K_STREAM_SELECT, k_stream_vscan, dim3((unsigned)grid_v), dim3(kBlock), 0, L.stream, s.ekids,
+              s.evoff, L.ctl, L.desc, L.desc_cap);
+    RO_LAUNCH(L, RO_K_STREAM_SELECT, k_stream_vmap, dim3((unsigned)L.num_cus * 8), dim3(kBlock), 0, L.stream,
+              s.evoff, s.elist, s.offsets, s.vmap, L.ctl);
+    hipError_t e = launch_virtual_scan(L, s.evoff, &L.ctl->n_items, s.vmap, s.canon, s.N, emit_off, s.sub_base);
+    if (e != hipSuccess) return e;
+    RO_LAUNCH(L, RO_K_STREAM_FINISH, k_stream_emit_check, dim3((unsigned)L.num_cus), dim3(256), 0, L.stream,
+              emit_off, s.evoff, cap_bytes, emit_data != nullptr ? 1 : 0, n_bytes, L.ctl);
+    if (emit_data != nullptr) {
+        e = launch_virtual_copy(L, s.evoff, &L.ctl->n_items, s.vmap, s.canon, s.N, s.sub_base, emit_data);
+        if (e != hipSuccess) return e;
+    }
+    RO_LAUNCH(L, RO_K_STREAM_FINISH, k_stream_finish, dim3(1), dim3(64), 0, L.stream, L.ctl);
+    return hipGetLastError();
+}
+
+}  // namespace ro

@@ -345,15 +345,74 @@ int ro_gather(ro_ctx *c, const ro_reports *r, const int64_t *offsets, int64_t n_
 int ro_stream_create(ro_ctx *c, const int64_t *offsets, int64_t n_parents, int64_t n_children,
                      ro_stream **out)
 {
-    (void)c; (void)offsets; (void)n_parents; (void)n_children;
     if (out) *out = nullptr;
-    return RO_EINVAL;
+    if (!c || !offsets || !out || n_parents < 0 || n_children < 0 || n_children >= ((int64_t)1 << 32))
+        return RO_EINVAL;
+    const int64_t P = n_parents, N = n_children;
+    int rc = ensure_desc(c, tiles_for(P > N ? P : N));
+    if (rc) return rc;
+    // one allocation, carved into 256-byte aligned arrays
+    const int64_t subs = (N / kTile + 2) * (kTile / kSub);
+    const size_t sizes[] = {
+        (size_t)(N > 0 ? N : 1) * sizeof(Canon),            // canon
+        (size_t)((N + 31) / 32 + 1) * sizeof(uint32_t),     // seen
+        (size_t)(3 * P + 1) * sizeof(int32_t),              // cnt
+        (size_t)(P + 1),                                    // emitted
+        (size_t)(P + 1) * sizeof(uint32_t),                 // elist
+        (size_t)(P + 1) * sizeof(int64_t),                  // ekids
+        (size_t)(P + 2) * sizeof(int64_t),                  // evoff
+        (size_t)(N + 1) * sizeof(uint32_t),                 // vmap
+        (size_t)subs * sizeof(int64_t),                     // sub_base
+    };
+    size_t offs[9], total = 0;
+    for (int i = 0; i < 9; ++i) {
+        offs[i] = total;
+        total += (sizes[i] + 255) & ~(size_t)255;
+    }
+    ro_stream *s = (ro_stream *)calloc(1, sizeof(ro_stream));
+    if (!s) return RO_EINVAL;
+    char *block = nullptr;
+    if (hipStreamSynchronize(c->stream) != hipSuccess || hipMalloc((void **)&block, total) != hipSuccess) {
+        free(s);
+        return RO_EHIP;
+    }
+    if (hipMemset(block, 0, total) != hipSuccess) {
+        (void)hipFree(block);
+        free(s);
+        return RO_EHIP;
+    }
+    s->ctx = c;
+    s->block = block;
+    StreamState &st = s->st;
+    st.offsets = offsets;
+    st.P = P;
+    st.N = N;
+    st.canon = (Canon *)(block + offs[0]);
+    st.seen = (uint32_t *)(block + offs[1]);
+    st.cnt = (int32_t *)(block + offs[2]);
+    st.emitted = (uint8_t *)(block + offs[3]);
+    st.elist = (uint32_t *)(block + offs[4]);
+    st.ekids = (int64_t *)(block + offs[5]);
+    st.evoff = (int64_t *)(block + offs[6]);
+    st.vmap = (uint32_t *)(block + offs[7]);
+    st.sub_base = (int64_t *)(block + offs[8]);
+    st.sub_cap = subs;
+    if (launch_stream_init(launch_of(c), st) != hipSuccess) {
+        (void)hipFree(block);
+        free(s);
+        return RO_EHIP;
+    }
+    *out = s;
+    return RO_OK;
 }
 
-int ro_stream_report(ro_ctx *c, ro_stream *s, const ro_reports *wave)
+int ro_stream_report(ro_ctx *c, ro_stream *s, const ro_reports *r)
 {
-    (void)c; (void)s; (void)wave;
-    return RO_EINVAL;
+    if (!c || !s || !r || s->ctx != c || r->n < 0) return RO_EINVAL;
+    if (r->n > 0 && (!r->parent || !r->ordinal || !r->state || !r->off)) return RO_EINVAL;
+    if (r->n == 0) return RO_OK;
+    return hip_fail(launch_stream_report(launch_of(c), s->st, r->parent, r->ordinal, r->state, r->off, r->data,
+                                         r->n));
 }
 
 int ro_stream_emit(ro_ctx *c, ro_stream *s, uint32_t *emit_parent, int64_t *emit_off,
@@ -361,16 +420,19 @@ int ro_stream_emit(ro_ctx *c, ro_stream *s, uint32_t *emit_parent, int64_t *emit
                    int32_t *n_success, int32_t *n_failed, int32_t *n_skipped,
                    uint8_t *parent_state, int64_t *n_emitted_dev, int64_t *n_bytes_dev)
 {
-    (void)c; (void)s; (void)emit_parent; (void)emit_off; (void)emit_data; (void)cap_parents;
-    (void)cap_bytes; (void)n_success; (void)n_failed; (void)n_skipped; (void)parent_state;
-    (void)n_emitted_dev; (void)n_bytes_dev;
-    return RO_EINVAL;
+    if (!c || !s || s->ctx != c || !emit_off || cap_parents < 0 || cap_bytes < 0) return RO_EINVAL;
+    return hip_fail(launch_stream_emit(launch_of(c), s->st, emit_parent, emit_off, emit_data, cap_parents,
+                                       cap_bytes, n_success, n_failed, n_skipped, parent_state, n_emitted_dev,
+                                       n_bytes_dev));
 }
 
 int ro_stream_destroy(ro_stream *s)
 {
-    (void)s;
-    return RO_EINVAL;
+    if (!s) return RO_EINVAL;
+    if (s->ctx) (void)hipStreamSynchronize(s->ctx->stream);
+    (void)hipFree(s->block);
+    free(s);
+    return RO_OK;
 }
 
 }  // extern "C"

@@ -114,7 +114,9 @@ struct StreamState {
     int32_t *cnt;            // [3*P] per-parent SUCCESS / FAILED / SKIPPED counts
     uint8_t *emitted;        // [P]
     uint32_t *elist;         // [P] emitted parents of the current emission
+    int64_t *ekids;          // [P] their child counts
     int64_t *evoff;          // [P+1] child offsets of the emitted parents (virtual children)
+    uint32_t *vmap;          // [N] canonical slot of each virtual child
     int64_t *sub_base;       // per sub-tile of virtual children
     int64_t sub_cap;
 };

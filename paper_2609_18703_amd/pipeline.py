@@ -20,7 +20,8 @@ from __future__ import annotations
 
 import torch
 
-__all__ = ["SingleLevelBuffers", "single_level", "NestedBuffers", "nested"]
+__all__ = ["SingleLevelBuffers", "single_level", "NestedBuffers", "nested", "StreamingBuffers",
+           "streaming"]
 
 
 def _empty(n, dtype):
@@ -120,3 +121,52 @@ def nested(ctx, b: NestedBuffers):
     ctx.gather(b.mid_parent, b.mid_ordinal, b.mid_state, b.mid_off, b.mid_data, b.offsets1,
                b.top_off, b.top_data, b.top_cnt[:b.P1], b.top_cnt[b.P1:2 * b.P1], b.top_cnt[2 * b.P1:],
                b.top_complete, b.top_state, n=N1, out_cap=b.cap)
+
+
+class StreamingBuffers:
+    """Device inputs and per-wave outputs of a streaming run over one expansion.
+
+    ``queues[w]`` are the children that turn terminal in wave w (in ready
+    order), ``states[w]`` / ``offs[w]`` their reports; every wave's bytes live
+    in one arena (``data``) that outlives the run.
+    """
+
+    def __init__(self, counts, queues, states, offs, data, n_children, batch_size, emit_cap_bytes):
+        P = counts.numel()
+        self.P, self.N, self.B = P, int(n_children), int(batch_size)
+        self.counts, self.queues, self.states, self.offs, self.data = counts, queues, states, offs, data
+        self.offsets = _empty(P + 1, torch.int64)
+        wmax = max((q.numel() for q in queues), default=1)
+        self.tag_parent = _empty(wmax, torch.int32)
+        self.tag_ordinal = _empty(wmax, torch.int32)
+        self.scalars = torch.zeros(4, dtype=torch.int64, device="cuda")   # M, nb, emitted, bytes
+        self.emit_parent = _empty(P, torch.int32)
+        self.emit_off = _empty(P + 1, torch.int64)
+        self.emit_cap = int(emit_cap_bytes)
+        self.emit_data = _empty(self.emit_cap, torch.uint8)
+        self.emit_cnt = _empty(3 * P, torch.int32)
+        self.emit_state = _empty(P, torch.uint8)
+
+
+def streaming(ctx, b: StreamingBuffers, on_wave=None):
+    """expand once; per wave: batch -> stream report -> stream emit.
+
+    ``on_wave(w)`` (optional) runs after each wave's emission is enqueued, to
+    consume that wave's outputs before the next wave overwrites them.
+    """
+    P = b.P
+    ctx.expand(b.counts, b.offsets)
+    st = ctx.stream(b.offsets, b.N)
+    try:
+        for w, q in enumerate(b.queues):
+            n = q.numel()
+            ctx.batch(q, None, b.offsets, b.B, None, b.tag_parent, b.tag_ordinal,
+                      b.scalars[0:1], b.scalars[1:2], q_len=n, out_cap=n)
+            st.report(b.tag_parent, b.tag_ordinal, b.states[w], b.offs[w], b.data, n=n)
+            st.emit(b.emit_parent, b.emit_off, b.emit_data, b.emit_cnt[:P], b.emit_cnt[P:2 * P],
+                    b.emit_cnt[2 * P:], b.emit_state, b.scalars[2:3], b.scalars[3:4],
+                    cap_parents=P, cap_bytes=b.emit_cap)
+            if on_wave is not None:
+                on_wave(w)
+    finally:
+        st.close()

@@ -344,7 +344,7 @@ int oracle_stream_report(oracle_stream *s, const uint32_t *rep_parent,
             return OR_EDUP;
         s->seen[c] = 1;
         s->state[c] = rep_state[i];
-        s->src[c] = data + rep_off[i];
+        s->src[c] = data != NULL ? data + rep_off[i] : NULL;   /* NULL: metadata only */
         s->len[c] = rep_state[i] == ST_SUCCESS ? rep_off[i + 1] - rep_off[i] : 0;
         s->cnt[rep_state[i]][p] += 1;
     }

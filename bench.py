@@ -35,12 +35,67 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--parents", type=int, default=100_000, help="parents of the Zipf(1.2) workload")
-    ap.add_argument("--cpu-parents", type=int, default=4000,
-                    help="parents in the CPU-oracle sample (same distributions)")
+    ap.add_argument("--cpu-parents", type=int, default=100_000,
+                    help="parents in the CPU-oracle sample (same distributions; about 10 s of one core)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
+    ap.add_argument("--rocprof-summary", metavar="DIR", default=None,
+                    help="print per-kernel averages from rocprofv3 CSV output under DIR and exit")
     return ap.parse_args()
+
+
+# kernel whose HBM counters feed roofline.traffic, the file holding them, and
+# the source they were taken from (a changed source voids the figure)
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gather_copy_zipf41M_counters.txt")
+TRAFFIC_SOURCE = os.path.join(ROOT, "paper_2609_18703_amd", "csrc", "k_gather.hip")
+
+
+def source_sha256(path):
+    import hashlib
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def traffic_from_profile():
+    """Calibrated HBM bytes per launch of the copy kernel, or None when the
+    counters were taken on a different kernel source."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    vals = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("source_sha256") != source_sha256(TRAFFIC_SOURCE):
+        return None
+    try:
+        return int(vals["calibrated_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def rocprof_summary(root):
+    """Per-kernel averages from rocprofv3 --output-format csv files under root."""
+    import csv
+    import glob
+    from collections import defaultdict
+    dur = defaultdict(list)
+    ctr = defaultdict(list)
+    for path in glob.glob(os.path.join(root, "**", "*kernel_trace.csv"), recursive=True):
+        for row in csv.DictReader(open(path)):
+            dur[row["Kernel_Name"].split("(")[0]].append(int(row["End_Timestamp"]) - int(row["Start_Timestamp"]))
+    for path in glob.glob(os.path.join(root, "**", "*counter_collection.csv"), recursive=True):
+        for row in csv.DictReader(open(path)):
+            ctr[(row["Kernel_Name"].split("(")[0], row["Counter_Name"])].append(float(row["Counter_Value"]))
+    if dur:
+        print(f"{'kernel':48s} {'calls':>6s} {'avg_us':>12s} {'total_ms':>10s}")
+        for k, v in sorted(dur.items(), key=lambda kv: -sum(kv[1])):
+            print(f"{k[:48]:48s} {len(v):6d} {sum(v) / len(v) / 1e3:12.2f} {sum(v) / 1e6:10.3f}")
+    if ctr:
+        print(f"{'kernel':48s} {'counter':12s} {'n':>4s} {'avg_KiB':>14s}")
+        for (k, c), v in sorted(ctr.items()):
+            print(f"{k[:48]:48s} {c:12s} {len(v):4d} {sum(v) / len(v):14.1f}")
 
 
 def log(*a):
@@ -70,6 +125,9 @@ def alg_bytes(kind, P, N, M, S):
 
 def main():
     args = parse()
+    if args.rocprof_summary:
+        rocprof_summary(args.rocprof_summary)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: this build has no multi-GPU path "
               f"(asked for --gpus {args.gpus}).", file=sys.stderr)
@@ -171,7 +229,8 @@ def main():
         },
         "roofline": {
             "bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
-            "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+            "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": traffic_from_profile() if dom == "gather_copy" else None,
             "alg_bytes_per_launch": dom_bytes, "avg_launch_ms": round(dom_avg_ms, 4),
         },
         "step_alg_GBps": round(total_alg / (ms_step * 1e-3) / 1e9, 1),

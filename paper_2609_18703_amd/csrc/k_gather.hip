@@ -105,6 +105,8 @@ __global__ __launch_bounds__(kBlock) void k_gather_scan(
     __shared__ int32_t s_last;
     __shared__ int64_t s_p[2];
     __shared__ int32_t s_cnt[3][kCntLds];
+    __shared__ uint32_t s_len[kTile + kTile / 16];
+    __shared__ alignas(16) uint8_t s_st[kTile];
     const int64_t N0 = offsets[P];
     // over capacity, or an invalid Expansion found by the scatter: no tiles
     const int64_t N = (N0 <= canon_cap && read_err(ctl) == 0) ? N0 : 0;
@@ -127,25 +129,45 @@ __global__ __launch_bounds__(kBlock) void k_gather_scan(
         const int64_t R = min64(pl - pf + 1, kCntLds);
         for (int j = threadIdx.x; j < 3 * kCntLds; j += kBlock) (&s_cnt[0][0])[j] = 0;
 
-        // pass 1: surviving lengths and filled slots
+        // pass 1: surviving lengths and filled slots.  Each wave reads its 1024
+        // slots lane-contiguously (1 KiB per load instruction) into LDS; then
+        // every thread takes its 16 consecutive children from there.  s_len is
+        // padded by one word per 16 so that both access patterns are free of
+        // bank conflicts.
+        {
+            const int wv = (int)(threadIdx.x >> 6), ln = lane_id();
+#pragma unroll
+            for (int k = 0; k < kItems; ++k) {
+                const int j = wv * (64 * kItems) + k * 64 + ln;
+                const int64_t c = ct0 + j;
+                uint32_t L = 0, S = 4;        // state, or 4 = not reported in this call
+                if (c < ct1) {
+                    const Canon e = canon[vmap ? (int64_t)vmap[c] : c];
+                    if ((e.tag >> 2) == epoch) {
+                        S = e.tag & 3u;
+                        L = S == RO_SUCCESS ? e.len : 0;
+                    }
+                }
+                s_len[j + (j >> 4)] = L;
+                s_st[j] = (uint8_t)S;
+            }
+        }
+        __syncthreads();
         const int64_t c0 = ct0 + (int64_t)threadIdx.x * kItems;
         uint32_t len[kItems];
-        uint32_t stv[kItems];          // state, or 4 = not reported in this call
+        uint32_t stv[kItems];
         int64_t sum = 0, filled = 0;
+        {
+            const uint4 sv = *reinterpret_cast<const uint4 *>(&s_st[threadIdx.x * kItems]);
+            const uint32_t sw[4] = {sv.x, sv.y, sv.z, sv.w};
 #pragma unroll
-        for (int k = 0; k < kItems; ++k) {
-            const int64_t c = c0 + k;
-            len[k] = 0;
-            stv[k] = 4;
-            if (c < ct1) {
-                const Canon e = canon[vmap ? (int64_t)vmap[c] : c];
-                if ((e.tag >> 2) == epoch) {
-                    stv[k] = e.tag & 3u;
-                    len[k] = stv[k] == RO_SUCCESS ? e.len : 0;
-                    ++filled;
-                }
+            for (int k = 0; k < kItems; ++k) {
+                const int j = (int)threadIdx.x * kItems + k;
+                len[k] = s_len[j + (j >> 4)];
+                stv[k] = (sw[k >> 2] >> (8 * (k & 3))) & 0xffu;
+                filled += stv[k] < 4 ? 1 : 0;
+                sum += len[k];
             }
-            sum += len[k];
         }
         filled_total += filled;
         int64_t tot;

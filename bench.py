@@ -1,23 +1,30 @@
 #!/usr/bin/env python3
 """Throughput of expand + FIFO batch + ordered gather on one MI355X.
 
-One step = the whole path over one batch of the synthetic workload: ro_expand
-(counts -> offsets and lineage keys), ro_batch over the ready queue for the
-dispatched children, ro_batch over the list of children sealed before
-dispatch, and ro_gather of all reports into parent slots.  Inputs
-(counts, ready queue, masks, report states, report offsets and record bytes)
-are resident in HBM before the timed region; record bytes are generated
-untimed by the generator's device fill.
+One step = the whole path over one batch of a synthetic workload, with every
+input resident in HBM before the timed region (record bytes are generated
+untimed by the generator's device fill):
 
-Prints one JSON line.  The default workload is 100,000 parents with Zipf(1.2)
-child counts truncated to [1, 10^4] (about 41.1M children) and lognormal
-16-4096-byte records (about 25 GB surviving payload).
+  zipf-single   (default) ro_expand, ro_batch over the ready queue for the
+                dispatched children, ro_batch over the children sealed before
+                dispatch, ro_gather of all reports into parent slots.
+                100,000 parents, Zipf(1.2) child counts truncated to
+                [1, 10^4] (about 41.1M children), lognormal 16-4096-byte
+                records (about 25 GB surviving payload), B = 256.
+  docs-nested   two levels: 20,000 documents -> pages -> regions, B = 512.
+  videos-nested two levels: 2,000 videos -> clips -> frames, 1,024-B frames.
+  stream-waves  10^7 children under 500,000 parents turning terminal over 50
+                waves: per wave ro_batch, ro_stream_report, ro_stream_emit.
+
+Prints one JSON line.  Children/s counts every child entity created at every
+level (pages + regions, clips + frames).
 """
 from __future__ import annotations
 
 import argparse
 import json
 import os
+import platform
 import sys
 import time
 
@@ -27,6 +34,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, published
+WORKLOADS = ("zipf-single", "docs-nested", "videos-nested", "stream-waves")
 
 
 def parse():
@@ -34,9 +42,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--parents", type=int, default=100_000, help="parents of the Zipf(1.2) workload")
-    ap.add_argument("--cpu-parents", type=int, default=100_000,
-                    help="parents in the CPU-oracle sample (same distributions; about 10 s of one core)")
+    ap.add_argument("--workload", choices=WORKLOADS, default="zipf-single")
+    ap.add_argument("--parents", type=int, default=None,
+                    help="top-level parents (default: the workload's own size)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
@@ -45,10 +53,12 @@ def parse():
     return ap.parse_args()
 
 
-# kernel whose HBM counters feed roofline.traffic, the file holding them, and
-# the source they were taken from (a changed source voids the figure)
+# kernel whose HBM counters feed roofline.traffic, the workload and file
+# holding them, and the source they were taken from (a changed source voids
+# the figure)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gather_copy_zipf41M_counters.txt")
 TRAFFIC_SOURCE = os.path.join(ROOT, "paper_2609_18703_amd", "csrc", "k_gather.hip")
+TRAFFIC_WORKLOAD = ("zipf-single", "gather_copy")
 
 
 def source_sha256(path):
@@ -102,26 +112,196 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def alg_bytes(kind, P, N, M, S):
-    """Algorithmic HBM bytes of one launch of each kernel kind.
+def cdiv(a, b):
+    return (a + b - 1) // b
 
-    P parents, N children, M dispatched children, S surviving payload bytes.
-    Reads and writes the path must do, counted once; cache-resident lookups
-    (offsets searches, per-parent atomics) are not counted.
-    """
-    nsub = (N + 1023) // 1024
+
+# ---------------------------------------------------------------- algorithmic bytes
+#
+# Reads and writes the path must do, counted once per step and per kernel
+# kind; cache-resident lookups (offsets searches, per-parent atomics, seen
+# bits) are not counted.  A kind launched several times per step sums its
+# launches.
+
+def _gather_bytes(P, N, S):
+    """One ro_gather of N reports into P parents moving S payload bytes."""
+    nsub = cdiv(N, 256)
     return {
-        "expand_scan": 12 * P + 8,                   # counts in, offsets out
-        "expand_tags": 8 * N,                        # (parent, ordinal) out
-        "batch_samples": 0,
-        "batch": None,                               # per call, see below
-        "gather_scatter": 17 * N + 16 * N + 12 * P,  # report tags/state/offsets in, canonical slot out, counters zeroed
-        "gather_scan": 16 * N + 8 * P + 8 * nsub,    # canonical slots in, slot offsets and sub-tile bases out
-        "gather_finalize": 30 * P,
-        "gather_copy": 16 * N + 8 * nsub + 2 * S,    # canonical slots + payload in and out
+        # report parent/ordinal/state/offset in, canonical 16-B slot out, counters zeroed
+        "gather_scatter": 33 * N + 12 * P,
+        # canonical slots in, parent slot offsets and sub-tile bases out
+        "gather_scan": 16 * N + 8 * P + 8 * nsub,
+        # counters and offsets in, complete and state out
+        "gather_finalize": 22 * P,
+        # canonical slots and sub-tile bases in, payload read and written
+        "gather_copy": 16 * N + 8 * nsub + 2 * S,
         "gather_reset": 0,
-    }[kind]
+    }
 
+
+def _add(acc, d):
+    for k, v in d.items():
+        acc[k] = acc.get(k, 0) + v
+    return acc
+
+
+def alg_single(P, N, M, S):
+    a = {"expand_scan": 12 * P + 8, "expand_tags": 8 * N,
+         "batch_samples": 2 * 4 * cdiv(N, 64),            # coarse child->parent map, per batch call
+         # ready queue: ids + mask in, tags of M out; sealed list: ids in, tags out
+         "batch": 5 * N + 8 * M + 12 * (N - M)}
+    return _add(a, _gather_bytes(P, N, S))
+
+
+def alg_nested(P1, N1, N2, S2, S1):
+    a = {"expand_scan": 12 * P1 + 12 * N1 + 16, "expand_tags": 8 * N1 + 8 * N2,
+         "batch_samples": 4 * cdiv(N1, 64) + 4 * cdiv(N2, 64),
+         "batch": 12 * N1 + 12 * N2}
+    _add(a, _gather_bytes(N1, N2, S2))
+    return _add(a, _gather_bytes(P1, N1, S1))
+
+
+def alg_stream(P, N, S, n_waves, emit_wave):
+    """emit_wave[p]: the wave in which parent p completes."""
+    nsub = cdiv(N, 256)
+    alive = int((emit_wave.astype(np.int64) + 1).sum())   # parent-waves a parent is still open
+    return {
+        "expand_scan": 12 * P + 8,
+        "batch_samples": n_waves * 4 * cdiv(N, 64),
+        "batch": 12 * N,                                   # wave ids in, tags out
+        "stream_report": 33 * N,                           # report in, canonical slot out
+        # per wave: emitted flags of every parent, counters of the open ones;
+        # once per parent: its emission record; virtual expansion: offsets in,
+        # per-child slot map out
+        "stream_select": n_waves * P + 20 * alive + 30 * P + 24 * P + 4 * N,
+        "stream_scan": 20 * N + 8 * P + 8 * nsub,
+        "stream_copy": 20 * N + 8 * nsub + 2 * S,
+        "stream_finish": 16 * P,
+        "misc": cdiv(N, 8) + 13 * P,                       # reset of seen bits, counters, flags
+    }
+
+
+# ---------------------------------------------------------------- workloads
+
+class Job:
+    """A staged workload: step() enqueues one step; alg maps kernel kinds to
+    algorithmic bytes per step."""
+
+    def __init__(self, name, step, children, alg, config, check, leaves=None):
+        self.name, self.step, self.children, self.alg = name, step, children, alg
+        self.config, self.check, self.leaves = config, check, leaves
+
+
+def stage_zipf(ctx, parents):
+    import torch
+    import workloads as W
+    from workloads import device as D
+    from paper_2609_18703_amd import pipeline as PL
+    c = W.config2(n_parents=parents or 100_000)
+    r = c.reports
+    P, N, M = c.n_parents, c.n_children, c.n_dispatched
+    S = int(r.off[-1])
+    log(f"[bench] zipf-single: P={P} N={N} dispatched={M} surviving bytes={S}")
+    data = torch.empty(max(S, 1), dtype=torch.uint8, device="cuda")
+    D.fill_records_dev(D.to_dev(r.seed), D.to_dev(r.off), data)
+    b = PL.SingleLevelBuffers(
+        D.to_dev(c.counts), D.to_dev(c.queue.view(np.int32)), D.to_dev(c.keep),
+        D.to_dev(c.sealed_ids.view(np.int32)), D.to_dev(r.state), D.to_dev(r.off), data, N, M,
+        c.batch_size, out_cap=S)
+    ctx.reserve(N, P, N)
+
+    def check():
+        assert int(b.out_off[P].item()) == S
+
+    cfg = {"workload": f"single-level Zipf(1.2) fan-out: {P} parents, counts truncated to [1,10000], "
+                       f"{N} children, lognormal(6,1) records clipped to [16,4096] B, 3% failed, "
+                       f"2% skipped, random ready order, B={c.batch_size}, seed 1",
+           "parents": P, "children": N, "dispatched": M, "surviving_bytes": S, "batch_size": c.batch_size}
+    return Job("zipf-single", lambda: PL.single_level(ctx, b), N, alg_single(P, N, M, S), cfg, check)
+
+
+def stage_nested(ctx, which, parents):
+    import workloads as W
+    from workloads import device as D
+    from paper_2609_18703_amd import pipeline as PL
+    if which == "docs-nested":
+        n = W.config3(n_docs=parents or 20_000)
+        desc = "two-level documents->pages->regions: {P} docs, pages lognormal(2.3,0.9) clipped to " \
+               "[1,2000], regions Poisson(8)+1, records uniform [32,1024] B, all succeed, B=512, seed 2"
+    else:
+        n = W.config4(n_videos=parents or 2_000)
+        desc = "two-level videos->clips->frames: {P} videos, clips Pareto(1.1, x_min 5) clipped to " \
+               "[1,50000], frames uniform [16,300], 1024-B frames, 1% failed, B=1024, seed 3"
+    r = n.reports
+    P1, N1, N2 = len(n.counts1), len(n.queue1), len(n.queue2)
+    S2 = int(r.off[-1])
+    log(f"[bench] {which}: top={P1} mid={N1} leaves={N2} leaf bytes={S2}")
+    data = D.reports_data_dev(r)
+    b = PL.NestedBuffers(D.to_dev(n.counts1), D.to_dev(n.queue1.view(np.int32)), n.batch1,
+                         D.to_dev(n.counts2), D.to_dev(n.queue2.view(np.int32)), n.batch2,
+                         D.to_dev(r.state), D.to_dev(r.off), data, N1, N2)
+    ctx.reserve(N2, max(N1, P1), N2)
+    # surviving bytes at the top level: mid slots whose leaves all succeeded
+    off2 = np.concatenate([[0], np.cumsum(n.counts2.astype(np.int64))])
+    ok_leaf = (n.states == W.SUCCESS)
+    lens = np.where(ok_leaf, n.lengths, 0)
+    mid_bytes = np.add.reduceat(lens, off2[:-1]) if N2 else np.zeros(N1, np.int64)
+    mid_failed = np.add.reduceat((n.states == W.FAILED).astype(np.int64), off2[:-1]) if N2 else np.zeros(N1)
+    mid_bytes = np.where(n.counts2 > 0, mid_bytes, 0)
+    mid_failed = np.where(n.counts2 > 0, mid_failed, 0)
+    S1 = int(mid_bytes[mid_failed == 0].sum())
+
+    def check():
+        assert int(b.mid_off[N1].item()) == S2 and int(b.top_off[P1].item()) == S1
+
+    cfg = {"workload": desc.format(P=P1), "top_parents": P1, "mid_children": N1, "leaf_children": N2,
+           "leaf_bytes": S2, "top_bytes": S1, "batch_size": [n.batch1, n.batch2]}
+    return Job(which, lambda: PL.nested(ctx, b), N1 + N2, alg_nested(P1, N1, N2, S2, S1), cfg, check,
+               leaves=N2)
+
+
+def stage_stream(ctx, parents):
+    import torch
+    import workloads as W
+    from workloads import device as D
+    from paper_2609_18703_amd import pipeline as PL
+    P0 = parents or 500_000
+    s = W.config5(n_parents=P0, n_children=20 * P0)
+    P, N = s.n_parents, s.n_children
+    total = int(s.wave_reports[-1].off[-1])
+    log(f"[bench] stream-waves: P={P} N={N} waves={len(s.waves)} bytes={total}")
+    arena = torch.empty(max(total, 1), dtype=torch.uint8, device="cuda")
+    for rep in s.wave_reports:
+        D.fill_records_dev(D.to_dev(rep.seed), D.to_dev(rep.off), arena)
+    b = PL.StreamingBuffers(D.to_dev(s.counts), [D.to_dev(q.view(np.int32)) for q in s.waves],
+                            [D.to_dev(rep.state) for rep in s.wave_reports],
+                            [D.to_dev(rep.off) for rep in s.wave_reports], arena, N, s.batch_size, total)
+    ctx.reserve(N, P, max(len(q) for q in s.waves))
+    ctx.expand(b.counts, b.offsets)
+    st = ctx.stream(b.offsets, N)
+    # wave in which each parent completes
+    wave_of = np.empty(N, np.int64)
+    for w, q in enumerate(s.waves):
+        wave_of[q] = w
+    offs = np.concatenate([[0], np.cumsum(s.counts.astype(np.int64))])
+    ew = np.maximum.reduceat(wave_of, offs[:-1]) if N else np.zeros(P, np.int64)
+    ew = np.where(s.counts > 0, ew, 0)
+
+    def step():
+        PL.streaming(ctx, b, st=st)
+
+    def check():
+        # the last wave emits exactly the parents completing in it
+        assert int(b.scalars[2].item()) == int((ew == len(s.waves) - 1).sum())
+
+    cfg = {"workload": f"streaming completion: {P} parents, {N} children, rank-frequency Zipf(1.1) counts "
+                       f"clipped to [1,100000], records uniform [64,512] B, all succeed, "
+                       f"{len(s.waves)} waves of {N // len(s.waves)} in random order, B={s.batch_size}, seed 4",
+           "parents": P, "children": N, "waves": len(s.waves), "bytes": total, "batch_size": s.batch_size}
+    return Job("stream-waves", step, N, alg_stream(P, N, total, len(s.waves), ew), cfg, check)
+
+
+# ---------------------------------------------------------------- main
 
 def main():
     args = parse()
@@ -134,109 +314,97 @@ def main():
         sys.exit(2)
 
     import torch
-    import workloads as W
-    from workloads import device as D
     import paper_2609_18703_amd as R
-    from paper_2609_18703_amd import pipeline as PL
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
 
     t0 = time.time()
-    c = W.config2(n_parents=args.parents)
-    r = c.reports
-    P, N, M = c.n_parents, c.n_children, c.n_dispatched
-    S = int(r.off[-1])
-    log(f"[bench] workload: P={P} N={N} dispatched={M} surviving bytes={S} (gen {time.time() - t0:.1f}s)")
-
-    data = torch.empty(max(S, 1), dtype=torch.uint8, device="cuda")
-    D.fill_records_dev(D.to_dev(r.seed), D.to_dev(r.off), data)
-    b = PL.SingleLevelBuffers(
-        D.to_dev(c.counts), D.to_dev(c.queue.view(np.int32)), D.to_dev(c.keep), D.to_dev(c.sealed_ids.view(np.int32)),
-        D.to_dev(r.state), D.to_dev(r.off), data, N, M, c.batch_size, out_cap=S)
+    ctx = R.Context()
+    if args.workload == "zipf-single":
+        job = stage_zipf(ctx, args.parents)
+    elif args.workload == "stream-waves":
+        job = stage_stream(ctx, args.parents)
+    else:
+        job = stage_nested(ctx, args.workload, args.parents)
     torch.cuda.synchronize()
     log(f"[bench] staged in HBM ({time.time() - t0:.1f}s)")
 
-    ctx = R.Context()
-    ctx.reserve(N, P, N)
     for _ in range(args.warmup):
-        PL.single_level(ctx, b)
+        job.step()
     ctx.check("warmup")
     torch.cuda.synchronize()
     log("[bench] warmup done")
 
-    # timed region: K steps on the context's (torch's current) stream
+    # timed region: K steps on the context's (torch's current) stream, one
+    # event pair per step
     ctx.trace(True)
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
-    ev0.record()
-    for _ in range(args.steps):
-        PL.single_level(ctx, b)
-    ev1.record()
+    evs[0].record()
+    for i in range(args.steps):
+        job.step()
+        evs[i + 1].record()
     torch.cuda.synchronize()
-    ms_total = ev0.elapsed_time(ev1)
+    per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
+    ms_total = evs[0].elapsed_time(evs[-1])
     kern = ctx.trace_read()
     ctx.trace(False)
     ctx.check("timed steps")
     ms_step = ms_total / args.steps
-    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step")
+    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step (median {float(np.median(per_step)):.3f}, "
+        f"min {min(per_step):.3f})")
+    job.check()
 
-    # sanity: slot offsets and counts of the last step
-    tot = int(b.out_off[P].item())
-    assert tot == S, (tot, S)
-
-    # per-kernel algorithmic rates
+    # per-kernel algorithmic rates; the dominant kernel kind is the one with
+    # the most device time
     per_kernel = {}
     total_alg = 0
     for k, (n_launch, ms) in kern.items():
-        if k == "batch":
-            # two launches per step: the ready queue (N entries in, M tags out) and
-            # the sealed list (N-M entries in, N-M tags out)
-            per_step = 5 * N + 4 * (N - M) + 8 * N
-            ab = per_step / 2
-        else:
-            ab = alg_bytes(k, P, N, M, S)
-        avg_ms = ms / n_launch
-        per_kernel[k] = {"launches_per_step": n_launch / args.steps, "avg_ms": round(avg_ms, 4),
-                         "alg_GBps": round(ab / (avg_ms * 1e-3) / 1e9, 1) if avg_ms > 0 and ab else None}
-        total_alg += ab * n_launch / args.steps
+        ab = job.alg.get(k)
+        rate = None
+        if ab and ms > 0:
+            rate = round(ab * args.steps / (ms * 1e-3) / 1e9, 1)
+            total_alg += ab
+        per_kernel[k] = {"launches_per_step": n_launch / args.steps, "avg_ms": round(ms / n_launch, 4),
+                         "ms_per_step": round(ms / args.steps, 4), "alg_GBps": rate}
     dom = max(kern.items(), key=lambda kv: kv[1][1])[0]
+    dom_launches = kern[dom][0] / args.steps
     dom_avg_ms = kern[dom][1] / kern[dom][0]
-    dom_bytes = alg_bytes(dom, P, N, M, S) if dom != "batch" else 9 * N
+    dom_bytes = job.alg.get(dom, 0) / dom_launches
     achieved = dom_bytes / (dom_avg_ms * 1e-3) / 1e9
+    value = job.children / (ms_step * 1e-3)
 
     result = {
         "metric": "children/sec through expand+batch+gather; achieved HBM GB/s vs peak",
-        "value": round(N / (ms_step * 1e-3), 1),
+        "value": round(value, 1),
         "unit": "children/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
+        "ms_per_step_median": round(float(np.median(per_step)), 4),
+        "ms_per_step_min": round(min(per_step), 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "u8",
         "data": "synthetic",
-        "config": {
-            "workload": f"single-level Zipf(1.2) fan-out: {P} parents, counts truncated to [1,10000], "
-                        f"{N} children, lognormal(6,1) records clipped to [16,4096] B, 3% failed, "
-                        f"2% skipped, random ready order, B={c.batch_size}, seed 1",
-            "parents": P, "children": N, "dispatched": M, "surviving_bytes": S,
-            "batch_size": c.batch_size,
-        },
+        "config": job.config,
         "roofline": {
             "bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
             "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": traffic_from_profile() if dom == "gather_copy" else None,
-            "alg_bytes_per_launch": dom_bytes, "avg_launch_ms": round(dom_avg_ms, 4),
+            "traffic": traffic_from_profile() if (job.name, dom) == TRAFFIC_WORKLOAD else None,
+            "alg_bytes_per_launch": int(dom_bytes), "avg_launch_ms": round(dom_avg_ms, 4),
+            "launches_per_step": dom_launches,
         },
         "step_alg_GBps": round(total_alg / (ms_step * 1e-3) / 1e9, 1),
         "step_frac_of_peak": round(total_alg / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
         "kernels": per_kernel,
     }
+    if job.leaves is not None:
+        result["leaf_children_per_s"] = round(job.leaves / (ms_step * 1e-3), 1)
 
     if args.calib_copy_mib:
         n = args.calib_copy_mib << 20
@@ -254,44 +422,90 @@ def main():
         result["calib_copy"] = {"bytes": n, "avg_ms": round(ms, 4), "GBps": round(2 * n / (ms * 1e-3) / 1e9, 1)}
         del src, dst
 
-    del b, data
+    del job
     torch.cuda.empty_cache()
 
     if not args.no_cpu:
-        result["cpu_baseline"] = cpu_baseline(args.cpu_parents)
+        result["cpu_baseline"] = cpu_baseline(args.workload)
 
     print(json.dumps(result), flush=True)
 
 
-def cpu_baseline(n_parents):
-    """The oracle, single threaded, on a bounded sample of the same workload."""
+def _cpu_info():
+    model = platform.processor() or ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return model, os.cpu_count()
+
+
+def cpu_baseline(workload):
+    """The oracle, single threaded, on a bounded sample of the workload
+    (about 10-30 s of one core): the same distributions at a smaller size
+    where the full one would take longer."""
     import torch
     import oracle as O
     import workloads as W
     from workloads import device as D
 
-    c = W.config2(n_parents=n_parents)
-    r = c.reports
-    S = int(r.off[-1])
-    dev = torch.empty(max(S, 1), dtype=torch.uint8, device="cuda")
-    D.fill_records_dev(D.to_dev(r.seed), D.to_dev(r.off), dev)
-    data = dev.cpu().numpy()
-    del dev
     L = O.lib()
-    t = time.perf_counter()
-    offs, cp, co = O.expand(c.counts, L=L)
-    b1 = O.batch(c.queue, c.keep, offs, c.batch_size, L=L)
-    b2 = O.batch(c.sealed_ids, None, offs, c.batch_size, L=L)
-    par = np.concatenate([b1[1], b2[1]])
-    ordi = np.concatenate([b1[2], b2[2]])
-    g = O.gather(par, ordi, r.state, r.off, data, offs, L=L)
-    dt = time.perf_counter() - t
-    assert int(g["out_off"][-1]) == S
-    log(f"[bench] cpu oracle: {c.n_children} children in {dt:.2f}s")
-    return {"value": round(c.n_children / dt, 1), "unit": "children/s", "cores": 1, "kind": "oracle",
-            "sample": f"same distributions with {n_parents} parents: {c.n_children} children, "
-                      f"{S} surviving bytes; expand + 2 batches + gather, single thread",
-            "seconds": round(dt, 2)}
+    if workload == "zipf-single":
+        n_parents = 100_000
+        c = W.config2(n_parents=n_parents)
+        r = c.reports
+        S = int(r.off[-1])
+        dev = torch.empty(max(S, 1), dtype=torch.uint8, device="cuda")
+        D.fill_records_dev(D.to_dev(r.seed), D.to_dev(r.off), dev)
+        data = dev.cpu().numpy()
+        del dev
+        t = time.perf_counter()
+        offs, cp, co = O.expand(c.counts, L=L)
+        b1 = O.batch(c.queue, c.keep, offs, c.batch_size, L=L)
+        b2 = O.batch(c.sealed_ids, None, offs, c.batch_size, L=L)
+        par = np.concatenate([b1[1], b2[1]])
+        ordi = np.concatenate([b1[2], b2[2]])
+        g = O.gather(par, ordi, r.state, r.off, data, offs, L=L)
+        dt = time.perf_counter() - t
+        assert int(g["out_off"][-1]) == S
+        n_child = c.n_children
+        sample = (f"the full workload ({n_parents} parents: {n_child} children, {S} surviving bytes); "
+                  f"expand + 2 batches + gather")
+    elif workload in ("docs-nested", "videos-nested"):
+        n = W.config3() if workload == "docs-nested" else W.config4(n_videos=300)
+        r = n.reports
+        data = r.data()
+        t = time.perf_counter()
+        want = O.nested(n.counts1, n.queue1, None, n.batch1, n.counts2, n.queue2, None, n.batch2,
+                        r.state, r.off, data, L=L)
+        dt = time.perf_counter() - t
+        assert int(want["low"]["out_off"][-1]) == int(r.off[-1])
+        n_child = len(n.queue1) + len(n.queue2)
+        sample = (f"{len(n.counts1)} top parents, {len(n.queue1)} + {len(n.queue2)} children, "
+                  f"{int(r.off[-1])} leaf bytes; expand, batch, expand, batch, gather, gather")
+    else:
+        s = W.config5(n_parents=100_000, n_children=2_000_000)
+        arena = np.concatenate([rep.data() for rep in s.wave_reports] + [np.zeros(1, np.uint8)])
+        t = time.perf_counter()
+        offs = O.expand(s.counts, tags=False, L=L)
+        st = O.Stream(offs, L=L)
+        for q, rep in zip(s.waves, s.wave_reports):
+            _, par, ordi, _ = O.batch(q, None, offs, s.batch_size, L=L)
+            st.report(par, ordi, rep.state, rep.off, arena)
+            st.emit()
+        st.close()
+        dt = time.perf_counter() - t
+        n_child = s.n_children
+        sample = (f"{s.n_parents} parents, {n_child} children over {len(s.waves)} waves "
+                  f"(same distributions, a fifth of the size); expand + per wave batch, report, emit")
+    model, ncpu = _cpu_info()
+    log(f"[bench] cpu oracle: {n_child} children in {dt:.2f}s")
+    return {"value": round(n_child / dt, 1), "unit": "children/s", "cores": 1, "kind": "oracle",
+            "sample": sample + ", single thread", "seconds": round(dt, 2), "cpu_model": model,
+            "host_cpus": ncpu}
 
 
 if __name__ == "__main__":

@@ -188,6 +188,15 @@ int ro_stream_emit(ro_ctx *ctx, ro_stream *s, uint32_t *emit_parent, int64_t *em
                    int32_t *n_success, int32_t *n_failed, int32_t *n_skipped,
                    uint8_t *parent_state, int64_t *n_emitted_dev, int64_t *n_bytes_dev);
 
+/* Start the stream over for a new run on the same expansion (same offsets
+ * buffer, same P and N; the offsets may be rewritten in between): every
+ * report, count and emission is forgotten, the allocation is kept.
+ * Stream-ordered like the other calls, allocates nothing and enqueues no
+ * memset node.  A new Call over a parent batch of the same shape (Sec. 4,
+ * per-Call queue) then reuses the state instead of creating it again.
+ * RO_EINVAL if s belongs to another context. */
+int ro_stream_reset(ro_ctx *ctx, ro_stream *s);
+
 int ro_stream_destroy(ro_stream *s);
 
 #ifdef __cplusplus

@@ -15,10 +15,11 @@
 //              aggregated), per-sub-tile output bases.
 //   finalize : per parent: complete / state, trailing slot offsets, duplicate
 //              and capacity checks.
-//   copy     : per sub-tile of 1024 canonical children, a workgroup rebuilds
-//              the destination offsets in LDS and writes its contiguous output
-//              window as aligned 16-byte stores; sources are byte-aligned
-//              records read as aligned 16-byte pairs and realigned in registers.
+//   copy     : the output is cut into byte ranges of equal size; per range,
+//              a wave rebuilds the destination offsets of the canonical
+//              sub-tiles it overlaps and writes the range as aligned 16-byte
+//              stores; sources are byte-aligned records read as aligned
+//              16-byte pairs and realigned in registers.
 #include "ro_device.h"
 
 namespace ro {
@@ -81,8 +82,9 @@ __global__ __launch_bounds__(kBlock) void k_gather_scatter(
 }
 
 // ---------------------------------------------------------------- scan
-// One tile = 4096 canonical children, 16 consecutive per thread; a wave
-// covers exactly one copy sub-tile (1024 children).
+// One tile = 4096 canonical children, 16 consecutive per thread; every 16
+// threads cover one copy sub-tile of 256 children and record its first output
+// byte.
 //
 // The same kernel serves the streaming emission: there the "parents" are the
 // parents emitted by this call (their count P only known on the device, read
@@ -396,7 +398,7 @@ __device__ __forceinline__ void store_partial(uint64_t A, const uint4 &v, int b0
     for (int b = b0; b < b1; ++b) st8(A + (uint64_t)b, (uint8_t)(dword_of(v, b >> 2) >> (8 * (b & 3))));
 }
 
-// A sub-tile whose output window is under 2 GiB: positions relative to the
+// One unit's window of a sub-tile (at most 1 GiB): positions relative to the
 // window start fit in 32 bits.  The wave sweeps its window 1 KiB at a time,
 // lane `lane` taking chunk 64*g + lane, so the record each lane reads from
 // only moves forward.  Every chunk strictly inside the window is written with
@@ -442,36 +444,50 @@ __device__ __forceinline__ void copy_window32(const int32_t *s_dst, const uint64
     }
 }
 
-// A sub-tile with an output window of 2 GiB or more (records of megabytes):
-// one record at a time across the wave, 64-bit positions, edges bytewise.
-__device__ __forceinline__ void copy_records64(const int64_t *s_dst, const uint64_t *s_src, uint64_t outa,
-                                               int64_t D0, int lane)
+// First sub-tile whose output holds byte `lo`: the largest s in [0, nsub)
+// with sub_base[s] <= lo (sub_base[0] = 0).  Each round, the 64 lanes probe
+// 64 evenly spaced entries of the remaining range and a ballot keeps the gap
+// that holds the answer, so a range of n entries takes about log_65(n) rounds
+// of one load each.
+__device__ __forceinline__ int64_t find_sub_tile(const int64_t *__restrict__ sub_base, int64_t nsub, int64_t lo,
+                                                 int lane)
 {
-    for (int r = 0; r < kSub; ++r) {
-        const int64_t L = s_dst[r + 1] - s_dst[r];
-        if (L <= 0) continue;
-        const uint64_t D = outa + (uint64_t)(D0 + s_dst[r]);
-        const uint64_t a0 = D & ~(uint64_t)15, a1 = (D + (uint64_t)L - 1) & ~(uint64_t)15;
-        const int64_t nch = (int64_t)((a1 - a0) >> 4) + 1;
-        for (int64_t k = lane; k < nch; k += 64) {
-            const uint64_t A = a0 + ((uint64_t)k << 4);
-            const int64_t x = (int64_t)(A - D);               // chunk start, relative to the record
-            const int64_t lo = x > 0 ? x : 0;
-            const int64_t hi = min64(x + 16, L);
-            Piece p;
-            piece_load(p, s_src[r] + (uint64_t)x, (int)(lo - x), (int)(hi - 1 - x));
-            uint4 acc = make_uint4(0u, 0u, 0u, 0u);
-            piece_merge(acc, p);
-            if (lo == x && hi == x + 16) st16(A, acc);
-            else store_partial(A, acc, (int)(lo - x), (int)(hi - x));
-        }
+    int64_t l = 0, h = nsub;
+    while (h - l > 1) {
+        const int64_t idx = l + ((h - l) * (int64_t)(lane + 1)) / 65;
+        const bool le = sub_base[idx] <= lo;
+        const uint64_t m = __ballot(le);
+        const int k = __popcll(m);                 // the true probes form a prefix
+        const int64_t nl = k > 0 ? __shfl(idx, k - 1, 64) : l;
+        const int64_t nh = k < 64 ? __shfl(idx, k, 64) : h;
+        l = nl;
+        h = nh;
     }
+    return l;
 }
 
-// Each wave works alone on one sub-tile of kSub canonical children at a time:
-// it rebuilds the sub-tile's destination offsets with a wave scan into its own
-// LDS slice, then writes the sub-tile's contiguous output window.  No
-// workgroup barrier is involved, so waves never wait for one another.
+// Output bytes are split into units of G bytes (the last one shorter), cut
+// where the destination address is 16-byte aligned, so that unit edges need
+// no partial stores.  G is chosen from the total so that every wave of the
+// grid gets about kCopyUnits units, but never under kCopyMinUnit bytes (a
+// unit re-reads the slot descriptors of the sub-tiles it touches) nor over
+// 1 GiB (positions inside a unit are 32-bit).
+#ifndef RO_COPY_UNITS
+#define RO_COPY_UNITS 2
+#endif
+#ifndef RO_COPY_MIN_UNIT
+#define RO_COPY_MIN_UNIT 16384
+#endif
+constexpr int64_t kCopyUnits = RO_COPY_UNITS;
+constexpr int64_t kCopyMinUnit = RO_COPY_MIN_UNIT;
+
+// Each wave works alone on its units of output bytes, with no workgroup
+// barrier.  For each sub-tile of kSub canonical children that a unit touches,
+// it rebuilds the destination offsets with a wave scan, clips every record to
+// the unit's byte range (shifting the source start of a record that begins
+// before it), and writes that range with aligned 16-byte stores.  Byte-sized
+// units keep the chip busy whether the records are a few bytes or megabytes
+// long, and few parents or many.
 #ifndef RO_COPY_WAVES
 #define RO_COPY_WAVES 4
 #endif
@@ -483,61 +499,70 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_
     constexpr int kWaves = kBlock / 64;
     const int64_t P = P_dev ? *P_dev : P_arg;
     const uint32_t epoch = epoch_arg ? epoch_arg : ctl->canon_epoch;
-    __shared__ int64_t s_dst_all[kWaves][kSub + 1];     // destination offset of each record, relative
-    __shared__ int32_t s_dst32_all[kWaves][kSub + 1];   // the same, when the window is under 2 GiB
-    __shared__ uint64_t s_src_all[kWaves][kSub];
+    __shared__ int32_t s_dst_all[kWaves][kSub + 1];     // clipped destination offset of each record
+    __shared__ uint64_t s_src_all[kWaves][kSub];        // source address of its first clipped byte
     if (read_err(ctl) != 0) return;                      // any recorded error: copy nothing
     const int64_t N0 = offsets[P];
     const int64_t N = N0 <= canon_cap ? N0 : 0;
+    const int64_t T = N > 0 ? ctl->total : 0;           // output bytes, from the scan
+    if (T <= 0) return;
     const int64_t nsub = (N + kSub - 1) / kSub;
     const uint64_t outa = reinterpret_cast<uint64_t>(out);
+    const int64_t mis = (int64_t)(outa & 15);
+    const int64_t nwaves = (int64_t)gridDim.x * kWaves;
+    int64_t G = (T + nwaves * kCopyUnits - 1) / (nwaves * kCopyUnits);
+    G = (G + 1023) & ~(int64_t)1023;
+    G = G < kCopyMinUnit ? kCopyMinUnit : (G > ((int64_t)1 << 30) ? ((int64_t)1 << 30) : G);
+    const int64_t nunits = (T + mis + G - 1) / G;
     const int wave = (int)(threadIdx.x >> 6), lane = lane_id();
-    int64_t *s_dst = s_dst_all[wave];
-    int32_t *s_dst32 = s_dst32_all[wave];
+    int32_t *s_dst = s_dst_all[wave];
     uint64_t *s_src = s_src_all[wave];
-    for (int64_t sb = (int64_t)blockIdx.x * kWaves + wave; sb < nsub; sb += (int64_t)gridDim.x * kWaves) {
-        const int64_t c0 = sb * kSub;
-        const int64_t cnt = min64(kSub, N - c0);
-        // prologue: surviving lengths -> relative destination offsets
-        int64_t lsum = 0;
-        uint32_t l[kCopyPer];
-        uint64_t s[kCopyPer];
-#pragma unroll
-        for (int k = 0; k < kCopyPer; ++k) {
-            const int64_t r = (int64_t)lane * kCopyPer + k;
-            l[k] = 0;
-            s[k] = 0;
-            if (r < cnt) {
-                const Canon e = canon[vmap ? (int64_t)vmap[c0 + r] : c0 + r];
-                if (e.tag == ((epoch << 2) | RO_SUCCESS)) {
-                    l[k] = e.len;
-                    s[k] = e.src;
-                }
-            }
-            lsum += l[k];
-        }
-        const int64_t inc = wave_incl_sum(lsum);
-        const int64_t tot = __shfl(inc, 63, 64);
-        int64_t run = inc - lsum;
-#pragma unroll
-        for (int k = 0; k < kCopyPer; ++k) {
-            const int r = lane * kCopyPer + k;
-            s_dst[r] = run;
-            s_dst32[r] = (int32_t)run;
-            s_src[r] = s[k];
-            run += l[k];
-        }
-        if (lane == 0) {
-            s_dst[kSub] = tot;
-            s_dst32[kSub] = (int32_t)tot;
-        }
-        __builtin_amdgcn_wave_barrier();
-        if (tot > 0) {
+    for (int64_t u = (int64_t)blockIdx.x * kWaves + wave; u < nunits; u += nwaves) {
+        const int64_t lo = max64(u * G - mis, 0);
+        const int64_t hi = min64((u + 1) * G - mis, T);
+        for (int64_t sb = find_sub_tile(sub_base, nsub, lo, lane); sb < nsub; ++sb) {
             const int64_t D0 = sub_base[sb];
-            if (tot < ((int64_t)1 << 31)) copy_window32(s_dst32, s_src, (int)tot, outa, D0, lane);
-            else copy_records64(s_dst, s_src, outa, D0, lane);
+            if (D0 >= hi) break;
+            const int64_t c0 = sb * kSub;
+            const int64_t cnt = min64(kSub, N - c0);
+            // surviving lengths -> destination offsets relative to the sub-tile
+            int64_t lsum = 0;
+            uint32_t l[kCopyPer];
+            uint64_t s[kCopyPer];
+#pragma unroll
+            for (int k = 0; k < kCopyPer; ++k) {
+                const int64_t r = (int64_t)lane * kCopyPer + k;
+                l[k] = 0;
+                s[k] = 0;
+                if (r < cnt) {
+                    const Canon e = canon[vmap ? (int64_t)vmap[c0 + r] : c0 + r];
+                    if (e.tag == ((epoch << 2) | RO_SUCCESS)) {
+                        l[k] = e.len;
+                        s[k] = e.src;
+                    }
+                }
+                lsum += l[k];
+            }
+            const int64_t inc = wave_incl_sum(lsum);
+            const int64_t tot = __shfl(inc, 63, 64);
+            // this unit's part of the sub-tile: [ws, we), relative to D0
+            const int64_t ws = max64(lo - D0, 0), we = min64(hi - D0, tot);
+            if (we > ws) {
+                int64_t run = inc - lsum;
+#pragma unroll
+                for (int k = 0; k < kCopyPer; ++k) {
+                    const int r = lane * kCopyPer + k;
+                    const int64_t cs = min64(max64(run, ws), we);
+                    s_dst[r] = (int32_t)(cs - ws);
+                    s_src[r] = s[k] + (uint64_t)(cs - run);
+                    run += l[k];
+                }
+                if (lane == 0) s_dst[kSub] = (int32_t)(we - ws);
+                __builtin_amdgcn_wave_barrier();
+                copy_window32(s_dst, s_src, (int)(we - ws), outa, D0 + ws, lane);
+                __builtin_amdgcn_wave_barrier();
+            }
         }
-        __builtin_amdgcn_wave_barrier();
     }
 }
 

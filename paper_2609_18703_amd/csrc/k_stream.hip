@@ -228,6 +228,26 @@ __global__ void k_stream_finish(Ctl *ctl)
     }
 }
 
+// Forgets every report and emission: seen bits, per-parent counters and
+// emitted flags back to zero.  Canonical slots need no clearing, since a slot
+// is read only for children of emitted parents, and those were all reported.
+__global__ void k_stream_clear(uint32_t *__restrict__ seen, int64_t n_seen, int32_t *__restrict__ cnt,
+                               int64_t n_cnt, uint8_t *__restrict__ emitted, int64_t n_emitted)
+{
+    const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = g; i < n_seen; i += stride) seen[i] = 0;
+    for (int64_t i = g; i < n_cnt; i += stride) cnt[i] = 0;
+    for (int64_t i = g; i < n_emitted; i += stride) emitted[i] = 0;
+}
+
+hipError_t launch_stream_reset(const Launch &L, StreamState &s)
+{
+    RO_LAUNCH(L, RO_K_MISC, k_stream_clear, dim3((unsigned)L.num_cus * 4), dim3(256), 0, L.stream, s.seen,
+              (s.N + 31) / 32 + 1, s.cnt, 3 * s.P + 1, s.emitted, s.P + 1);
+    return launch_stream_init(L, s);
+}
+
 hipError_t launch_stream_init(const Launch &L, StreamState &s)
 {
     RO_LAUNCH(L, RO_K_MISC, k_stream_check, dim3((unsigned)L.num_cus), dim3(256), 0, L.stream, s.offsets, s.P,

@@ -426,6 +426,12 @@ int ro_stream_emit(ro_ctx *c, ro_stream *s, uint32_t *emit_parent, int64_t *emit
                                        n_bytes_dev));
 }
 
+int ro_stream_reset(ro_ctx *c, ro_stream *s)
+{
+    if (!c || !s || s->ctx != c) return RO_EINVAL;
+    return hip_fail(launch_stream_reset(launch_of(c), s->st));
+}
+
 int ro_stream_destroy(ro_stream *s)
 {
     if (!s) return RO_EINVAL;

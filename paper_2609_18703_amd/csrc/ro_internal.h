@@ -122,6 +122,7 @@ struct StreamState {
 };
 
 hipError_t launch_stream_init(const Launch &L, StreamState &s);
+hipError_t launch_stream_reset(const Launch &L, StreamState &s);
 hipError_t launch_stream_report(const Launch &L, StreamState &s, const uint32_t *rp,
                                 const uint32_t *ro, const uint8_t *rs, const int64_t *roff,
                                 const uint8_t *data, int64_t n);

@@ -148,15 +148,21 @@ class StreamingBuffers:
         self.emit_state = _empty(P, torch.uint8)
 
 
-def streaming(ctx, b: StreamingBuffers, on_wave=None):
+def streaming(ctx, b: StreamingBuffers, on_wave=None, st=None):
     """expand once; per wave: batch -> stream report -> stream emit.
 
     ``on_wave(w)`` (optional) runs after each wave's emission is enqueued, to
-    consume that wave's outputs before the next wave overwrites them.
+    consume that wave's outputs before the next wave overwrites them.  ``st``
+    (optional) is a stream created earlier over ``b.offsets``: it is reset and
+    reused instead of creating one for this run.
     """
     P = b.P
     ctx.expand(b.counts, b.offsets)
-    st = ctx.stream(b.offsets, b.N)
+    own = st is None
+    if own:
+        st = ctx.stream(b.offsets, b.N)
+    else:
+        st.reset()
     try:
         for w, q in enumerate(b.queues):
             n = q.numel()
@@ -169,4 +175,5 @@ def streaming(ctx, b: StreamingBuffers, on_wave=None):
             if on_wave is not None:
                 on_wave(w)
     finally:
-        st.close()
+        if own:
+            st.close()

@@ -66,12 +66,13 @@ def load(path=None):
     L.ro_stream_create.argtypes = [P, P, i64, i64, pp]
     L.ro_stream_report.argtypes = [P, P, C.POINTER(ReportsT)]
     L.ro_stream_emit.argtypes = [P, P, P, P, P, i64, i64, P, P, P, P, P, P]
+    L.ro_stream_reset.argtypes = [P, P]
     L.ro_stream_destroy.argtypes = [P]
     L.ro_ctx_trace.argtypes = [P, C.c_int]
     L.ro_ctx_trace_read.argtypes = [P, P, P, i32]
     for name in ("ro_ctx_trace", "ro_ctx_trace_read", "ro_ctx_create", "ro_ctx_set_stream", "ro_ctx_reserve", "ro_ctx_status",
                  "ro_ctx_destroy", "ro_expand", "ro_batch", "ro_gather", "ro_stream_create",
-                 "ro_stream_report", "ro_stream_emit", "ro_stream_destroy"):
+                 "ro_stream_report", "ro_stream_emit", "ro_stream_reset", "ro_stream_destroy"):
         getattr(L, name).restype = C.c_int
     if path == LIB_PATH:
         _lib = L
@@ -204,6 +205,10 @@ class Stream:
                                          _ptr(n_success), _ptr(n_failed), _ptr(n_skipped),
                                          _ptr(parent_state), _ptr(n_emitted), _ptr(n_bytes)),
                "ro_stream_emit")
+
+    def reset(self):
+        """Forget every report and emission (stream-ordered; keeps the allocation)."""
+        _check(self.ctx.L.ro_stream_reset(self.ctx.h, self.h), "ro_stream_reset")
 
     def close(self):
         if getattr(self, "h", None):

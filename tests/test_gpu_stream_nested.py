@@ -86,9 +86,10 @@ def test_nested_canonical_order(ctx):
 
 
 # ------------------------------------------------------------------ streaming
-def _stream_case(ctx, counts, waves, B=64):
+def _stream_case(ctx, counts, waves, B=64, runs=1):
     """waves: list of (child ids, states, lengths); all reports of a wave are in
-    its queue order; bytes of every wave live in one arena."""
+    its queue order; bytes of every wave live in one arena.  With runs > 1 the
+    whole stream is replayed on one stream state, reset between runs."""
     from paper_2609_18703_amd import pipeline as PL
     counts = np.asarray(counts, np.int32)
     offs = O.expand(counts, tags=False)
@@ -126,10 +127,17 @@ def _stream_case(ctx, counts, waves, B=64):
                         data=b.emit_data.cpu().numpy()[:nb], ns=b.emit_cnt.cpu().numpy()[:E],
                         nf=b.emit_cnt.cpu().numpy()[P:P + E], nk=b.emit_cnt.cpu().numpy()[2 * P:2 * P + E],
                         state=b.emit_state.cpu().numpy()[:E], nbytes=nb))
-    PL.streaming(ctx, b, on_wave)
+    if runs == 1:
+        PL.streaming(ctx, b, on_wave)
+    else:
+        ctx.expand(b.counts, b.offsets)          # the stream validates its offsets when created
+        st = ctx.stream(b.offsets, N)
+        for _ in range(runs):
+            PL.streaming(ctx, b, on_wave, st=st)
+        st.close()
     ctx.check("stream")
-    assert len(got) == len(want)
-    for w, (g, o) in enumerate(zip(got, want)):
+    assert len(got) == runs * len(want)
+    for w, (g, o) in enumerate(zip(got, want * runs)):
         assert np.array_equal(g["parent"], o["parent"]), w
         assert np.array_equal(g["off"], o["off"]), w
         assert g["nbytes"] == o["n_bytes"], w
@@ -144,6 +152,24 @@ def test_stream_config5_shape(ctx):
     waves = [(q, r.state, np.diff(r.off)) for q, r in zip(s.waves, s.wave_reports)]
     _say("stream config5-shaped", len(waves))
     _stream_case(ctx, s.counts, waves, B=s.batch_size)
+
+
+def test_stream_reset_replays(ctx):
+    """A reset stream forgets every report and emission: three runs over one
+    stream state give the oracle's emissions each time (empty parents are
+    emitted again by each run's first call)."""
+    rng = np.random.default_rng(21)
+    counts = rng.integers(0, 9, 4000).astype(np.int32)
+    N = int(counts.sum())
+    parts = np.split(rng.permutation(N).astype(np.uint32), [N // 3, N // 2])
+    waves = [(ids, rng.choice(np.array([0, 0, 1, 2], np.uint8), len(ids)),
+              rng.integers(1, 200, len(ids)).astype(np.int64)) for ids in parts]
+    _say("stream reset replays", [len(p) for p in parts])
+    got = _stream_case(ctx, counts, waves, B=100, runs=3)
+    empties = set(np.flatnonzero(counts == 0).tolist())
+    assert empties
+    for r in range(3):
+        assert empties <= set(got[r * len(waves)]["parent"].tolist()), r
 
 
 @pytest.mark.parametrize("seed", [0, 1, 2])

@@ -141,6 +141,58 @@ __global__ __launch_bounds__(kBlock) void k_batch(
     ticket_done(ctl, epoch, desc, desc_cap, &s_last);
 }
 
+// Every queue entry is ready (no mask): the FIFO compaction is the identity,
+// slot i holds queue[i], so no scan is needed and each entry is independent.
+// A block takes 1024 consecutive entries, lane-contiguous, so every load and
+// store instruction of a wave covers 256 contiguous bytes.
+constexpr int kAllPer = 4;
+
+__global__ __launch_bounds__(kBlock) void k_batch_all(
+    const uint32_t *__restrict__ queue, int64_t Q, const int64_t *__restrict__ offsets, int64_t P,
+    const uint32_t *__restrict__ cmap, int64_t cmap_cap, int32_t B, uint32_t *__restrict__ out_child,
+    uint32_t *__restrict__ out_parent, uint32_t *__restrict__ out_ordinal, int64_t out_cap, int64_t *n_out,
+    int64_t *n_batches, Ctl *ctl)
+{
+    const int64_t N = offsets[P];
+    int64_t nmap = (N + (1 << kCmapShift) - 1) >> kCmapShift;
+    nmap = nmap < cmap_cap ? nmap : cmap_cap;
+    const bool want_tags = out_parent != nullptr || out_ordinal != nullptr;
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        if (Q > out_cap) raise_err(ctl, RO_ECAP);
+        if (n_out) *n_out = Q;
+        if (n_batches) *n_batches = (Q + B - 1) / B;
+    }
+    const int64_t lim = Q < out_cap ? Q : out_cap;
+    bool bad_range = false;
+    for (int64_t i0 = (int64_t)blockIdx.x * (kBlock * kAllPer); i0 < Q;
+         i0 += (int64_t)gridDim.x * (kBlock * kAllPer)) {
+        uint32_t q[kAllPer];
+#pragma unroll
+        for (int k = 0; k < kAllPer; ++k) {
+            const int64_t i = i0 + k * kBlock + threadIdx.x;
+            q[k] = i < Q ? queue[i] : 0u;
+        }
+#pragma unroll
+        for (int k = 0; k < kAllPer; ++k) {
+            const int64_t i = i0 + k * kBlock + threadIdx.x;
+            if (i >= Q) continue;
+            const int64_t c = q[k];
+            if (c >= N) {
+                bad_range = true;
+                continue;
+            }
+            if (i >= lim) continue;
+            if (out_child) out_child[i] = q[k];
+            if (want_tags) {
+                const int64_t p = parent_of(cmap, nmap, offsets, P, c);
+                if (out_parent) out_parent[i] = (uint32_t)p;
+                if (out_ordinal) out_ordinal[i] = (uint32_t)(c - offsets[p]);
+            }
+        }
+    }
+    if (bad_range) raise_err(ctl, RO_ERANGE);
+}
+
 hipError_t launch_batch(const Launch &L, const uint32_t *queue, const uint8_t *keep,
                         int64_t Q, const int64_t *offsets, int64_t P, int32_t B,
                         uint32_t *out_child, uint32_t *out_parent, uint32_t *out_ordinal,
@@ -151,6 +203,14 @@ hipError_t launch_batch(const Launch &L, const uint32_t *queue, const uint8_t *k
         const int64_t grid_m = (int64_t)L.num_cus * 4;
         RO_LAUNCH(L, RO_K_BATCH_SAMPLES, k_batch_cmap, dim3((unsigned)grid_m), dim3(256), 0, L.stream,
                   offsets, P, cmap, cmap_cap);
+    }
+    if (keep == nullptr) {
+        int64_t grid_a = (Q + kBlock * kAllPer - 1) / (kBlock * kAllPer);
+        grid_a = grid_a < 1 ? 1 : (grid_a > (int64_t)L.num_cus * 8 ? (int64_t)L.num_cus * 8 : grid_a);
+        RO_LAUNCH(L, RO_K_BATCH, k_batch_all, dim3((unsigned)grid_a), dim3(kBlock), 0, L.stream, queue, Q,
+                  offsets, P, cmap, cmap_cap, B, out_child, out_parent, out_ordinal, out_cap, n_out, n_batches,
+                  L.ctl);
+        return hipGetLastError();
     }
     const int64_t ntiles = Q > 0 ? (Q + kTile - 1) / kTile : 1;
     const int64_t cap_grid = (int64_t)L.num_cus * 4;

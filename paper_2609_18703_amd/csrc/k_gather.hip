@@ -476,7 +476,7 @@ __device__ __forceinline__ int64_t find_sub_tile(const int64_t *__restrict__ sub
 #define RO_COPY_UNITS 2
 #endif
 #ifndef RO_COPY_MIN_UNIT
-#define RO_COPY_MIN_UNIT 16384
+#define RO_COPY_MIN_UNIT 4096
 #endif
 constexpr int64_t kCopyUnits = RO_COPY_UNITS;
 constexpr int64_t kCopyMinUnit = RO_COPY_MIN_UNIT;
@@ -594,12 +594,13 @@ hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w
 // The streaming emission's pass over its virtual expansion (emitted parents'
 // children): byte scan into emitted slot offsets, then the ordered copy.
 hipError_t launch_virtual_scan(const Launch &L, const int64_t *voff, const int64_t *E_dev, const uint32_t *vmap,
-                               const Canon *canon, int64_t canon_cap, int64_t *emit_off, int64_t *sub_base)
+                               const Canon *canon, int64_t canon_cap, int64_t *emit_off, int32_t *ns,
+                               int32_t *nf, int32_t *nk, int64_t *sub_base)
 {
     const int64_t grid_s = (int64_t)L.num_cus * 4;
     RO_LAUNCH(L, RO_K_STREAM_SCAN, k_gather_scan, dim3((unsigned)grid_s), dim3(kBlock), 0, L.stream, voff,
-              (int64_t)0, E_dev, vmap, 1u, canon, canon_cap, emit_off, (int32_t *)nullptr, (int32_t *)nullptr,
-              (int32_t *)nullptr, sub_base, L.ctl, L.desc, L.desc_cap);
+              (int64_t)0, E_dev, vmap, 1u, canon, canon_cap, emit_off, ns, nf, nk, sub_base, L.ctl, L.desc,
+              L.desc_cap);
     return hipGetLastError();
 }
 

@@ -11,7 +11,7 @@ namespace ro {
 constexpr int kBlock = 256;                 // threads per workgroup (4 waves of 64)
 constexpr int kItems = 16;                  // items per thread in scan tiles
 constexpr int kTile = kBlock * kItems;      // 4096 entries per scan tile
-constexpr int kSub = 256;                   // children per copy sub-tile (one wave's unit of work)
+constexpr int kSub = 256;                   // children per copy sub-tile (the scan records where each starts)
 constexpr int kCntLds = 1024;               // parents aggregated in LDS per tile
 
 // Canonical per-child record written by the report scatter.  `tag` holds the
@@ -111,16 +111,19 @@ struct StreamState {
     int64_t P, N;
     Canon *canon;            // [N] accepted reports (tag epoch 1 = accepted)
     uint32_t *seen;          // [N/32] duplicate detection bitmap
-    int32_t *cnt;            // [3*P] per-parent SUCCESS / FAILED / SKIPPED counts
+    int32_t *cnt;            // [P+1] reports per parent (parents with few children)
+    int32_t *big;            // [stream_big_size(N)] spread report counters of large parents
     uint8_t *emitted;        // [P]
     uint32_t *elist;         // [P] emitted parents of the current emission
-    int64_t *ekids;          // [P] their child counts
     int64_t *evoff;          // [P+1] child offsets of the emitted parents (virtual children)
+    int32_t *ecnt;           // [3*(P+1)] SUCCESS / FAILED / SKIPPED counts per emitted parent
     uint32_t *vmap;          // [N] canonical slot of each virtual child
     int64_t *sub_base;       // per sub-tile of virtual children
     int64_t sub_cap;
 };
 
+int64_t stream_big_size(int64_t N);
+int64_t stream_desc_tiles(int64_t P, int64_t N);
 hipError_t launch_stream_init(const Launch &L, StreamState &s);
 hipError_t launch_stream_reset(const Launch &L, StreamState &s);
 hipError_t launch_stream_report(const Launch &L, StreamState &s, const uint32_t *rp,

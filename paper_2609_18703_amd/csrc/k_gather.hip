@@ -82,6 +82,27 @@ __global__ __launch_bounds__(kBlock) void k_gather_scatter(
 }
 
 // ---------------------------------------------------------------- scan
+// Searches over the tile-relative parent offsets held in LDS.
+// Largest i in [lo, hi) with a[i] <= x, given a[lo] <= x.
+__device__ __forceinline__ int lds_last_le(const int16_t *a, int lo, int hi, int x)
+{
+    while (hi - lo > 1) {
+        const int m = (lo + hi) >> 1;
+        if (a[m] <= x) lo = m; else hi = m;
+    }
+    return lo;
+}
+
+// First i in [lo, hi) with a[i] >= x (hi if none).
+__device__ __forceinline__ int lds_first_ge(const int16_t *a, int lo, int hi, int x)
+{
+    while (lo < hi) {
+        const int m = (lo + hi) >> 1;
+        if (a[m] < x) lo = m + 1; else hi = m;
+    }
+    return lo;
+}
+
 // One tile = 4096 canonical children, 16 consecutive per thread; every 16
 // threads cover one copy sub-tile of 256 children and record its first output
 // byte.
@@ -89,8 +110,8 @@ __global__ __launch_bounds__(kBlock) void k_gather_scatter(
 // The same kernel serves the streaming emission: there the "parents" are the
 // parents emitted by this call (their count P only known on the device, read
 // from *P_dev), `offsets` is the exclusive scan of their child counts, child
-// v lives in canonical slot vmap[v], the slot epoch is fixed, and no
-// per-parent counts are produced (ns = nf = nk = null).
+// v lives in canonical slot vmap[v], the slot epoch is fixed, and the
+// counts go to the emitted parents' entries.
 __global__ __launch_bounds__(kBlock) void k_gather_scan(
     const int64_t *__restrict__ offsets, int64_t P_arg, const int64_t *__restrict__ P_dev,
     const uint32_t *__restrict__ vmap, uint32_t epoch_arg, const Canon *__restrict__ canon, int64_t canon_cap,
@@ -105,8 +126,9 @@ __global__ __launch_bounds__(kBlock) void k_gather_scan(
     __shared__ uint64_t s_b;
     __shared__ int64_t s_t;
     __shared__ int32_t s_last;
-    __shared__ int64_t s_p[2];
+    __shared__ int64_t s_p[3];
     __shared__ int32_t s_cnt[3][kCntLds];
+    __shared__ int16_t s_off[kTile + 2];        // offsets[pf..pl+1] - ct0, clamped to [-1, kTile + 1]
     __shared__ uint32_t s_len[kTile + kTile / 16];
     __shared__ alignas(16) uint8_t s_st[kTile];
     const int64_t N0 = offsets[P];
@@ -122,13 +144,30 @@ __global__ __launch_bounds__(kBlock) void k_gather_scan(
         if (t >= ntiles) break;
         const int64_t ct0 = t * kTile;
         const int64_t ct1 = min64(ct0 + kTile, N);
-        if (threadIdx.x == 0) {
-            s_p[0] = upper_bound_g(offsets, 0, P + 1, ct0) - 1;
-            s_p[1] = upper_bound_g(offsets, s_p[0], P + 1, ct1 - 1) - 1;
+        // the tile's parents, one wave-parallel search each: pf holds child
+        // ct0, pl holds child ct1 - 1, q0 is the first parent starting at or
+        // after ct0 (empty parents before pf may start exactly at ct0)
+        if (threadIdx.x < 3 * 64) {
+            const int w = (int)(threadIdx.x >> 6);
+            int64_t r;
+            if (w == 0) r = wave_last_le(offsets, 0, P + 1, ct0);
+            else if (w == 1) r = wave_last_le(offsets, 0, P + 1, ct1 - 1);
+            else r = ct0 == 0 ? 0 : wave_last_le(offsets, 0, P + 1, ct0 - 1) + 1;
+            if (lane_id() == 0) s_p[w] = r;
         }
         __syncthreads();
-        const int64_t pf = s_p[0], pl = s_p[1];
-        const int64_t R = min64(pl - pf + 1, kCntLds);
+        const int64_t pf = s_p[0], pl = s_p[1], q0t = s_p[2];
+        const int64_t Rp = pl - pf + 1;
+        const int64_t R = min64(Rp, kCntLds);
+        // with few enough parents, pass 2 searches a tile-relative copy of
+        // their offsets in LDS instead of global memory
+        const bool lds_ok = Rp <= kTile;
+        if (lds_ok) {
+            for (int64_t j = threadIdx.x; j <= Rp; j += kBlock) {
+                const int64_t v = offsets[pf + j] - ct0;
+                s_off[j] = (int16_t)(v < -1 ? -1 : (v > kTile + 1 ? kTile + 1 : v));
+            }
+        }
         for (int j = threadIdx.x; j < 3 * kCntLds; j += kBlock) (&s_cnt[0][0])[j] = 0;
 
         // pass 1: surviving lengths and filled slots.  Each wave reads its 1024
@@ -183,43 +222,65 @@ __global__ __launch_bounds__(kBlock) void k_gather_scan(
 
         // pass 2: parents -- slot offsets and run-length counts
         if (c0 < ct1) {
-            int64_t p = upper_bound_g(offsets, pf, pl + 1, c0) - 1;
-            int64_t pos = base;
-            if (offsets[p] == c0) {
-                // every parent whose first child is c0 (empty ones included)
-                const int64_t q0 = lower_bound_g(offsets, 0, p + 1, c0);
-                if (out_off)
-                    for (int64_t q = q0; q <= p; ++q) out_off[q] = pos;
-            }
-            int64_t next = offsets[p + 1];
             int32_t run[3] = {0, 0, 0};
-            for (int k = 0; k < kItems; ++k) {
-                const int64_t c = c0 + k;
-                if (c >= ct1) break;
-                if (c >= next) {
+            auto flush = [&](int64_t p) {
 #pragma unroll
-                    for (int s = 0; s < 3; ++s) {
-                        if (run[s]) {
-                            if (p - pf < R) atomicAdd(&s_cnt[s][p - pf], run[s]);
-                            else if (cnt_out[s]) atomicAdd(&cnt_out[s][p], run[s]);
-                            run[s] = 0;
-                        }
+                for (int s = 0; s < 3; ++s) {
+                    if (run[s]) {
+                        if (p - pf < R) atomicAdd(&s_cnt[s][p - pf], run[s]);
+                        else if (cnt_out[s]) atomicAdd(&cnt_out[s][p], run[s]);
+                        run[s] = 0;
                     }
-                    const int64_t pn = advance_parent(offsets, P, p, c);
+                }
+            };
+            int64_t pos = base;
+            if (lds_ok) {
+                const int r0 = (int)(c0 - ct0), rend = (int)(ct1 - ct0);
+                int j = lds_last_le(s_off, 0, (int)Rp, r0);
+                if (s_off[j] == r0 && out_off) {
+                    // every parent whose first child is c0 (empty ones included)
+                    const int64_t qa = r0 == 0 ? q0t : pf + lds_first_ge(s_off, 1, j + 1, r0);
+                    for (int64_t q = qa; q <= pf + j; ++q) out_off[q] = pos;
+                }
+                int next = s_off[j + 1];
+                for (int k = 0; k < kItems; ++k) {
+                    const int rc = r0 + k;
+                    if (rc >= rend) break;
+                    if (rc >= next) {
+                        flush(pf + j);
+                        const int jn = lds_last_le(s_off, j + 1, (int)Rp, rc);
+                        if (out_off)
+                            for (int64_t q = pf + j + 1; q <= pf + jn; ++q) out_off[q] = pos;
+                        j = jn;
+                        next = s_off[j + 1];
+                    }
+                    if (stv[k] < 3) run[stv[k]] += 1;
+                    pos += len[k];
+                }
+                flush(pf + j);
+            } else {
+                int64_t p = upper_bound_g(offsets, pf, pl + 1, c0) - 1;
+                if (offsets[p] == c0) {
+                    const int64_t q0 = c0 == ct0 ? q0t : lower_bound_g(offsets, pf, p + 1, c0);
                     if (out_off)
-                        for (int64_t q = p + 1; q <= pn; ++q) out_off[q] = pos;
-                    p = pn;
-                    next = offsets[p + 1];
+                        for (int64_t q = q0; q <= p; ++q) out_off[q] = pos;
                 }
-                if (stv[k] < 3) run[stv[k]] += 1;
-                pos += len[k];
-            }
-#pragma unroll
-            for (int s = 0; s < 3; ++s) {
-                if (run[s]) {
-                    if (p - pf < R) atomicAdd(&s_cnt[s][p - pf], run[s]);
-                    else if (cnt_out[s]) atomicAdd(&cnt_out[s][p], run[s]);
+                int64_t next = offsets[p + 1];
+                for (int k = 0; k < kItems; ++k) {
+                    const int64_t c = c0 + k;
+                    if (c >= ct1) break;
+                    if (c >= next) {
+                        flush(p);
+                        const int64_t pn = advance_parent(offsets, P, p, c);
+                        if (out_off)
+                            for (int64_t q = p + 1; q <= pn; ++q) out_off[q] = pos;
+                        p = pn;
+                        next = offsets[p + 1];
+                    }
+                    if (stv[k] < 3) run[stv[k]] += 1;
+                    pos += len[k];
                 }
+                flush(p);
             }
         }
         __syncthreads();
@@ -445,25 +506,10 @@ __device__ __forceinline__ void copy_window32(const int32_t *s_dst, const uint64
 }
 
 // First sub-tile whose output holds byte `lo`: the largest s in [0, nsub)
-// with sub_base[s] <= lo (sub_base[0] = 0).  Each round, the 64 lanes probe
-// 64 evenly spaced entries of the remaining range and a ballot keeps the gap
-// that holds the answer, so a range of n entries takes about log_65(n) rounds
-// of one load each.
-__device__ __forceinline__ int64_t find_sub_tile(const int64_t *__restrict__ sub_base, int64_t nsub, int64_t lo,
-                                                 int lane)
+// with sub_base[s] <= lo (sub_base[0] = 0).
+__device__ __forceinline__ int64_t find_sub_tile(const int64_t *__restrict__ sub_base, int64_t nsub, int64_t lo)
 {
-    int64_t l = 0, h = nsub;
-    while (h - l > 1) {
-        const int64_t idx = l + ((h - l) * (int64_t)(lane + 1)) / 65;
-        const bool le = sub_base[idx] <= lo;
-        const uint64_t m = __ballot(le);
-        const int k = __popcll(m);                 // the true probes form a prefix
-        const int64_t nl = k > 0 ? __shfl(idx, k - 1, 64) : l;
-        const int64_t nh = k < 64 ? __shfl(idx, k, 64) : h;
-        l = nl;
-        h = nh;
-    }
-    return l;
+    return wave_last_le(sub_base, 0, nsub, lo);
 }
 
 // Output bytes are split into units of G bytes (the last one shorter), cut
@@ -520,7 +566,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_
     for (int64_t u = (int64_t)blockIdx.x * kWaves + wave; u < nunits; u += nwaves) {
         const int64_t lo = max64(u * G - mis, 0);
         const int64_t hi = min64((u + 1) * G - mis, T);
-        for (int64_t sb = find_sub_tile(sub_base, nsub, lo, lane); sb < nsub; ++sb) {
+        for (int64_t sb = find_sub_tile(sub_base, nsub, lo); sb < nsub; ++sb) {
             const int64_t D0 = sub_base[sb];
             if (D0 >= hi) break;
             const int64_t c0 = sb * kSub;

@@ -238,6 +238,27 @@ __device__ __forceinline__ int64_t advance_parent(const int64_t *offsets, int64_
     return upper_bound_g(offsets, p, P + 1, c) - 1;
 }
 
+// Largest i in [lo, hi) with a[i] <= x, for nondecreasing a with a[lo] <= x.
+// Called by all 64 lanes of a wave, which get the same result.  Each round
+// the lanes probe 64 evenly spaced entries of the remaining range and a
+// ballot keeps the gap holding the answer, so n entries take about
+// log_65(n) rounds of one load each.
+__device__ __forceinline__ int64_t wave_last_le(const int64_t *a, int64_t lo, int64_t hi, int64_t x)
+{
+    const int lane = lane_id();
+    int64_t l = lo, h = hi;
+    while (h - l > 1) {
+        const int64_t idx = l + ((h - l) * (int64_t)(lane + 1)) / 65;
+        const uint64_t m = __ballot(a[idx] <= x);
+        const int k = __popcll(m);                 // the true probes form a prefix
+        const int64_t nl = k > 0 ? __shfl(idx, k - 1, 64) : l;
+        const int64_t nh = k < 64 ? __shfl(idx, k, 64) : h;
+        l = nl;
+        h = nh;
+    }
+    return l;
+}
+
 __device__ __forceinline__ int64_t min64(int64_t a, int64_t b) { return a < b ? a : b; }
 __device__ __forceinline__ int64_t max64(int64_t a, int64_t b) { return a > b ? a : b; }
 

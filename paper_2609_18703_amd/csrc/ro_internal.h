@@ -12,7 +12,7 @@ constexpr int kBlock = 256;                 // threads per workgroup (4 waves of
 constexpr int kItems = 16;                  // items per thread in scan tiles
 constexpr int kTile = kBlock * kItems;      // 4096 entries per scan tile
 constexpr int kSub = 256;                   // children per copy sub-tile (the scan records where each starts)
-constexpr int kCntLds = 1024;               // parents aggregated in LDS per tile
+constexpr int kCntLds = 512;                // parents whose counts a tile aggregates in LDS
 
 // Canonical per-child record written by the report scatter.  `tag` holds the
 // call epoch (bits 31..2) and the terminal state (bits 1..0): an entry is

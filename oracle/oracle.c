@@ -168,14 +168,17 @@ static int key_cmp(const void *a, const void *b)
  * order.  Outputs per parent p: counts of SUCCESS/FAILED/SKIPPED reports,
  * complete = all k_p children have a terminal report, parent_state, and the
  * slot out_data[out_off[p], out_off[p+1]) holding the SUCCESS bytes in
- * ordinal order.  out_data may be NULL (metadata only). */
+ * ordinal order.  out_data may be NULL (metadata only).  child_dst (NULL or
+ * [N+1]) receives, for every child in canonical order, the output position
+ * where its bytes start (its bytes, if any, end where the next child's
+ * start; child_dst[N] = total). */
 int oracle_gather(const uint32_t *rep_parent, const uint32_t *rep_ordinal,
                   const uint8_t *rep_state, const int64_t *rep_off,
                   const uint8_t *data, int64_t n_reports,
                   const int64_t *offsets, int64_t n_parents,
                   int64_t *out_off, uint8_t *out_data, int64_t out_cap,
                   int32_t *n_success, int32_t *n_failed, int32_t *n_skipped,
-                  uint8_t *complete, uint8_t *parent_state)
+                  uint8_t *complete, uint8_t *parent_state, int64_t *child_dst)
 {
     if (n_reports < 0 || n_parents < 0 || offsets == NULL || out_off == NULL)
         return OR_EINVAL;
@@ -231,27 +234,32 @@ int oracle_gather(const uint32_t *rep_parent, const uint32_t *rep_ordinal,
         free(keys);
         return OR_ECAP;
     }
-    /* 4. per parent, ascending: counts, completion, state, ordered bytes */
+    /* 4. per parent, ascending: counts, completion, state, and the bytes of
+     *    its children in ordinal order (a child without a SUCCESS report
+     *    adds none) */
     int64_t j = 0, pos = 0;
     for (int64_t p = 0; p < n_parents; ++p) {
         int32_t ns = 0, nf = 0, nk = 0;
-        out_off[p] = pos;
-        while (j < m && (int64_t)keys[j].parent == p) {
-            int64_t i = keys[j].index;
-            if (rep_state[i] == ST_SUCCESS) {
-                int64_t len = rep_off[i + 1] - rep_off[i];
-                if (out_data != NULL && len > 0)
-                    memcpy(out_data + pos, data + rep_off[i], (size_t)len);
-                pos += len;
-                ++ns;
-            } else if (rep_state[i] == ST_FAILED) {
-                ++nf;
-            } else {
-                ++nk;
-            }
-            ++j;
-        }
         int64_t k = offsets[p + 1] - offsets[p];
+        out_off[p] = pos;
+        for (int64_t o = 0; o < k; ++o) {
+            if (child_dst) child_dst[offsets[p] + o] = pos;
+            if (j < m && (int64_t)keys[j].parent == p && (int64_t)keys[j].ordinal == o) {
+                int64_t i = keys[j].index;
+                if (rep_state[i] == ST_SUCCESS) {
+                    int64_t len = rep_off[i + 1] - rep_off[i];
+                    if (out_data != NULL && len > 0)
+                        memcpy(out_data + pos, data + rep_off[i], (size_t)len);
+                    pos += len;
+                    ++ns;
+                } else if (rep_state[i] == ST_FAILED) {
+                    ++nf;
+                } else {
+                    ++nk;
+                }
+                ++j;
+            }
+        }
         int done = ((int64_t)ns + nf + nk == k);
         if (n_success) n_success[p] = ns;
         if (n_failed)  n_failed[p] = nf;
@@ -261,6 +269,7 @@ int oracle_gather(const uint32_t *rep_parent, const uint32_t *rep_ordinal,
             parent_state[p] = !done ? ST_PENDING : (nf > 0 ? ST_FAILED : ST_SUCCESS);
     }
     out_off[n_parents] = pos;
+    if (child_dst) child_dst[offsets[n_parents]] = pos;
     free(keys);
     return OR_OK;
 }

@@ -50,7 +50,7 @@ def _load(path):
     i64 = C.c_int64
     L.oracle_expand.argtypes = [P, i64, P, P, P, i64]
     L.oracle_batch.argtypes = [P, P, i64, P, i64, C.c_int32, P, P, P, i64, P, P, P]
-    L.oracle_gather.argtypes = [P, P, P, P, P, i64, P, i64, P, P, i64, P, P, P, P, P]
+    L.oracle_gather.argtypes = [P, P, P, P, P, i64, P, i64, P, P, i64, P, P, P, P, P, P]
     L.oracle_stream_create.argtypes = [P, i64]
     L.oracle_stream_create.restype = P
     L.oracle_stream_destroy.argtypes = [P]
@@ -121,8 +121,9 @@ def batch(queue, keep, offsets, batch_size, L=None):
     return child[:m], parent[:m], ordinal[:m], sizes[:nb]
 
 
-def gather(parent, ordinal, state, off, data, offsets, with_data=True, L=None):
-    """Ordered gather; returns a dict of per-parent outputs."""
+def gather(parent, ordinal, state, off, data, offsets, with_data=True, child_dst=False, L=None):
+    """Ordered gather; returns a dict of per-parent outputs (and, with
+    child_dst, every child's output start position, N+1 entries)."""
     L = L or lib()
     parent = np.ascontiguousarray(parent, dtype=np.uint32)
     ordinal = np.ascontiguousarray(ordinal, dtype=np.uint32)
@@ -140,12 +141,15 @@ def gather(parent, ordinal, state, off, data, offsets, with_data=True, L=None):
     nk = np.zeros(max(P, 1), np.int32)
     comp = np.zeros(max(P, 1), np.uint8)
     pst = np.zeros(max(P, 1), np.uint8)
+    cdst = np.zeros(int(offsets[-1]) + 1, np.int64) if child_dst else None
     _check(L.oracle_gather(_p(parent), _p(ordinal), _p(state), _p(off),
                            _p(data) if with_data else None, n, _p(offsets), P,
                            _p(out_off), _p(out_data), cap, _p(ns), _p(nf), _p(nk),
-                           _p(comp), _p(pst)), "gather")
+                           _p(comp), _p(pst), _p(cdst) if child_dst else None), "gather")
     res = dict(out_off=out_off, n_success=ns[:P], n_failed=nf[:P], n_skipped=nk[:P],
                complete=comp[:P], parent_state=pst[:P])
+    if child_dst:
+        res["child_dst_off"] = cdst
     if with_data:
         res["out_data"] = out_data[:int(out_off[-1])]
     return res

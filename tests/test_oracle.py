@@ -202,6 +202,38 @@ def test_gather_vs_brute_random():
         _compare_brute(_run_gather(reports, counts), brute.gather(reports, counts))
 
 
+def test_gather_child_positions():
+    """Per-child output positions: the bytes between a child's position and
+    the next child's are exactly its own SUCCESS record (empty for any other
+    state or no report), and a parent's first child starts its slot."""
+    rng = np.random.default_rng(23)
+    for trial in range(200):
+        P = int(rng.integers(0, 8))
+        counts = [int(x) for x in rng.integers(0, 5, P)]
+        reports = _random_reports(rng, counts, p_report=float(rng.choice([1.0, 0.6])),
+                                  states=(0, 0, 1, 2, 3), max_len=7)
+        offsets = O.expand(np.array(counts, np.int32), tags=False)
+        par = np.array([r[0] for r in reports], np.uint32)
+        ordi = np.array([r[1] for r in reports], np.uint32)
+        st = np.array([r[2] for r in reports], np.uint8)
+        lens = np.array([len(r[3]) for r in reports], np.int64)
+        off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+        data = np.frombuffer(b"".join(r[3] for r in reports) or b"\0", np.uint8)
+        g = O.gather(par, ordi, st, off, data, offsets, child_dst=True)
+        cd = g["child_dst_off"]
+        N = int(offsets[-1])
+        assert len(cd) == N + 1 and cd[N] == g["out_off"][P]
+        want = {}
+        for p_, o_, s_, b_ in reports:
+            if s_ == O.SUCCESS:
+                want[int(offsets[p_]) + o_] = b_
+        for c in range(N):
+            assert bytes(g["out_data"][cd[c]:cd[c + 1]]) == want.get(c, b""), (trial, c)
+        for p_ in range(P):
+            if counts[p_] > 0:
+                assert cd[offsets[p_]] == g["out_off"][p_]
+
+
 def test_gather_round_trip_and_content():
     """gather(batch(expand(x))) puts every record of parent p back in ordinal
     order; each record's bytes are the splitmix64 stream of its own key."""

@@ -153,12 +153,14 @@ def alg_single(P, N, M, S):
     return _add(a, _gather_bytes(P, N, S))
 
 
-def alg_nested(P1, N1, N2, S2, S1):
+def alg_nested(P1, N1, N2, S2, S1, upper_in_place):
+    """Two levels; when every mid slot survives, the top slots are the mid
+    slots as they lie, so the top level moves no payload (in-place gather)."""
     a = {"expand_scan": 12 * P1 + 12 * N1 + 16, "expand_tags": 8 * N1 + 8 * N2,
          "batch_samples": 4 * cdiv(N1, 64) + 4 * cdiv(N2, 64),
          "batch": 12 * N1 + 12 * N2}
     _add(a, _gather_bytes(N1, N2, S2))
-    return _add(a, _gather_bytes(P1, N1, S1))
+    return _add(a, _gather_bytes(P1, N1, 0 if upper_in_place else S1))
 
 
 def alg_stream(P, N, S, n_waves, emit_wave):
@@ -236,11 +238,6 @@ def stage_nested(ctx, which, parents):
     P1, N1, N2 = len(n.counts1), len(n.queue1), len(n.queue2)
     S2 = int(r.off[-1])
     log(f"[bench] {which}: top={P1} mid={N1} leaves={N2} leaf bytes={S2}")
-    data = D.reports_data_dev(r)
-    b = PL.NestedBuffers(D.to_dev(n.counts1), D.to_dev(n.queue1.view(np.int32)), n.batch1,
-                         D.to_dev(n.counts2), D.to_dev(n.queue2.view(np.int32)), n.batch2,
-                         D.to_dev(r.state), D.to_dev(r.off), data, N1, N2)
-    ctx.reserve(N2, max(N1, P1), N2)
     # surviving bytes at the top level: mid slots whose leaves all succeeded
     off2 = np.concatenate([[0], np.cumsum(n.counts2.astype(np.int64))])
     ok_leaf = (n.states == W.SUCCESS)
@@ -250,14 +247,21 @@ def stage_nested(ctx, which, parents):
     mid_bytes = np.where(n.counts2 > 0, mid_bytes, 0)
     mid_failed = np.where(n.counts2 > 0, mid_failed, 0)
     S1 = int(mid_bytes[mid_failed == 0].sum())
+    # no leaf fails: the top level aliases the mid bytes (nothing to move)
+    in_place = S1 == S2 and not (n.states == W.FAILED).any()
+    data = D.reports_data_dev(r)
+    b = PL.NestedBuffers(D.to_dev(n.counts1), D.to_dev(n.queue1.view(np.int32)), n.batch1,
+                         D.to_dev(n.counts2), D.to_dev(n.queue2.view(np.int32)), n.batch2,
+                         D.to_dev(r.state), D.to_dev(r.off), data, N1, N2, upper_in_place=in_place)
+    ctx.reserve(N2, max(N1, P1), N2)
 
     def check():
         assert int(b.mid_off[N1].item()) == S2 and int(b.top_off[P1].item()) == S1
 
     cfg = {"workload": desc.format(P=P1), "top_parents": P1, "mid_children": N1, "leaf_children": N2,
-           "leaf_bytes": S2, "top_bytes": S1, "batch_size": [n.batch1, n.batch2]}
-    return Job(which, lambda: PL.nested(ctx, b), N1 + N2, alg_nested(P1, N1, N2, S2, S1), cfg, check,
-               leaves=N2)
+           "leaf_bytes": S2, "top_bytes": S1, "batch_size": [n.batch1, n.batch2], "upper_in_place": in_place}
+    return Job(which, lambda: PL.nested(ctx, b), N1 + N2, alg_nested(P1, N1, N2, S2, S1, in_place), cfg,
+               check, leaves=N2)
 
 
 def stage_stream(ctx, parents):

@@ -151,6 +151,10 @@ typedef struct ro_gather_out {
     uint8_t *complete;        /* 1 iff all k_p children have a terminal report (NULL ok) */
     uint8_t *parent_state;    /* RO_PENDING if incomplete, else RO_FAILED if any member
                                  failed, else RO_SUCCESS (NULL ok)                        */
+    int64_t *child_dst_off;   /* [N + 1] or NULL: output position of every child in
+                                 canonical order; child c's bytes (none unless it has a
+                                 SUCCESS report) are [child_dst_off[c],
+                                 child_dst_off[c+1]), child_dst_off[N] = out_off[P]     */
 } ro_gather_out;
 
 /* F.reduce: ordered gather of reports into parent slots.  Slot p holds the
@@ -160,7 +164,12 @@ typedef struct ro_gather_out {
  * no children is complete and RO_SUCCESS with an empty slot.  Errors:
  * RO_ERANGE, RO_ESTATE, RO_EINVAL (offsets), RO_EDUP (two reports for one
  * child), RO_ECAP (bytes > out_cap, or N above the reservation).
- * out_data must not overlap the report bytes. */
+ * out_data must not overlap the report bytes, with one exception: it may be
+ * the reports' own data pointer when every copied record already sits at
+ * its output position, as in the upper level of a nested gather whose lower
+ * slots all survive (Sec. 4: a parent's value is its members' values in
+ * order, so the lower slots already are the upper ones).  Nothing is then
+ * copied; a record that would have to move is RO_EINVAL. */
 int ro_gather(ro_ctx *ctx, const ro_reports *reports, const int64_t *offsets, int64_t n_parents,
               const ro_gather_out *out);
 

@@ -116,8 +116,8 @@ __global__ __launch_bounds__(kBlock) void k_gather_scan(
     const int64_t *__restrict__ offsets, int64_t P_arg, const int64_t *__restrict__ P_dev,
     const uint32_t *__restrict__ vmap, uint32_t epoch_arg, const Canon *__restrict__ canon, int64_t canon_cap,
     int64_t *__restrict__ out_off, int32_t *__restrict__ ns, int32_t *__restrict__ nf,
-    int32_t *__restrict__ nk, int64_t *__restrict__ sub_base, Ctl *ctl, uint64_t *desc,
-    int64_t desc_cap)
+    int32_t *__restrict__ nk, int64_t *__restrict__ cdst, int64_t *__restrict__ sub_base, Ctl *ctl,
+    uint64_t *desc, int64_t desc_cap)
 {
     const int64_t P = P_dev ? *P_dev : P_arg;
     const uint32_t epoch = epoch_arg ? epoch_arg : ctl->canon_epoch;
@@ -255,6 +255,7 @@ __global__ __launch_bounds__(kBlock) void k_gather_scan(
                         next = s_off[j + 1];
                     }
                     if (stv[k] < 3) run[stv[k]] += 1;
+                    if (cdst) cdst[c0 + k] = pos;
                     pos += len[k];
                 }
                 flush(pf + j);
@@ -278,6 +279,7 @@ __global__ __launch_bounds__(kBlock) void k_gather_scan(
                         next = offsets[p + 1];
                     }
                     if (stv[k] < 3) run[stv[k]] += 1;
+                    if (cdst) cdst[c] = pos;
                     pos += len[k];
                 }
                 flush(p);
@@ -309,7 +311,7 @@ __global__ __launch_bounds__(kBlock) void k_gather_finalize(
     const int64_t *__restrict__ offsets, int64_t P, int64_t canon_cap, int64_t *__restrict__ out_off,
     int64_t out_cap, int has_data, const int32_t *__restrict__ ns, const int32_t *__restrict__ nf,
     const int32_t *__restrict__ nk, uint8_t *__restrict__ complete, uint8_t *__restrict__ pstate,
-    Ctl *ctl)
+    int64_t *__restrict__ cdst, Ctl *ctl)
 {
     const int64_t N0 = offsets[P];
     const int64_t N = N0 <= canon_cap ? N0 : 0;
@@ -317,6 +319,7 @@ __global__ __launch_bounds__(kBlock) void k_gather_finalize(
     const int64_t gtid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (gtid == 0) {
         if (out_off) out_off[P] = total;
+        if (cdst && N0 <= canon_cap) cdst[N0] = total;
         if (ctl->n_filled != ctl->n_valid) raise_err(ctl, RO_EDUP);
         if (has_data && total > out_cap) raise_err(ctl, RO_ECAP);
     }
@@ -540,7 +543,7 @@ constexpr int64_t kCopyMinUnit = RO_COPY_MIN_UNIT;
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_WAVES))) void k_gather_copy(
     const int64_t *__restrict__ offsets, int64_t P_arg, const int64_t *__restrict__ P_dev,
     const uint32_t *__restrict__ vmap, uint32_t epoch_arg, const Canon *__restrict__ canon, int64_t canon_cap,
-    const int64_t *__restrict__ sub_base, uint8_t *__restrict__ out, Ctl *ctl)
+    const int64_t *__restrict__ sub_base, uint8_t *__restrict__ out, int in_place, Ctl *ctl)
 {
     constexpr int kWaves = kBlock / 64;
     const int64_t P = P_dev ? *P_dev : P_arg;
@@ -595,13 +598,24 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_
             const int64_t ws = max64(lo - D0, 0), we = min64(hi - D0, tot);
             if (we > ws) {
                 int64_t run = inc - lsum;
+                bool moves = false;
 #pragma unroll
                 for (int k = 0; k < kCopyPer; ++k) {
                     const int r = lane * kCopyPer + k;
                     const int64_t cs = min64(max64(run, ws), we);
+                    const int64_t ce = min64(max64(run + (int64_t)l[k], ws), we);
+                    const uint64_t src = s[k] + (uint64_t)(cs - run);
                     s_dst[r] = (int32_t)(cs - ws);
-                    s_src[r] = s[k] + (uint64_t)(cs - run);
+                    s_src[r] = src;
+                    moves |= ce > cs && src != outa + (uint64_t)(D0 + cs);
                     run += l[k];
+                }
+                if (in_place) {
+                    // output aliases the report bytes: records that already
+                    // sit at their output position need no copy, any other
+                    // would overwrite bytes still to be read
+                    if (__ballot(moves) != 0 && lane == 0) raise_err(ctl, RO_EINVAL);
+                    continue;
                 }
                 if (lane == 0) s_dst[kSub] = (int32_t)(we - ws);
                 __builtin_amdgcn_wave_barrier();
@@ -621,17 +635,17 @@ hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w
     const int64_t grid_s = (int64_t)L.num_cus * 4;
     RO_LAUNCH(L, RO_K_GATHER_SCAN, k_gather_scan, dim3((unsigned)grid_s), dim3(kBlock), 0, L.stream, a.offsets, a.P,
               (const int64_t *)nullptr, (const uint32_t *)nullptr, 0u, w.canon, w.canon_cap, a.out_off, a.ns,
-              a.nf, a.nk, w.sub_base, L.ctl, L.desc, L.desc_cap);
+              a.nf, a.nk, a.cdst, w.sub_base, L.ctl, L.desc, L.desc_cap);
     int64_t grid_f = (a.P + kBlock - 1) / kBlock;
     grid_f = grid_f < 1 ? 1 : (grid_f > (int64_t)L.num_cus * 8 ? (int64_t)L.num_cus * 8 : grid_f);
     RO_LAUNCH(L, RO_K_GATHER_FINALIZE, k_gather_finalize, dim3((unsigned)grid_f), dim3(kBlock), 0, L.stream, a.offsets,
                        a.P, w.canon_cap, a.out_off, a.out_cap, a.out_data != nullptr ? 1 : 0, a.ns, a.nf,
-                       a.nk, a.complete, a.pstate, L.ctl);
+                       a.nk, a.complete, a.pstate, a.cdst, L.ctl);
     if (a.out_data != nullptr) {
         const int64_t grid_c = (int64_t)L.num_cus * 8;
         RO_LAUNCH(L, RO_K_GATHER_COPY, k_gather_copy, dim3((unsigned)grid_c), dim3(kBlock), 0, L.stream, a.offsets,
                   a.P, (const int64_t *)nullptr, (const uint32_t *)nullptr, 0u, w.canon, w.canon_cap, w.sub_base,
-                  a.out_data, L.ctl);
+                  a.out_data, a.out_data == a.data ? 1 : 0, L.ctl);
     }
     RO_LAUNCH(L, RO_K_GATHER_RESET, k_gather_reset, dim3(1), dim3(64), 0, L.stream, L.ctl);
     return hipGetLastError();
@@ -645,8 +659,8 @@ hipError_t launch_virtual_scan(const Launch &L, const int64_t *voff, const int64
 {
     const int64_t grid_s = (int64_t)L.num_cus * 4;
     RO_LAUNCH(L, RO_K_STREAM_SCAN, k_gather_scan, dim3((unsigned)grid_s), dim3(kBlock), 0, L.stream, voff,
-              (int64_t)0, E_dev, vmap, 1u, canon, canon_cap, emit_off, ns, nf, nk, sub_base, L.ctl, L.desc,
-              L.desc_cap);
+              (int64_t)0, E_dev, vmap, 1u, canon, canon_cap, emit_off, ns, nf, nk, (int64_t *)nullptr, sub_base,
+              L.ctl, L.desc, L.desc_cap);
     return hipGetLastError();
 }
 
@@ -655,7 +669,7 @@ hipError_t launch_virtual_copy(const Launch &L, const int64_t *voff, const int64
 {
     const int64_t grid_c = (int64_t)L.num_cus * 8;
     RO_LAUNCH(L, RO_K_STREAM_COPY, k_gather_copy, dim3((unsigned)grid_c), dim3(kBlock), 0, L.stream, voff,
-              (int64_t)0, E_dev, vmap, 1u, canon, canon_cap, sub_base, out, L.ctl);
+              (int64_t)0, E_dev, vmap, 1u, canon, canon_cap, sub_base, out, 0, L.ctl);
     return hipGetLastError();
 }
 

@@ -327,6 +327,7 @@ int ro_gather(ro_ctx *c, const ro_reports *r, const int64_t *offsets, int64_t n_
     a.nk = o->n_skipped;
     a.complete = o->complete;
     a.pstate = o->parent_state;
+    a.cdst = o->child_dst_off;
     if (!a.ns || !a.nf || !a.nk) {
         if ((rc = ensure_cnt(c, n_parents))) return rc;
         if (!a.ns) a.ns = c->cnt;

@@ -94,6 +94,7 @@ struct GatherArgs {
     int64_t out_cap;
     int32_t *ns, *nf, *nk;
     uint8_t *complete, *pstate;
+    int64_t *cdst;           // per-child output positions (or null)
 };
 
 struct GatherWs {

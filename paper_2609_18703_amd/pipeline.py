@@ -71,10 +71,17 @@ def single_level(ctx, b: SingleLevelBuffers):
 
 
 class NestedBuffers:
-    """Device inputs and outputs of a two-level pipeline (top -> mid -> leaf)."""
+    """Device inputs and outputs of a two-level pipeline (top -> mid -> leaf).
+
+    With ``upper_in_place`` the top level's bytes are the mid level's buffer
+    itself: valid when every mid slot survives (no failed leaf), since each
+    top slot then is the run of its mid slots as they already lie.  The upper
+    gather checks this on the device and copies nothing (RO_EINVAL if a mid
+    slot would have to move).
+    """
 
     def __init__(self, counts1, queue1, batch1, counts2, queue2, batch2, leaf_state, leaf_off,
-                 leaf_data, n_mid, n_leaf, want_data=True):
+                 leaf_data, n_mid, n_leaf, want_data=True, upper_in_place=False):
         P1 = counts1.numel()
         self.P1, self.N1, self.N2 = P1, int(n_mid), int(n_leaf)
         self.counts1, self.queue1, self.B1 = counts1, queue1, int(batch1)
@@ -99,7 +106,12 @@ class NestedBuffers:
         self.mid_complete = _empty(N1, torch.uint8)
         self.mid_state = _empty(N1, torch.uint8)
         self.top_off = _empty(P1 + 1, torch.int64)
-        self.top_data = _empty(cap, torch.uint8) if want_data else None
+        if not want_data:
+            self.top_data = None
+        elif upper_in_place:
+            self.top_data = self.mid_data
+        else:
+            self.top_data = _empty(cap, torch.uint8)
         self.top_cnt = _empty(3 * P1, torch.int32)
         self.top_complete = _empty(P1, torch.uint8)
         self.top_state = _empty(P1, torch.uint8)

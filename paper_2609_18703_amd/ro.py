@@ -38,7 +38,7 @@ class ReportsT(C.Structure):
 class GatherOutT(C.Structure):
     _fields_ = [("out_off", C.c_void_p), ("out_data", C.c_void_p), ("out_cap", C.c_int64),
                 ("n_success", C.c_void_p), ("n_failed", C.c_void_p), ("n_skipped", C.c_void_p),
-                ("complete", C.c_void_p), ("parent_state", C.c_void_p)]
+                ("complete", C.c_void_p), ("parent_state", C.c_void_p), ("child_dst_off", C.c_void_p)]
 
 
 _lib = None
@@ -155,12 +155,12 @@ class Context:
 
     def gather(self, parent, ordinal, state, off, data, offsets, out_off, out_data=None,
                n_success=None, n_failed=None, n_skipped=None, complete=None, parent_state=None,
-               n=None, out_cap=None):
+               n=None, out_cap=None, child_dst_off=None):
         rep = _reports(parent, ordinal, state, off, data, n)
         if out_cap is None:
             out_cap = out_data.numel() if out_data is not None else 0
         out = GatherOutT(_ptr(out_off), _ptr(out_data), int(out_cap), _ptr(n_success), _ptr(n_failed),
-                         _ptr(n_skipped), _ptr(complete), _ptr(parent_state))
+                         _ptr(n_skipped), _ptr(complete), _ptr(parent_state), _ptr(child_dst_off))
         _check(self.L.ro_gather(self.h, C.byref(rep), _ptr(offsets), offsets.numel() - 1, C.byref(out)),
                "ro_gather")
 

@@ -156,7 +156,7 @@ def _gather_case(ctx, counts, par, ordi, st, off, data, extra_lead=0):
     offs = O.expand(counts, tags=False)
     P = len(counts)
     n = len(par)
-    want = O.gather(par, ordi, st, off, data, offs)
+    want = O.gather(par, ordi, st, off, data, offs, child_dst=True)
     lead = torch.zeros(extra_lead + len(data) + 16, dtype=torch.uint8, device="cuda")
     lead[extra_lead:extra_lead + len(data)] = torch.from_numpy(data).cuda()
     d_data = lead[extra_lead:]
@@ -173,10 +173,12 @@ def _gather_case(ctx, counts, par, ordi, st, off, data, extra_lead=0):
     d_par = D.to_dev(par.view(np.int32)) if n else z32
     d_ord = D.to_dev(ordi.view(np.int32)) if n else z32
     d_st = D.to_dev(st) if n else torch.zeros(1, dtype=torch.uint8, device="cuda")
+    cdst = torch.full((int(offs[-1]) + 1,), -5, dtype=torch.int64, device="cuda")
     ctx.gather(d_par, d_ord, d_st, D.to_dev(off), d_data, D.to_dev(offs), o_off, out, ns, nf, nk,
-               comp, pst, n=n, out_cap=tot)
+               comp, pst, n=n, out_cap=tot, child_dst_off=cdst)
     ctx.check("gather")
     assert np.array_equal(o_off.cpu().numpy(), want["out_off"])
+    assert np.array_equal(cdst.cpu().numpy(), want["child_dst_off"])
     assert np.array_equal(ns.cpu().numpy()[:P], want["n_success"])
     assert np.array_equal(nf.cpu().numpy()[:P], want["n_failed"])
     assert np.array_equal(nk.cpu().numpy()[:P], want["n_skipped"])

@@ -39,13 +39,13 @@ def _u32(t, n):
 
 
 # ------------------------------------------------------------------ nested
-def _nested_case(ctx, n):
+def _nested_case(ctx, n, upper_in_place=False):
     from paper_2609_18703_amd import pipeline as PL
     r = n.reports
     data = r.data()
     b = PL.NestedBuffers(D.to_dev(n.counts1), _i32(n.queue1), n.batch1, D.to_dev(n.counts2), _i32(n.queue2),
                          n.batch2, D.to_dev(r.state), D.to_dev(r.off), D.to_dev(data), len(n.queue1),
-                         len(n.queue2))
+                         len(n.queue2), upper_in_place=upper_in_place)
     PL.nested(ctx, b)
     ctx.check("nested")
     want = O.nested(n.counts1, n.queue1, None, n.batch1, n.counts2, n.queue2, None, n.batch2,
@@ -67,6 +67,30 @@ def _nested_case(ctx, n):
     assert np.array_equal(b.top_cnt.cpu().numpy()[:P1], up["n_success"])
     assert np.array_equal(b.top_cnt.cpu().numpy()[P1:2 * P1], up["n_failed"])
     assert np.array_equal(b.top_data.cpu().numpy()[:int(up["out_off"][-1])], up["out_data"])
+
+
+@pytest.mark.parametrize("n_docs", [1, 37, 400])
+def test_nested_documents_upper_in_place(ctx, n_docs):
+    """No region fails, so each document slot is its pages' slots as they
+    already lie: the upper gather aliases the page buffer and copies nothing,
+    with the same results as a separate buffer."""
+    _say("nested docs in place", n_docs)
+    _nested_case(ctx, W.config3(n_docs=n_docs), upper_in_place=True)
+
+
+def test_nested_upper_in_place_rejects_moves(ctx):
+    """With a failed frame, clips drop out of their video's slot and later
+    clips would have to move: an in-place upper gather is RO_EINVAL."""
+    from paper_2609_18703_amd import pipeline as PL
+    n = W.config4(n_videos=40)
+    assert (n.states == W.FAILED).any()
+    r = n.reports
+    b = PL.NestedBuffers(D.to_dev(n.counts1), _i32(n.queue1), n.batch1, D.to_dev(n.counts2), _i32(n.queue2),
+                         n.batch2, D.to_dev(r.state), D.to_dev(r.off), D.to_dev(r.data()), len(n.queue1),
+                         len(n.queue2), upper_in_place=True)
+    PL.nested(ctx, b)
+    assert ctx.status() == O.EINVAL
+    ctx.check("after in-place rejection")
 
 
 @pytest.mark.parametrize("n_docs", [1, 37, 400])

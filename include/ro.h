@@ -175,7 +175,7 @@ int ro_gather(ro_ctx *ctx, const ro_reports *reports, const int64_t *offsets, in
 
 /* Streaming gather over one expansion (offsets[P+1] on the device, kept by
  * reference until ro_stream_destroy).  The stream's own state lives in
- * device memory allocated here (about 20 bytes per child and 30 per parent). */
+ * device memory allocated here (about 32 bytes per child and 34 per parent). */
 typedef struct ro_stream ro_stream;
 int ro_stream_create(ro_ctx *ctx, const int64_t *offsets, int64_t n_parents, int64_t n_children,
                      ro_stream **out);

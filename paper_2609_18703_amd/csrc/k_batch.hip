@@ -199,10 +199,17 @@ hipError_t launch_batch(const Launch &L, const uint32_t *queue, const uint8_t *k
                         int64_t out_cap, int64_t *n_out, int64_t *n_batches, uint32_t *cmap,
                         int64_t cmap_cap)
 {
-    if (out_parent != nullptr || out_ordinal != nullptr) {
+    // The coarse map costs a search per 64 children; a short unmasked queue
+    // (fewer entries than parents, such as one wave of a stream) searches
+    // the offsets directly instead and skips the extra launch.
+    const bool tags = out_parent != nullptr || out_ordinal != nullptr;
+    const bool use_map = tags && !(keep == nullptr && Q < P);
+    if (use_map) {
         const int64_t grid_m = (int64_t)L.num_cus * 4;
         RO_LAUNCH(L, RO_K_BATCH_SAMPLES, k_batch_cmap, dim3((unsigned)grid_m), dim3(256), 0, L.stream,
                   offsets, P, cmap, cmap_cap);
+    } else {
+        cmap_cap = 0;
     }
     if (keep == nullptr) {
         int64_t grid_a = (Q + kBlock * kAllPer - 1) / (kBlock * kAllPer);

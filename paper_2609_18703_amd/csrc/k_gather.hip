@@ -20,7 +20,7 @@
 //              sub-tiles it overlaps and writes the range as aligned 16-byte
 //              stores; sources are byte-aligned records read as aligned
 //              16-byte pairs and realigned in registers.
-#include "ro_device.h"
+#include "ro_copy.h"
 
 namespace ro {
 
@@ -82,45 +82,16 @@ __global__ __launch_bounds__(kBlock) void k_gather_scatter(
 }
 
 // ---------------------------------------------------------------- scan
-// Searches over the tile-relative parent offsets held in LDS.
-// Largest i in [lo, hi) with a[i] <= x, given a[lo] <= x.
-__device__ __forceinline__ int lds_last_le(const int16_t *a, int lo, int hi, int x)
-{
-    while (hi - lo > 1) {
-        const int m = (lo + hi) >> 1;
-        if (a[m] <= x) lo = m; else hi = m;
-    }
-    return lo;
-}
-
-// First i in [lo, hi) with a[i] >= x (hi if none).
-__device__ __forceinline__ int lds_first_ge(const int16_t *a, int lo, int hi, int x)
-{
-    while (lo < hi) {
-        const int m = (lo + hi) >> 1;
-        if (a[m] < x) lo = m + 1; else hi = m;
-    }
-    return lo;
-}
-
 // One tile = 4096 canonical children, 16 consecutive per thread; every 16
 // threads cover one copy sub-tile of 256 children and record its first output
 // byte.
-//
-// The same kernel serves the streaming emission: there the "parents" are the
-// parents emitted by this call (their count P only known on the device, read
-// from *P_dev), `offsets` is the exclusive scan of their child counts, child
-// v lives in canonical slot vmap[v], the slot epoch is fixed, and the
-// counts go to the emitted parents' entries.
 __global__ __launch_bounds__(kBlock) void k_gather_scan(
-    const int64_t *__restrict__ offsets, int64_t P_arg, const int64_t *__restrict__ P_dev,
-    const uint32_t *__restrict__ vmap, uint32_t epoch_arg, const Canon *__restrict__ canon, int64_t canon_cap,
+    const int64_t *__restrict__ offsets, int64_t P, const Canon *__restrict__ canon, int64_t canon_cap,
     int64_t *__restrict__ out_off, int32_t *__restrict__ ns, int32_t *__restrict__ nf,
     int32_t *__restrict__ nk, int64_t *__restrict__ cdst, int64_t *__restrict__ sub_base, Ctl *ctl,
     uint64_t *desc, int64_t desc_cap)
 {
-    const int64_t P = P_dev ? *P_dev : P_arg;
-    const uint32_t epoch = epoch_arg ? epoch_arg : ctl->canon_epoch;
+    const uint32_t epoch = ctl->canon_epoch;
     const uint32_t sepoch = scan_epoch(ctl);
     __shared__ int64_t s_wave[kBlock / 64];
     __shared__ uint64_t s_b;
@@ -183,7 +154,7 @@ __global__ __launch_bounds__(kBlock) void k_gather_scan(
                 const int64_t c = ct0 + j;
                 uint32_t L = 0, S = 4;        // state, or 4 = not reported in this call
                 if (c < ct1) {
-                    const Canon e = canon[vmap ? (int64_t)vmap[c] : c];
+                    const Canon e = canon[c];
                     if ((e.tag >> 2) == epoch) {
                         S = e.tag & 3u;
                         L = S == RO_SUCCESS ? e.len : 0;
@@ -349,186 +320,12 @@ __global__ void k_gather_reset(Ctl *ctl)
 }
 
 // ---------------------------------------------------------------- copy
-// Payload accesses use explicit global-address-space pointers so they compile
-// to global_load/global_store (flat accesses would also hold up every LDS
-// read of the record search behind outstanding memory traffic).
-#define RO_GLOBAL __attribute__((address_space(1)))
-
-typedef uint32_t v4u32 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ uint4 ld16(uint64_t a)
-{
-    const v4u32 t = *(const RO_GLOBAL v4u32 *)a;
-    return make_uint4(t.x, t.y, t.z, t.w);
-}
-__device__ __forceinline__ void st16(uint64_t a, uint4 v)
-{
-    const v4u32 t = {v.x, v.y, v.z, v.w};
-    *(RO_GLOBAL v4u32 *)a = t;
-}
-__device__ __forceinline__ uint8_t ld8(uint64_t a) { return *(const RO_GLOBAL uint8_t *)a; }
-__device__ __forceinline__ void st8(uint64_t a, uint8_t v) { *(RO_GLOBAL uint8_t *)a = v; }
-
-// Bytes sh..sh+15 of the 32-byte pair (lo, hi).
-__device__ __forceinline__ uint4 shift16(const uint4 &lo, const uint4 &hi, uint32_t sh)
-{
-    const uint32_t dw = sh >> 2, bs = sh & 3;
-    uint32_t w0, w1, w2, w3, w4;
-    if (dw == 0)      { w0 = lo.x; w1 = lo.y; w2 = lo.z; w3 = lo.w; w4 = hi.x; }
-    else if (dw == 1) { w0 = lo.y; w1 = lo.z; w2 = lo.w; w3 = hi.x; w4 = hi.y; }
-    else if (dw == 2) { w0 = lo.z; w1 = lo.w; w2 = hi.x; w3 = hi.y; w4 = hi.z; }
-    else              { w0 = lo.w; w1 = hi.x; w2 = hi.y; w3 = hi.z; w4 = hi.w; }
-    uint4 r;
-    r.x = __builtin_amdgcn_alignbyte(w1, w0, bs);
-    r.y = __builtin_amdgcn_alignbyte(w2, w1, bs);
-    r.z = __builtin_amdgcn_alignbyte(w3, w2, bs);
-    r.w = __builtin_amdgcn_alignbyte(w4, w3, bs);
-    return r;
-}
-
-// One record's share of an output chunk: output bytes fv..lv (0..15) come
-// from source addresses S+fv .. S+lv.  Only the aligned 16-byte source
-// chunks holding some of those bytes are read, so no load leaves a page the
-// record occupies.
-struct Piece {
-    uint4 lo, hi;
-    uint32_t sh;
-    int fv, lv;
-};
-
-__device__ __forceinline__ void piece_load(Piece &p, uint64_t S, int fv, int lv)
-{
-    const uint64_t c0 = S & ~(uint64_t)15;
-    p.sh = (uint32_t)(S & 15);
-    p.fv = fv;
-    p.lv = lv;
-    const bool need0 = S + (uint64_t)fv < c0 + 16;
-    const bool need1 = S + (uint64_t)lv >= c0 + 16;
-    // Both loads are unconditional (a conditional load makes the compiler
-    // zero its destination first, which waits for every outstanding memory
-    // operation); a half that is not needed re-reads the one that is, and
-    // its bytes are masked off by piece_merge.
-    p.lo = ld16(need0 ? c0 : c0 + 16);
-    p.hi = ld16(need1 ? c0 + 16 : c0);
-}
-
-// Byte mask of output bytes fv..lv that fall in dword j.
-__device__ __forceinline__ uint32_t byte_mask(int j, int fv, int lv)
-{
-    const int a = fv - 4 * j > 0 ? fv - 4 * j : 0;
-    const int b = lv - 4 * j < 3 ? lv - 4 * j : 3;
-    if (a > b) return 0u;
-    return (0xffffffffu >> (8 * (3 - b))) & (0xffffffffu << (8 * a));
-}
-
-__device__ __forceinline__ void piece_merge(uint4 &acc, const Piece &p)
-{
-    const uint4 v = shift16(p.lo, p.hi, p.sh);
-    uint32_t m;
-    m = byte_mask(0, p.fv, p.lv); acc.x = (acc.x & ~m) | (v.x & m);
-    m = byte_mask(1, p.fv, p.lv); acc.y = (acc.y & ~m) | (v.y & m);
-    m = byte_mask(2, p.fv, p.lv); acc.z = (acc.z & ~m) | (v.z & m);
-    m = byte_mask(3, p.fv, p.lv); acc.w = (acc.w & ~m) | (v.w & m);
-}
-
-__device__ __forceinline__ uint32_t dword_of(const uint4 &v, int j)
-{
-    return j == 0 ? v.x : (j == 1 ? v.y : (j == 2 ? v.z : v.w));
-}
-
-constexpr int kCopyPer = kSub / 64;       // records per lane in a wave's copy prologue
-
-// Largest r in [r, kSub] with s_dst[r] <= pos, given s_dst[r] <= pos: a few
-// linear steps (the usual distance between neighbouring chunks), then a
-// binary search.  Zero-length records are stepped over.
-__device__ __forceinline__ int advance_record(const int32_t *s_dst, int r, int pos)
-{
-#pragma unroll 1
-    for (int step = 0; step < 6; ++step) {
-        if (s_dst[r + 1] > pos) return r;
-        ++r;
-    }
-    int rl = r, rh = kSub + 1;
-    while (rh - rl > 1) {
-        const int mid = (rl + rh) >> 1;
-        if (s_dst[mid] <= pos) rl = mid; else rh = mid;
-    }
-    return rl;
-}
-
-// Store the bytes [b0, b1) (0..16) of a 16-byte chunk value at A.
-__device__ __forceinline__ void store_partial(uint64_t A, const uint4 &v, int b0, int b1)
-{
-    for (int b = b0; b < b1; ++b) st8(A + (uint64_t)b, (uint8_t)(dword_of(v, b >> 2) >> (8 * (b & 3))));
-}
-
-// One unit's window of a sub-tile (at most 1 GiB): positions relative to the
-// window start fit in 32 bits.  The wave sweeps its window 1 KiB at a time,
-// lane `lane` taking chunk 64*g + lane, so the record each lane reads from
-// only moves forward.  Every chunk strictly inside the window is written with
-// one aligned 16-byte store; chunks that straddle records are assembled from
-// their pieces first, with all of their loads in flight together.
-__device__ __forceinline__ void copy_window32(const int32_t *s_dst, const uint64_t *s_src, int tot,
-                                              uint64_t outa, int64_t D0, int lane)
-{
-    const uint64_t a0 = (outa + (uint64_t)D0) & ~(uint64_t)15;
-    const uint64_t a1 = (outa + (uint64_t)(D0 + tot) - 1) & ~(uint64_t)15;
-    const int nchunks = (int)((a1 - a0) >> 4) + 1;
-    const int xbase = (int)((int64_t)(a0 - outa) - D0);     // -15..0
-    int r = 0;
-    for (int ch = lane; ch < nchunks; ch += 64) {
-        const int x = xbase + ch * 16;
-        const int lo = x > 0 ? x : 0;
-        const int hi = x + 16 < tot ? x + 16 : tot;
-        r = advance_record(s_dst, r, lo);
-        const int d1 = s_dst[r + 1];
-        const int e1 = hi < d1 ? hi : d1;
-        Piece p;
-        piece_load(p, s_src[r] + (uint64_t)(int64_t)(x - s_dst[r]), lo - x, e1 - 1 - x);
-        uint4 acc = make_uint4(0u, 0u, 0u, 0u);
-        if (e1 < hi) {
-            // the chunk also holds the start of the next record(s)
-            int q = advance_record(s_dst, r, e1);
-            int e = e1;
-            while (e < hi) {
-                const int dq = s_dst[q + 1];
-                const int e2 = hi < dq ? hi : dq;
-                Piece pq;
-                piece_load(pq, s_src[q] + (uint64_t)(int64_t)(x - s_dst[q]), e - x, e2 - 1 - x);
-                piece_merge(acc, pq);
-                e = e2;
-                if (e < hi) q = advance_record(s_dst, q, e);
-            }
-            r = q;
-        }
-        piece_merge(acc, p);
-        const uint64_t A = outa + (uint64_t)(D0 + x);
-        if (lo == x && hi == x + 16) st16(A, acc);
-        else store_partial(A, acc, lo - x, hi - x);     // first or last chunk of the window
-    }
-}
-
 // First sub-tile whose output holds byte `lo`: the largest s in [0, nsub)
 // with sub_base[s] <= lo (sub_base[0] = 0).
 __device__ __forceinline__ int64_t find_sub_tile(const int64_t *__restrict__ sub_base, int64_t nsub, int64_t lo)
 {
     return wave_last_le(sub_base, 0, nsub, lo);
 }
-
-// Output bytes are split into units of G bytes (the last one shorter), cut
-// where the destination address is 16-byte aligned, so that unit edges need
-// no partial stores.  G is chosen from the total so that every wave of the
-// grid gets about kCopyUnits units, but never under kCopyMinUnit bytes (a
-// unit re-reads the slot descriptors of the sub-tiles it touches) nor over
-// 1 GiB (positions inside a unit are 32-bit).
-#ifndef RO_COPY_UNITS
-#define RO_COPY_UNITS 2
-#endif
-#ifndef RO_COPY_MIN_UNIT
-#define RO_COPY_MIN_UNIT 4096
-#endif
-constexpr int64_t kCopyUnits = RO_COPY_UNITS;
-constexpr int64_t kCopyMinUnit = RO_COPY_MIN_UNIT;
 
 // Each wave works alone on its units of output bytes, with no workgroup
 // barrier.  For each sub-tile of kSub canonical children that a unit touches,
@@ -537,17 +334,12 @@ constexpr int64_t kCopyMinUnit = RO_COPY_MIN_UNIT;
 // before it), and writes that range with aligned 16-byte stores.  Byte-sized
 // units keep the chip busy whether the records are a few bytes or megabytes
 // long, and few parents or many.
-#ifndef RO_COPY_WAVES
-#define RO_COPY_WAVES 4
-#endif
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_WAVES))) void k_gather_copy(
-    const int64_t *__restrict__ offsets, int64_t P_arg, const int64_t *__restrict__ P_dev,
-    const uint32_t *__restrict__ vmap, uint32_t epoch_arg, const Canon *__restrict__ canon, int64_t canon_cap,
+    const int64_t *__restrict__ offsets, int64_t P, const Canon *__restrict__ canon, int64_t canon_cap,
     const int64_t *__restrict__ sub_base, uint8_t *__restrict__ out, int in_place, Ctl *ctl)
 {
     constexpr int kWaves = kBlock / 64;
-    const int64_t P = P_dev ? *P_dev : P_arg;
-    const uint32_t epoch = epoch_arg ? epoch_arg : ctl->canon_epoch;
+    const uint32_t epoch = ctl->canon_epoch;
     __shared__ int32_t s_dst_all[kWaves][kSub + 1];     // clipped destination offset of each record
     __shared__ uint64_t s_src_all[kWaves][kSub];        // source address of its first clipped byte
     if (read_err(ctl) != 0) return;                      // any recorded error: copy nothing
@@ -559,10 +351,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_
     const uint64_t outa = reinterpret_cast<uint64_t>(out);
     const int64_t mis = (int64_t)(outa & 15);
     const int64_t nwaves = (int64_t)gridDim.x * kWaves;
-    int64_t G = (T + nwaves * kCopyUnits - 1) / (nwaves * kCopyUnits);
-    G = (G + 1023) & ~(int64_t)1023;
-    G = G < kCopyMinUnit ? kCopyMinUnit : (G > ((int64_t)1 << 30) ? ((int64_t)1 << 30) : G);
-    const int64_t nunits = (T + mis + G - 1) / G;
+    int64_t G, nunits;
+    copy_units(T, nwaves, mis, G, nunits);
     const int wave = (int)(threadIdx.x >> 6), lane = lane_id();
     int32_t *s_dst = s_dst_all[wave];
     uint64_t *s_src = s_src_all[wave];
@@ -584,7 +374,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_
                 l[k] = 0;
                 s[k] = 0;
                 if (r < cnt) {
-                    const Canon e = canon[vmap ? (int64_t)vmap[c0 + r] : c0 + r];
+                    const Canon e = canon[c0 + r];
                     if (e.tag == ((epoch << 2) | RO_SUCCESS)) {
                         l[k] = e.len;
                         s[k] = e.src;
@@ -634,8 +424,7 @@ hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w
               a.nk, L.ctl);
     const int64_t grid_s = (int64_t)L.num_cus * 4;
     RO_LAUNCH(L, RO_K_GATHER_SCAN, k_gather_scan, dim3((unsigned)grid_s), dim3(kBlock), 0, L.stream, a.offsets, a.P,
-              (const int64_t *)nullptr, (const uint32_t *)nullptr, 0u, w.canon, w.canon_cap, a.out_off, a.ns,
-              a.nf, a.nk, a.cdst, w.sub_base, L.ctl, L.desc, L.desc_cap);
+              w.canon, w.canon_cap, a.out_off, a.ns, a.nf, a.nk, a.cdst, w.sub_base, L.ctl, L.desc, L.desc_cap);
     int64_t grid_f = (a.P + kBlock - 1) / kBlock;
     grid_f = grid_f < 1 ? 1 : (grid_f > (int64_t)L.num_cus * 8 ? (int64_t)L.num_cus * 8 : grid_f);
     RO_LAUNCH(L, RO_K_GATHER_FINALIZE, k_gather_finalize, dim3((unsigned)grid_f), dim3(kBlock), 0, L.stream, a.offsets,
@@ -644,32 +433,9 @@ hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w
     if (a.out_data != nullptr) {
         const int64_t grid_c = (int64_t)L.num_cus * 8;
         RO_LAUNCH(L, RO_K_GATHER_COPY, k_gather_copy, dim3((unsigned)grid_c), dim3(kBlock), 0, L.stream, a.offsets,
-                  a.P, (const int64_t *)nullptr, (const uint32_t *)nullptr, 0u, w.canon, w.canon_cap, w.sub_base,
-                  a.out_data, a.out_data == a.data ? 1 : 0, L.ctl);
+                  a.P, w.canon, w.canon_cap, w.sub_base, a.out_data, a.out_data == a.data ? 1 : 0, L.ctl);
     }
     RO_LAUNCH(L, RO_K_GATHER_RESET, k_gather_reset, dim3(1), dim3(64), 0, L.stream, L.ctl);
-    return hipGetLastError();
-}
-
-// The streaming emission's pass over its virtual expansion (emitted parents'
-// children): byte scan into emitted slot offsets, then the ordered copy.
-hipError_t launch_virtual_scan(const Launch &L, const int64_t *voff, const int64_t *E_dev, const uint32_t *vmap,
-                               const Canon *canon, int64_t canon_cap, int64_t *emit_off, int32_t *ns,
-                               int32_t *nf, int32_t *nk, int64_t *sub_base)
-{
-    const int64_t grid_s = (int64_t)L.num_cus * 4;
-    RO_LAUNCH(L, RO_K_STREAM_SCAN, k_gather_scan, dim3((unsigned)grid_s), dim3(kBlock), 0, L.stream, voff,
-              (int64_t)0, E_dev, vmap, 1u, canon, canon_cap, emit_off, ns, nf, nk, (int64_t *)nullptr, sub_base,
-              L.ctl, L.desc, L.desc_cap);
-    return hipGetLastError();
-}
-
-hipError_t launch_virtual_copy(const Launch &L, const int64_t *voff, const int64_t *E_dev, const uint32_t *vmap,
-                               const Canon *canon, int64_t canon_cap, const int64_t *sub_base, uint8_t *out)
-{
-    const int64_t grid_c = (int64_t)L.num_cus * 8;
-    RO_LAUNCH(L, RO_K_STREAM_COPY, k_gather_copy, dim3((unsigned)grid_c), dim3(kBlock), 0, L.stream, voff,
-              (int64_t)0, E_dev, vmap, 1u, canon, canon_cap, sub_base, out, 0, L.ctl);
     return hipGetLastError();
 }
 

@@ -7,38 +7,59 @@
 // facts are published once and conflicting repeats are rejected (Sec. 4,
 // publication rules).
 //
-// Per wave:   report  -> canonical slots + seen bits + one count per report.
+// Per wave:   report  -> canonical slots + seen bits (+ a count for parents
+//                        with many children).
 // Per emit:   select  -> ascending list of newly complete parents and the
 //                        exclusive scan of their child counts (two look-back
 //                        chains in one pass over all parents): a "virtual"
 //                        expansion whose children are the emitted parents'
 //                        children, in order;
-//             vmap    -> canonical slot of every virtual child;
-//             then the gather's canonical scan (slot offsets and per-state
-//             counts of the emitted parents) and copy kernels run over the
-//             virtual expansion, and finish closes the call.
-#include "ro_device.h"
+//             scan    -> over the virtual children: each one's canonical slot,
+//                        output position and source, the emitted slot
+//                        offsets and per-state counts;
+//             out     -> counts, states, trailing offsets, capacity, and the
+//                        emitted bytes from the per-child positions.
+#include "ro_copy.h"
 
 namespace ro {
 
 constexpr uint32_t kStreamEpoch = 1;      // slot tag epoch of an accepted stream report
 
-// Reports of a parent with many children would all add to one counter, and
-// atomics on one address serialise.  A parent with at least kBig children
-// counts into kSpread counters on separate lines instead, indexed by its
-// first child >> kBigShift (two such parents never share that index, since
-// each spans kBig children or more).
-constexpr int kBigShift = 10;
-constexpr int64_t kBig = (int64_t)1 << kBigShift;
+// How many children of a parent have reported, by its size k:
+//   k < kMid   the seen bits of its children (at most three words), no counter;
+//   k < kBig   one counter, indexed by its first child >> kMidShift;
+//   k >= kBig  kSpread counters on separate lines, indexed by its first
+//              child >> kBigShift: the reports of a parent with many children
+//              would otherwise all add to one address, and atomics on one
+//              address serialise.
+// A parent of at least 2^s children is the only one whose first child falls
+// in its 2^s-child block, so these indices never collide.
+constexpr int kMidShift = 6, kBigShift = 10;
+constexpr int64_t kMid = (int64_t)1 << kMidShift, kBig = (int64_t)1 << kBigShift;
 constexpr int kSpread = 16;
 
+int64_t stream_mid_size(int64_t N) { return (N >> kMidShift) + 1; }
 int64_t stream_big_slots(int64_t N) { return (N >> kBigShift) + 1; }
 int64_t stream_big_size(int64_t N) { return (int64_t)kSpread * stream_big_slots(N); }
 
-__device__ __forceinline__ int64_t reported(const int32_t *__restrict__ cnt, const int32_t *__restrict__ big,
-                                            int64_t nslots, int64_t p, int64_t st, int64_t k)
+__device__ __forceinline__ int64_t reported(const uint32_t *__restrict__ seen, const int32_t *__restrict__ mid,
+                                            const int32_t *__restrict__ big, int64_t nslots, int64_t st,
+                                            int64_t k)
 {
-    if (k < kBig) return cnt[p];
+    if (k <= 0) return 0;
+    if (k < kMid) {
+        const int64_t c1 = st + k;                  // children [st, c1)
+        int64_t n = 0;
+        for (int64_t w = st >> 5; w <= (c1 - 1) >> 5; ++w) {
+            uint32_t m = seen[w];
+            const int64_t b0 = w << 5;
+            if (st > b0) m &= 0xffffffffu << (st - b0);
+            if (c1 < b0 + 32) m &= 0xffffffffu >> (b0 + 32 - c1);
+            n += __popc(m);
+        }
+        return n;
+    }
+    if (k < kBig) return mid[st >> kMidShift];
     const int64_t j = st >> kBigShift;
     int64_t s = 0;
 #pragma unroll
@@ -59,7 +80,7 @@ __global__ void k_stream_check(const int64_t *__restrict__ offsets, int64_t P, i
 __global__ __launch_bounds__(kBlock) void k_stream_report(
     const uint32_t *__restrict__ rp, const uint32_t *__restrict__ ro_, const uint8_t *__restrict__ rs,
     const int64_t *__restrict__ roff, const uint8_t *data, int64_t n, const int64_t *__restrict__ offsets,
-    int64_t P, int64_t N, Canon *__restrict__ canon, uint32_t *__restrict__ seen, int32_t *__restrict__ cnt,
+    int64_t P, int64_t N, Canon *__restrict__ canon, uint32_t *__restrict__ seen, int32_t *__restrict__ mid,
     int32_t *__restrict__ big, int64_t nslots, Ctl *ctl)
 {
     const int64_t gtid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
@@ -92,19 +113,23 @@ __global__ __launch_bounds__(kBlock) void k_stream_report(
         e.len = (uint32_t)len;
         e.tag = (kStreamEpoch << 2) | s;
         canon[c] = e;
-        if (k < kBig) atomicAdd(&cnt[p], 1);
-        else atomicAdd(&big[spread + (st >> kBigShift)], 1);
+        if (k >= kBig) atomicAdd(&big[spread + (st >> kBigShift)], 1);
+        else if (k >= kMid) atomicAdd(&mid[st >> kMidShift], 1);
     }
     if (err) raise_err(ctl, err);
 }
 
-// Newly complete parents, compacted in ascending order (one tile = 4096
-// parents), and the exclusive scan of their child counts: two look-back
-// chains, one over emitted parents and one over their children.
+// Newly complete parents, compacted in ascending order (one tile = 2048
+// parents, eight per thread), and the exclusive scan of their child counts:
+// two look-back chains, one over emitted parents and one over their children.
+constexpr int kSTile = 2048;
+constexpr int kSItems = kSTile / kBlock;
+
 __global__ __launch_bounds__(kBlock) void k_stream_select(
-    const int64_t *__restrict__ offsets, int64_t P, const int32_t *__restrict__ cnt,
-    const int32_t *__restrict__ big, int64_t nslots, uint8_t *__restrict__ emitted,
-    uint32_t *__restrict__ elist, int64_t *__restrict__ evoff, uint32_t *__restrict__ emit_parent,
+    const int64_t *__restrict__ offsets, int64_t P, const uint32_t *__restrict__ seen,
+    const int32_t *__restrict__ mid, const int32_t *__restrict__ big, int64_t nslots,
+    uint8_t *__restrict__ emitted,
+    int64_t *__restrict__ ebase, int64_t *__restrict__ evoff, uint32_t *__restrict__ emit_parent,
     int32_t *__restrict__ ecnt, int64_t ecnt_stride, int64_t cap_parents, int64_t *n_emitted, Ctl *ctl,
     uint64_t *desc, uint64_t *desc_kids, int64_t desc_cap, int64_t ntiles)
 {
@@ -116,18 +141,18 @@ __global__ __launch_bounds__(kBlock) void k_stream_select(
     for (;;) {
         const int64_t t = next_ticket(ctl, &s_t);
         if (t >= ntiles) break;
-        const int64_t p0 = t * kTile + (int64_t)threadIdx.x * kItems;
+        const int64_t p0 = t * kSTile + (int64_t)threadIdx.x * kSItems;
         uint32_t fmask = 0;
-        uint32_t kk[kItems];
+        uint32_t kk[kSItems];
         int64_t kids = 0;
 #pragma unroll
-        for (int k = 0; k < kItems; ++k) {
+        for (int k = 0; k < kSItems; ++k) {
             const int64_t p = p0 + k;
             kk[k] = 0;
             if (p < P && !emitted[p]) {
                 const int64_t st = offsets[p];
                 const int64_t kp = offsets[p + 1] - st;
-                if (reported(cnt, big, nslots, p, st, kp) == kp) {
+                if (reported(seen, mid, big, nslots, st, kp) == kp) {
                     fmask |= 1u << k;
                     kk[k] = (uint32_t)kp;
                     kids += kp;
@@ -143,11 +168,11 @@ __global__ __launch_bounds__(kBlock) void k_stream_select(
         int64_t run = (int64_t)prek + exk;
         bool over = false;
 #pragma unroll
-        for (int k = 0; k < kItems; ++k) {
+        for (int k = 0; k < kSItems; ++k) {
             if (!(fmask & (1u << k))) continue;
             const int64_t p = p0 + k;
             if (e < cap_parents) {
-                elist[e] = (uint32_t)p;
+                ebase[e] = offsets[p] - run;      // canonical slot of virtual child v: ebase[e] + v
                 evoff[e] = run;
                 if (emit_parent) emit_parent[e] = (uint32_t)p;
                 ecnt[e] = 0;
@@ -179,84 +204,246 @@ __global__ __launch_bounds__(kBlock) void k_stream_select(
     ticket_done(ctl, epoch, desc, desc_cap, &s_last);
 }
 
-// vmap[v] = canonical slot of virtual child v: the (v - evoff[e])-th child of
-// emitted parent elist[e].  16 consecutive virtual children per thread.
-__global__ __launch_bounds__(kBlock) void k_stream_vmap(const int64_t *__restrict__ evoff,
-                                                        const uint32_t *__restrict__ elist,
-                                                        const int64_t *__restrict__ offsets,
-                                                        uint32_t *__restrict__ vmap, Ctl *ctl)
+// Byte scan over the virtual children of this emission, 1024 per tile (four
+// consecutive per thread; small tiles spread the random slot reads over many
+// compute units).  Virtual child v of emitted parent e lives in canonical
+// slot ebase[e] + v.  Writes each child's output position edst[v] and source
+// address esrc[v] for the copy, the emitted slot offsets, and per-state
+// counts (run lengths, aggregated in LDS).  Only the first min(grid, tiles)
+// workgroups take part.
+constexpr int kETile = 1024;
+constexpr int kEItems = kETile / kBlock;
+constexpr int kECntLds = 256;
+
+__global__ __launch_bounds__(kBlock) void k_emit_scan(
+    const int64_t *__restrict__ evoff, const int64_t *__restrict__ ebase, const Canon *__restrict__ canon,
+    int64_t *__restrict__ edst, uint64_t *__restrict__ esrc, int64_t *__restrict__ emit_off,
+    int32_t *__restrict__ ecnt, int64_t ecnt_stride, Ctl *ctl, uint64_t *desc, int64_t desc_cap)
 {
     const int64_t E = ctl->n_items;
     const int64_t V = ctl->n_virtual;
-    const int64_t nthreads = (V + kItems - 1) / kItems;
-    for (int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x; g < nthreads;
-         g += (int64_t)gridDim.x * kBlock) {
-        const int64_t v0 = g * kItems;
-        int64_t e = upper_bound_g(evoff, 0, E + 1, v0) - 1;
-        int64_t start = evoff[e];
-        int64_t base = offsets[elist[e]];
-        for (int k = 0; k < kItems; ++k) {
-            const int64_t v = v0 + k;
-            if (v >= V) break;
-            if (v >= evoff[e + 1]) {
-                e = advance_parent(evoff, E, e, v);
-                start = evoff[e];
-                base = offsets[elist[e]];
-            }
-            vmap[v] = (uint32_t)(base + (v - start));
+    const int64_t ntiles = (V + kETile - 1) / kETile;
+    if ((int64_t)blockIdx.x >= ntiles) return;
+    const uint32_t parts = (uint32_t)min64((int64_t)gridDim.x, ntiles);
+    const uint32_t sepoch = scan_epoch(ctl);
+    __shared__ int64_t s_wave[kBlock / 64];
+    __shared__ uint64_t s_b;
+    __shared__ int64_t s_t;
+    __shared__ int32_t s_last;
+    __shared__ int64_t s_p[3];
+    __shared__ int16_t s_off[kETile + 2];         // evoff[pf..pl+1] - vt0, clamped to [-1, kETile + 1]
+    __shared__ int64_t s_base[kETile + 1];        // ebase[pf..pl]
+    __shared__ int32_t s_cnt[3][kECntLds];
+    for (;;) {
+        const int64_t t = next_ticket(ctl, &s_t);
+        if (t >= ntiles) break;
+        const int64_t vt0 = t * kETile;
+        const int64_t vt1 = min64(vt0 + kETile, V);
+        // emitted parents of the tile: pf holds child vt0, pl holds vt1 - 1,
+        // q0 is the first one starting at or after vt0
+        if (threadIdx.x < 3 * 64) {
+            const int w = (int)(threadIdx.x >> 6);
+            int64_t r;
+            if (w == 0) r = wave_last_le(evoff, 0, E + 1, vt0);
+            else if (w == 1) r = wave_last_le(evoff, 0, E + 1, vt1 - 1);
+            else r = vt0 == 0 ? 0 : wave_last_le(evoff, 0, E + 1, vt0 - 1) + 1;
+            if (lane_id() == 0) s_p[w] = r;
         }
+        __syncthreads();
+        const int64_t pf = s_p[0], pl = s_p[1], q0t = s_p[2];
+        const int64_t Rp = pl - pf + 1;
+        const int64_t R = min64(Rp, kECntLds);
+        const bool lds_ok = Rp <= kETile;
+        if (lds_ok) {
+            for (int64_t j = threadIdx.x; j <= Rp; j += kBlock) {
+                const int64_t x = evoff[pf + j] - vt0;
+                s_off[j] = (int16_t)(x < -1 ? -1 : (x > kETile + 1 ? kETile + 1 : x));
+                if (j < Rp) s_base[j] = ebase[pf + j];
+            }
+        }
+        for (int j = threadIdx.x; j < 3 * kECntLds; j += kBlock) (&s_cnt[0][0])[j] = 0;
+        __syncthreads();
+        // this thread's four virtual children: slot, length, state, source
+        const int64_t v0 = vt0 + (int64_t)threadIdx.x * kEItems;
+        int64_t e0 = 0;
+        uint32_t len[kEItems], stv[kEItems];
+        uint64_t src[kEItems];
+        int64_t sum = 0;
+#pragma unroll
+        for (int k = 0; k < kEItems; ++k) {
+            len[k] = 0;
+            stv[k] = 4;
+            src[k] = 0;
+        }
+        if (v0 < vt1) {
+            int64_t e = lds_ok ? pf + lds_last_le(s_off, 0, (int)Rp, (int)(v0 - vt0))
+                               : upper_bound_g(evoff, pf, pl + 1, v0) - 1;
+            e0 = e;
+#pragma unroll
+            for (int k = 0; k < kEItems; ++k) {
+                const int64_t v = v0 + k;
+                if (v >= vt1) break;
+                if (lds_ok) {
+                    const int rv = (int)(v - vt0);
+                    if (rv >= s_off[e - pf + 1]) e = pf + lds_last_le(s_off, (int)(e - pf) + 1, (int)Rp, rv);
+                } else if (v >= evoff[e + 1]) {
+                    e = advance_parent(evoff, E, e, v);
+                }
+                const int64_t c = (lds_ok ? s_base[e - pf] : ebase[e]) + v;
+                const Canon x = canon[c];
+                if ((x.tag >> 2) == kStreamEpoch) {
+                    stv[k] = x.tag & 3u;
+                    len[k] = stv[k] == RO_SUCCESS ? x.len : 0;
+                    src[k] = x.src;
+                }
+                sum += len[k];
+            }
+        }
+        int64_t tot;
+        const int64_t ex = block_excl_scan(sum, s_wave, tot);
+        const uint64_t pre = tile_prefix(desc, t, sepoch, (uint64_t)tot, &s_b, ctl);
+        if (v0 < vt1) {
+            int64_t pos = (int64_t)pre + ex;
+            int64_t e = e0;
+            int32_t run[3] = {0, 0, 0};
+            auto flush = [&](int64_t q) {
+#pragma unroll
+                for (int s = 0; s < 3; ++s) {
+                    if (run[s]) {
+                        if (q - pf < R) atomicAdd(&s_cnt[s][q - pf], run[s]);
+                        else atomicAdd(&ecnt[s * ecnt_stride + q], run[s]);
+                        run[s] = 0;
+                    }
+                }
+            };
+            // emitted parents whose first child is v0 (empty ones included)
+            if (evoff[e] == v0) {
+                const int64_t qa = v0 == vt0 ? q0t : lower_bound_g(evoff, pf, e + 1, v0);
+                for (int64_t q = qa; q <= e; ++q) emit_off[q] = pos;
+            }
+#pragma unroll
+            for (int k = 0; k < kEItems; ++k) {
+                const int64_t v = v0 + k;
+                if (v >= vt1) break;
+                if (v >= evoff[e + 1]) {
+                    flush(e);
+                    const int64_t en = advance_parent(evoff, E, e, v);
+                    for (int64_t q = e + 1; q <= en; ++q) emit_off[q] = pos;
+                    e = en;
+                }
+                if (stv[k] < 3) run[stv[k]] += 1;
+                edst[v] = pos;
+                esrc[v] = src[k];
+                pos += len[k];
+            }
+            flush(e);
+        }
+        __syncthreads();
+        for (int64_t j = threadIdx.x; j < R; j += kBlock) {
+#pragma unroll
+            for (int s = 0; s < 3; ++s) {
+                const int32_t x = s_cnt[s][j];
+                if (x) atomicAdd(&ecnt[s * ecnt_stride + pf + j], x);
+            }
+        }
+        if (t == ntiles - 1 && threadIdx.x == 0) {
+            const int64_t total = (int64_t)pre + tot;
+            ctl->total = total;
+            edst[V] = total;
+            if (pre >= kSat) raise_err(ctl, RO_EOVERFLOW);
+        }
+        __syncthreads();
     }
+    ticket_done_n(ctl, sepoch, desc, desc_cap, &s_last, parts);
 }
 
-// After the scan: counts and state of every emitted parent, trailing slot
-// offsets, capacity check (before the copy).
-__global__ void k_stream_emit_check(int64_t *__restrict__ emit_off, const int64_t *__restrict__ evoff,
-                                    const int32_t *__restrict__ ecnt, int64_t ecnt_stride,
-                                    int32_t *__restrict__ ns, int32_t *__restrict__ nf, int32_t *__restrict__ nk,
-                                    uint8_t *__restrict__ pstate, int64_t cap_bytes, int has_data,
-                                    int64_t *n_bytes, Ctl *ctl)
+// Outputs of the emission once its scan is done: per emitted parent its
+// counts, state and (for parents without children at the very end) slot
+// offset; then the bytes.  The output is cut into byte units as in the
+// gather's copy, kEmitMinUnit bytes or more (a unit costs a search over the
+// positions, not a re-read of slot records, so small units pay here); a unit
+// finds its first child by a wave search over the output positions and takes
+// the children it covers 256 at a time, each clipped to the unit.
+constexpr int64_t kEmitMinUnit = 1024;
+
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_WAVES))) void k_emit_out(
+    int64_t *__restrict__ emit_off, const int64_t *__restrict__ evoff, const int32_t *__restrict__ ecnt,
+    int64_t ecnt_stride, int32_t *__restrict__ ns, int32_t *__restrict__ nf, int32_t *__restrict__ nk,
+    uint8_t *__restrict__ pstate, int64_t *n_bytes, const int64_t *__restrict__ edst,
+    const uint64_t *__restrict__ esrc, uint8_t *__restrict__ out, int64_t cap_bytes, Ctl *ctl)
 {
+    constexpr int kWaves = kBlock / 64;
+    __shared__ int32_t s_dst_all[kWaves][kSub + 1];
+    __shared__ uint64_t s_src_all[kWaves][kSub];
     const int64_t E = ctl->n_items;
     const int64_t V = ctl->n_virtual;
-    const int64_t total = V > 0 ? ctl->total : 0;
+    const int64_t T = V > 0 ? ctl->total : 0;
     const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (g == 0) {
-        emit_off[E] = total;
-        if (n_bytes) *n_bytes = total;
-        if (has_data && total > cap_bytes) raise_err(ctl, RO_ECAP);
+        emit_off[E] = T;
+        if (n_bytes) *n_bytes = T;
+        if (out && T > cap_bytes) raise_err(ctl, RO_ECAP);
     }
     for (int64_t e = g; e < E; e += (int64_t)gridDim.x * blockDim.x) {
-        // emitted parents without children at the very end get the total
-        if (evoff[e] >= V) emit_off[e] = total;
-        const int32_t a = ecnt[e], f = ecnt[ecnt_stride + e], s = ecnt[2 * ecnt_stride + e];
+        if (evoff[e] >= V) emit_off[e] = T;
+        const int32_t a = ecnt[e], f = ecnt[ecnt_stride + e], k = ecnt[2 * ecnt_stride + e];
         if (ns) ns[e] = a;
         if (nf) nf[e] = f;
-        if (nk) nk[e] = s;
+        if (nk) nk[e] = k;
         if (pstate) pstate[e] = f > 0 ? RO_FAILED : RO_SUCCESS;
     }
-}
-
-__global__ void k_stream_finish(Ctl *ctl)
-{
-    if (threadIdx.x == 0) {
-        ctl->n_items = 0;
-        ctl->n_virtual = 0;
-        ctl->total = 0;
-        ctl->n_filled = 0;    // counted by the canonical scan, unused here
+    if (out == nullptr || T <= 0 || T > cap_bytes || read_err(ctl) != 0) return;
+    const uint64_t outa = reinterpret_cast<uint64_t>(out);
+    const int64_t mis = (int64_t)(outa & 15);
+    const int64_t nwaves = (int64_t)gridDim.x * kWaves;
+    int64_t G = (T + nwaves * kCopyUnits - 1) / (nwaves * kCopyUnits);
+    G = (G + 15) & ~(int64_t)15;
+    G = G < kEmitMinUnit ? kEmitMinUnit : (G > ((int64_t)1 << 30) ? ((int64_t)1 << 30) : G);
+    const int64_t nunits = (T + mis + G - 1) / G;
+    const int wave = (int)(threadIdx.x >> 6), lane = lane_id();
+    int32_t *s_dst = s_dst_all[wave];
+    uint64_t *s_src = s_src_all[wave];
+    for (int64_t u = (int64_t)blockIdx.x * kWaves + wave; u < nunits; u += nwaves) {
+        const int64_t lo = max64(u * G - mis, 0);
+        const int64_t hi = min64((u + 1) * G - mis, T);
+        for (int64_t r0 = wave_last_le(edst, 0, V, lo); r0 < V; r0 += kSub) {
+            // children r0 .. r0 + kSub - 1, their starts clipped to [ws, we)
+            const int64_t dend = edst[min64(r0 + kSub, V)];
+            const int64_t ws = max64(lo, edst[r0]);
+            const int64_t we = min64(hi, dend);
+            if (we <= ws) {
+                if (dend >= hi) break;
+                continue;                          // only empty children here
+            }
+#pragma unroll
+            for (int k = 0; k < kSub / 64; ++k) {
+                const int i = k * 64 + lane;
+                const int64_t v = r0 + i;
+                const int64_t d = v < V ? edst[v] : T;
+                const int64_t cs = min64(max64(d, ws), we);
+                s_dst[i] = (int32_t)(cs - ws);
+                s_src[i] = (v < V ? esrc[v] : 0) + (uint64_t)(cs - d);
+            }
+            if (lane == 0) s_dst[kSub] = (int32_t)(we - ws);
+            __builtin_amdgcn_wave_barrier();
+            copy_window32(s_dst, s_src, (int)(we - ws), outa, ws, lane);
+            __builtin_amdgcn_wave_barrier();
+            if (dend >= hi) break;
+        }
     }
 }
 
 // Forgets every report and emission: seen bits, counters and emitted flags
 // back to zero.  Canonical slots need no clearing, since a slot is read only
 // for children of emitted parents, and those were all reported.
-__global__ void k_stream_clear(uint32_t *__restrict__ seen, int64_t n_seen, int32_t *__restrict__ cnt,
-                               int64_t n_cnt, int32_t *__restrict__ big, int64_t n_big,
+__global__ void k_stream_clear(uint32_t *__restrict__ seen, int64_t n_seen, int32_t *__restrict__ mid,
+                               int64_t n_mid, int32_t *__restrict__ big, int64_t n_big,
                                uint8_t *__restrict__ emitted, int64_t n_emitted)
 {
     const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = g; i < n_seen; i += stride) seen[i] = 0;
-    for (int64_t i = g; i < n_cnt; i += stride) cnt[i] = 0;
+    for (int64_t i = g; i < n_mid; i += stride) mid[i] = 0;
     for (int64_t i = g; i < n_big; i += stride) big[i] = 0;
     for (int64_t i = g; i < n_emitted; i += stride) emitted[i] = 0;
 }
@@ -264,7 +451,7 @@ __global__ void k_stream_clear(uint32_t *__restrict__ seen, int64_t n_seen, int3
 hipError_t launch_stream_reset(const Launch &L, StreamState &s)
 {
     RO_LAUNCH(L, RO_K_MISC, k_stream_clear, dim3((unsigned)L.num_cus * 4), dim3(256), 0, L.stream, s.seen,
-              (s.N + 31) / 32 + 1, s.cnt, s.P + 1, s.big, stream_big_size(s.N), s.emitted, s.P + 1);
+              (s.N + 31) / 32 + 1, s.mid, stream_mid_size(s.N), s.big, stream_big_size(s.N), s.emitted, s.P + 1);
     return launch_stream_init(L, s);
 }
 
@@ -281,20 +468,14 @@ hipError_t launch_stream_report(const Launch &L, StreamState &s, const uint32_t 
     int64_t grid = (n + kBlock - 1) / kBlock;
     grid = grid < 1 ? 1 : (grid > (int64_t)L.num_cus * 8 ? (int64_t)L.num_cus * 8 : grid);
     RO_LAUNCH(L, RO_K_STREAM_REPORT, k_stream_report, dim3((unsigned)grid), dim3(kBlock), 0, L.stream, rp, ro,
-              rs, roff, data, n, s.offsets, s.P, s.N, s.canon, s.seen, s.cnt, s.big, stream_big_slots(s.N),
+              rs, roff, data, n, s.offsets, s.P, s.N, s.canon, s.seen, s.mid, s.big, stream_big_slots(s.N),
               L.ctl);
     return hipGetLastError();
 }
 
-hipError_t launch_virtual_scan(const Launch &L, const int64_t *voff, const int64_t *E_dev, const uint32_t *vmap,
-                               const Canon *canon, int64_t canon_cap, int64_t *emit_off, int32_t *ns,
-                               int32_t *nf, int32_t *nk, int64_t *sub_base);
-hipError_t launch_virtual_copy(const Launch &L, const int64_t *voff, const int64_t *E_dev, const uint32_t *vmap,
-                               const Canon *canon, int64_t canon_cap, const int64_t *sub_base, uint8_t *out);
-
 int64_t stream_desc_tiles(int64_t P, int64_t N)
 {
-    const int64_t tp = (P + kTile - 1) / kTile + 1, tn = (N + kTile - 1) / kTile + 1;
+    const int64_t tp = (P + kSTile - 1) / kSTile + 1, tn = (N + kETile - 1) / kETile + 1;
     return 2 * tp > tn ? 2 * tp : tn;
 }
 
@@ -303,26 +484,19 @@ hipError_t launch_stream_emit(const Launch &L, StreamState &s, uint32_t *emit_pa
                               int32_t *nf, int32_t *nk, uint8_t *pstate, int64_t *n_emitted,
                               int64_t *n_bytes)
 {
-    const int64_t ntiles = s.P > 0 ? (s.P + kTile - 1) / kTile : 1;
-    if (2 * ntiles > L.desc_cap) return hipErrorInvalidValue;
+    const int64_t ntiles = s.P > 0 ? (s.P + kSTile - 1) / kSTile : 1;
+    if (2 * ntiles > L.desc_cap || (s.N + kETile - 1) / kETile > L.desc_cap) return hipErrorInvalidValue;
     const int64_t grid = ntiles < (int64_t)L.num_cus * 4 ? ntiles : (int64_t)L.num_cus * 4;
     const int64_t es = s.P + 1;
     RO_LAUNCH(L, RO_K_STREAM_SELECT, k_stream_select, dim3((unsigned)grid), dim3(kBlock), 0, L.stream,
-              s.offsets, s.P, s.cnt, s.big, stream_big_slots(s.N), s.emitted, s.elist, s.evoff, emit_parent,
+              s.offsets, s.P, s.seen, s.mid, s.big, stream_big_slots(s.N), s.emitted, s.ebase, s.evoff, emit_parent,
               s.ecnt, es, cap_parents, n_emitted, L.ctl, L.desc, L.desc + ntiles, L.desc_cap, ntiles);
-    RO_LAUNCH(L, RO_K_STREAM_SELECT, k_stream_vmap, dim3((unsigned)L.num_cus * 8), dim3(kBlock), 0, L.stream,
-              s.evoff, s.elist, s.offsets, s.vmap, L.ctl);
-    hipError_t e = launch_virtual_scan(L, s.evoff, &L.ctl->n_items, s.vmap, s.canon, s.N, emit_off, s.ecnt,
-                                       s.ecnt + es, s.ecnt + 2 * es, s.sub_base);
-    if (e != hipSuccess) return e;
-    RO_LAUNCH(L, RO_K_STREAM_FINISH, k_stream_emit_check, dim3((unsigned)L.num_cus), dim3(256), 0, L.stream,
-              emit_off, s.evoff, s.ecnt, es, ns, nf, nk, pstate, cap_bytes, emit_data != nullptr ? 1 : 0, n_bytes,
-              L.ctl);
-    if (emit_data != nullptr) {
-        e = launch_virtual_copy(L, s.evoff, &L.ctl->n_items, s.vmap, s.canon, s.N, s.sub_base, emit_data);
-        if (e != hipSuccess) return e;
-    }
-    RO_LAUNCH(L, RO_K_STREAM_FINISH, k_stream_finish, dim3(1), dim3(64), 0, L.stream, L.ctl);
+    const int64_t grid_s = (int64_t)L.num_cus * 2;
+    RO_LAUNCH(L, RO_K_STREAM_SCAN, k_emit_scan, dim3((unsigned)grid_s), dim3(kBlock), 0, L.stream, s.evoff,
+              s.ebase, s.canon, s.edst, s.esrc, emit_off, s.ecnt, es, L.ctl, L.desc, L.desc_cap);
+    const int64_t grid_c = (int64_t)L.num_cus * 8;
+    RO_LAUNCH(L, RO_K_STREAM_COPY, k_emit_out, dim3((unsigned)grid_c), dim3(kBlock), 0, L.stream, emit_off,
+              s.evoff, s.ecnt, es, ns, nf, nk, pstate, n_bytes, s.edst, s.esrc, emit_data, cap_bytes, L.ctl);
     return hipGetLastError();
 }
 

@@ -353,18 +353,17 @@ int ro_stream_create(ro_ctx *c, const int64_t *offsets, int64_t n_parents, int64
     int rc = ensure_desc(c, stream_desc_tiles(P, N));
     if (rc) return rc;
     // one allocation, carved into 256-byte aligned arrays
-    const int64_t subs = (N / kTile + 2) * (kTile / kSub);
     const size_t sizes[] = {
         (size_t)(N > 0 ? N : 1) * sizeof(Canon),            // canon
         (size_t)((N + 31) / 32 + 1) * sizeof(uint32_t),     // seen
-        (size_t)(P + 1) * sizeof(int32_t),                  // cnt
+        (size_t)stream_mid_size(N) * sizeof(int32_t),       // mid
         (size_t)stream_big_size(N) * sizeof(int32_t),       // big
         (size_t)(P + 1),                                    // emitted
-        (size_t)(P + 1) * sizeof(uint32_t),                 // elist
+        (size_t)(P + 1) * sizeof(int64_t),                  // ebase
         (size_t)(P + 2) * sizeof(int64_t),                  // evoff
         (size_t)(3 * (P + 1)) * sizeof(int32_t),            // ecnt
-        (size_t)(N + 1) * sizeof(uint32_t),                 // vmap
-        (size_t)subs * sizeof(int64_t),                     // sub_base
+        (size_t)(N + 1) * sizeof(int64_t),                  // edst
+        (size_t)(N + 1) * sizeof(uint64_t),                 // esrc
     };
     constexpr int kArrays = (int)(sizeof(sizes) / sizeof(sizes[0]));
     size_t offs[kArrays], total = 0;
@@ -392,15 +391,14 @@ int ro_stream_create(ro_ctx *c, const int64_t *offsets, int64_t n_parents, int64
     st.N = N;
     st.canon = (Canon *)(block + offs[0]);
     st.seen = (uint32_t *)(block + offs[1]);
-    st.cnt = (int32_t *)(block + offs[2]);
+    st.mid = (int32_t *)(block + offs[2]);
     st.big = (int32_t *)(block + offs[3]);
     st.emitted = (uint8_t *)(block + offs[4]);
-    st.elist = (uint32_t *)(block + offs[5]);
+    st.ebase = (int64_t *)(block + offs[5]);
     st.evoff = (int64_t *)(block + offs[6]);
     st.ecnt = (int32_t *)(block + offs[7]);
-    st.vmap = (uint32_t *)(block + offs[8]);
-    st.sub_base = (int64_t *)(block + offs[9]);
-    st.sub_cap = subs;
+    st.edst = (int64_t *)(block + offs[8]);
+    st.esrc = (uint64_t *)(block + offs[9]);
     if (launch_stream_init(launch_of(c), st) != hipSuccess) {
         (void)hipFree(block);
         free(s);

@@ -93,17 +93,19 @@ __device__ __forceinline__ void desc_put_raw(uint64_t *d, uint64_t w)
     __hip_atomic_store(d, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Called once by every workgroup after its last tile.  The last one resets
-// the ticket and advances the epoch; when the 16-bit epoch would wrap it
-// first clears every descriptor, so an old descriptor can never carry the
-// epoch of a later launch.
-__device__ __forceinline__ void ticket_done(Ctl *ctl, uint32_t epoch, uint64_t *desc, int64_t desc_cap,
-                                            int32_t *s_last)
+// Called once by every workgroup that takes part, after its last tile: the
+// first `parts` workgroups of the grid (ticket_done: all of them; the others
+// return without drawing a ticket).  The last one resets the ticket and
+// advances the epoch; when the 16-bit epoch would wrap it first clears every
+// descriptor, so an old descriptor can never carry the epoch of a later
+// launch.
+__device__ __forceinline__ void ticket_done_n(Ctl *ctl, uint32_t epoch, uint64_t *desc, int64_t desc_cap,
+                                              int32_t *s_last, uint32_t parts)
 {
     if (threadIdx.x == 0) {
         const uint32_t d = __hip_atomic_fetch_add(&ctl->done, 1u, __ATOMIC_RELAXED,
                                                   __HIP_MEMORY_SCOPE_AGENT);
-        *s_last = (d == gridDim.x - 1) ? 1 : 0;
+        *s_last = (d == parts - 1) ? 1 : 0;
     }
     __syncthreads();
     if (*s_last) {
@@ -118,6 +120,12 @@ __device__ __forceinline__ void ticket_done(Ctl *ctl, uint32_t epoch, uint64_t *
                                __HIP_MEMORY_SCOPE_AGENT);
         }
     }
+}
+
+__device__ __forceinline__ void ticket_done(Ctl *ctl, uint32_t epoch, uint64_t *desc, int64_t desc_cap,
+                                            int32_t *s_last)
+{
+    ticket_done_n(ctl, epoch, desc, desc_cap, s_last, gridDim.x);
 }
 
 // ---- decoupled look-back --------------------------------------------------
@@ -257,6 +265,27 @@ __device__ __forceinline__ int64_t wave_last_le(const int64_t *a, int64_t lo, in
         h = nh;
     }
     return l;
+}
+
+// Searches over tile-relative parent offsets held in LDS.
+// Largest i in [lo, hi) with a[i] <= x, given a[lo] <= x.
+__device__ __forceinline__ int lds_last_le(const int16_t *a, int lo, int hi, int x)
+{
+    while (hi - lo > 1) {
+        const int m = (lo + hi) >> 1;
+        if (a[m] <= x) lo = m; else hi = m;
+    }
+    return lo;
+}
+
+// First i in [lo, hi) with a[i] >= x (hi if none).
+__device__ __forceinline__ int lds_first_ge(const int16_t *a, int lo, int hi, int x)
+{
+    while (lo < hi) {
+        const int m = (lo + hi) >> 1;
+        if (a[m] < x) lo = m + 1; else hi = m;
+    }
+    return lo;
 }
 
 __device__ __forceinline__ int64_t min64(int64_t a, int64_t b) { return a < b ? a : b; }

@@ -112,17 +112,17 @@ struct StreamState {
     int64_t P, N;
     Canon *canon;            // [N] accepted reports (tag epoch 1 = accepted)
     uint32_t *seen;          // [N/32] duplicate detection bitmap
-    int32_t *cnt;            // [P+1] reports per parent (parents with few children)
+    int32_t *mid;            // [stream_mid_size(N)] report counters of parents with 64..1023 children
     int32_t *big;            // [stream_big_size(N)] spread report counters of large parents
     uint8_t *emitted;        // [P]
-    uint32_t *elist;         // [P] emitted parents of the current emission
+    int64_t *ebase;          // [P] per emitted parent: canonical slot of its first child minus evoff
     int64_t *evoff;          // [P+1] child offsets of the emitted parents (virtual children)
     int32_t *ecnt;           // [3*(P+1)] SUCCESS / FAILED / SKIPPED counts per emitted parent
-    uint32_t *vmap;          // [N] canonical slot of each virtual child
-    int64_t *sub_base;       // per sub-tile of virtual children
-    int64_t sub_cap;
+    int64_t *edst;           // [N+1] output position of each virtual child
+    uint64_t *esrc;          // [N] source address of each virtual child's bytes
 };
 
+int64_t stream_mid_size(int64_t N);
 int64_t stream_big_size(int64_t N);
 int64_t stream_desc_tiles(int64_t P, int64_t N);
 hipError_t launch_stream_init(const Launch &L, StreamState &s);

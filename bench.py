@@ -57,14 +57,19 @@ def parse():
 # holding them, and the source they were taken from (a changed source voids
 # the figure)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gather_copy_zipf41M_counters.txt")
-TRAFFIC_SOURCE = os.path.join(ROOT, "paper_2609_18703_amd", "csrc", "k_gather.hip")
+TRAFFIC_SOURCES = [os.path.join(ROOT, "paper_2609_18703_amd", "csrc", f)
+                   for f in ("k_gather.hip", "ro_copy.h", "ro_device.h", "ro_internal.h")]
 TRAFFIC_WORKLOAD = ("zipf-single", "gather_copy")
 
 
-def source_sha256(path):
+def source_sha256(paths=TRAFFIC_SOURCES):
+    """SHA-256 over the copy kernel's sources, concatenated in order."""
     import hashlib
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    h = hashlib.sha256()
+    for path in paths:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def traffic_from_profile():
@@ -77,7 +82,7 @@ def traffic_from_profile():
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             vals[k.strip()] = v.strip()
-    if vals.get("source_sha256") != source_sha256(TRAFFIC_SOURCE):
+    if vals.get("source_sha256") != source_sha256():
         return None
     try:
         return int(vals["calibrated_bytes_per_launch"])

@@ -21,13 +21,24 @@
  *   - Sec. 4 "Scheduling Ready Grains": one FIFO Ready Queue per Call holds
  *     ready Grains in enqueue order; elastic reservation removes at most B
  *     entries from its head and may mix parents.
+ *   - Sec. 4 "Commit, Failure, and Recovery": a typed GroupFailure puts a
+ *     suppression barrier on one (Call, parent): queued siblings are
+ *     suppressed before dispatch, in-flight siblings may finish but cannot
+ *     commit, siblings committed before it stay as they are.
  *
  * Readings where the paper is silent (all listed in the design notes):
  *   state SUCCESS = Present, FAILED = Failed (and Suppressed passed up from a
  *   lower level), SKIPPED = Dropped, PENDING = no report yet; bytes of a
  *   non-SUCCESS report are never copied; a parent with a failed member keeps
  *   its packed surviving bytes and is flagged FAILED; an incomplete parent is
- *   PENDING with the bytes seen so far packed in ordinal order.
+ *   PENDING with the bytes seen so far packed in ordinal order.  Group
+ *   failures: reports commit in the order given (one call or wave after
+ *   another); a GROUP_FAILED report commits as a failed member and bars its
+ *   parent, so every later report of that parent is rejected (not committed,
+ *   not counted, its bytes never copied); a barred parent is complete and
+ *   FAILED, its slot keeps the bytes committed before the barrier; a barred
+ *   parent's queued children are dropped by the batch.  GROUP_FAILED needs a
+ *   barrier array (one per Call); without one it is a bad state.
  *
  * Parity status: every function here is pinned by the CPU test suite (worked
  * examples from the paper's figures, brute-force enumeration on tiny inputs,
@@ -39,7 +50,7 @@
 
 enum { OR_OK = 0, OR_EINVAL = -1, OR_ERANGE = -2, OR_EDUP = -3, OR_ECAP = -4,
        OR_EOVERFLOW = -5, OR_ESTATE = -6 };
-enum { ST_SUCCESS = 0, ST_FAILED = 1, ST_SKIPPED = 2, ST_PENDING = 3 };
+enum { ST_SUCCESS = 0, ST_FAILED = 1, ST_SKIPPED = 2, ST_PENDING = 3, ST_GROUP_FAILED = 4 };
 
 /* ------------------------------------------------------------------------ */
 /* F.expand: child counts -> Expansion offsets and per-child lineage keys.   */
@@ -93,12 +104,13 @@ static uint32_t fifo_pop(fifo_t *q) { return q->slot[q->head++]; }
  * B entries from the head until the queue is empty.  Batch j is written to
  * slots [j*B, j*B + size_j) of the outputs; batch_size_out (optional) gets
  * size_j.  The (parent, ordinal) tags of child c come from the same per-parent
- * enumeration as oracle_expand. */
+ * enumeration as oracle_expand.  With a barrier array, an entry whose parent
+ * is barred is suppressed before dispatch: it never enters the queue. */
 int oracle_batch(const uint32_t *queue, const uint8_t *keep, int64_t q_len,
                  const int64_t *offsets, int64_t n_parents, int32_t batch_size,
                  uint32_t *out_child, uint32_t *out_parent, uint32_t *out_ordinal,
                  int64_t out_cap, int64_t *n_out, int64_t *n_batches,
-                 int64_t *batch_size_out)
+                 int64_t *batch_size_out, const uint8_t *barrier)
 {
     if (q_len < 0 || n_parents < 0 || batch_size <= 0 || offsets == NULL ||
         (q_len > 0 && queue == NULL))
@@ -120,6 +132,8 @@ int oracle_batch(const uint32_t *queue, const uint8_t *keep, int64_t q_len,
         if (keep != NULL && keep[i] == 0)
             continue;
         if ((int64_t)queue[i] >= n) { rc = OR_ERANGE; goto done; }
+        if (barrier != NULL && barrier[par[queue[i]]])
+            continue;                         /* suppressed: never dispatched */
         fifo_push(&q, queue[i]);
     }
     if (q.tail > out_cap) { rc = OR_ECAP; goto done; }
@@ -171,14 +185,17 @@ static int key_cmp(const void *a, const void *b)
  * ordinal order.  out_data may be NULL (metadata only).  child_dst (NULL or
  * [N+1]) receives, for every child in canonical order, the output position
  * where its bytes start (its bytes, if any, end where the next child's
- * start; child_dst[N] = total). */
+ * start; child_dst[N] = total).  barrier (NULL or [P], read and updated) is
+ * the Call's group-failure barrier; n_rejected (optional) counts the reports
+ * it rejected. */
 int oracle_gather(const uint32_t *rep_parent, const uint32_t *rep_ordinal,
                   const uint8_t *rep_state, const int64_t *rep_off,
                   const uint8_t *data, int64_t n_reports,
                   const int64_t *offsets, int64_t n_parents,
                   int64_t *out_off, uint8_t *out_data, int64_t out_cap,
                   int32_t *n_success, int32_t *n_failed, int32_t *n_skipped,
-                  uint8_t *complete, uint8_t *parent_state, int64_t *child_dst)
+                  uint8_t *complete, uint8_t *parent_state, int64_t *child_dst,
+                  uint8_t *barrier, int64_t *n_rejected)
 {
     if (n_reports < 0 || n_parents < 0 || offsets == NULL || out_off == NULL)
         return OR_EINVAL;
@@ -192,7 +209,7 @@ int oracle_gather(const uint32_t *rep_parent, const uint32_t *rep_ordinal,
     for (int64_t i = 0; i < n_reports; ++i) {
         if (rep_off[i + 1] < rep_off[i])
             return OR_EINVAL;
-        if (rep_state[i] > ST_PENDING)
+        if (rep_state[i] > ST_GROUP_FAILED || (rep_state[i] == ST_GROUP_FAILED && barrier == NULL))
             return OR_ESTATE;
         if (rep_state[i] == ST_PENDING)
             continue;                         /* no report for this slot */
@@ -203,13 +220,34 @@ int oracle_gather(const uint32_t *rep_parent, const uint32_t *rep_ordinal,
             return OR_ERANGE;
         ++n_valid;
     }
-    /* 2. stable sort of the report indices by (parent, ordinal) */
-    key_t *keys = (key_t *)malloc(sizeof(key_t) * (size_t)(n_valid > 0 ? n_valid : 1));
-    if (!keys)
+    /* 1b. commit in report order: a report of a barred parent is rejected; a
+     *     group failure commits as a failed member and bars its parent */
+    uint8_t *accepted = (uint8_t *)calloc((size_t)(n_reports > 0 ? n_reports : 1), 1);
+    if (!accepted)
         return OR_EINVAL;
-    int64_t m = 0;
+    int64_t rejected = 0;
     for (int64_t i = 0; i < n_reports; ++i) {
         if (rep_state[i] == ST_PENDING)
+            continue;
+        uint32_t p = rep_parent[i];
+        if (barrier != NULL && barrier[p]) {
+            ++rejected;
+            continue;
+        }
+        accepted[i] = 1;
+        if (rep_state[i] == ST_GROUP_FAILED)
+            barrier[p] = 1;
+    }
+    if (n_rejected) *n_rejected = rejected;
+    /* 2. stable sort of the accepted report indices by (parent, ordinal) */
+    key_t *keys = (key_t *)malloc(sizeof(key_t) * (size_t)(n_valid > 0 ? n_valid : 1));
+    if (!keys) {
+        free(accepted);
+        return OR_EINVAL;
+    }
+    int64_t m = 0;
+    for (int64_t i = 0; i < n_reports; ++i) {
+        if (!accepted[i])
             continue;
         keys[m].parent = rep_parent[i];
         keys[m].ordinal = rep_ordinal[i];
@@ -220,6 +258,7 @@ int oracle_gather(const uint32_t *rep_parent, const uint32_t *rep_ordinal,
     for (int64_t j = 1; j < m; ++j) {
         if (keys[j].parent == keys[j - 1].parent && keys[j].ordinal == keys[j - 1].ordinal) {
             free(keys);
+            free(accepted);
             return OR_EDUP;                   /* conflicting second fact */
         }
     }
@@ -232,6 +271,7 @@ int oracle_gather(const uint32_t *rep_parent, const uint32_t *rep_ordinal,
     }
     if (out_data != NULL && total > out_cap) {
         free(keys);
+        free(accepted);
         return OR_ECAP;
     }
     /* 4. per parent, ascending: counts, completion, state, and the bytes of
@@ -252,7 +292,7 @@ int oracle_gather(const uint32_t *rep_parent, const uint32_t *rep_ordinal,
                         memcpy(out_data + pos, data + rep_off[i], (size_t)len);
                     pos += len;
                     ++ns;
-                } else if (rep_state[i] == ST_FAILED) {
+                } else if (rep_state[i] == ST_FAILED || rep_state[i] == ST_GROUP_FAILED) {
                     ++nf;
                 } else {
                     ++nk;
@@ -260,17 +300,20 @@ int oracle_gather(const uint32_t *rep_parent, const uint32_t *rep_ordinal,
                 ++j;
             }
         }
-        int done = ((int64_t)ns + nf + nk == k);
+        /* a barred parent's uncommitted children are suppressed: it is done */
+        int barred = barrier != NULL && barrier[p];
+        int done = barred || ((int64_t)ns + nf + nk == k);
         if (n_success) n_success[p] = ns;
         if (n_failed)  n_failed[p] = nf;
         if (n_skipped) n_skipped[p] = nk;
         if (complete)  complete[p] = (uint8_t)done;
         if (parent_state)
-            parent_state[p] = !done ? ST_PENDING : (nf > 0 ? ST_FAILED : ST_SUCCESS);
+            parent_state[p] = !done ? ST_PENDING : ((barred || nf > 0) ? ST_FAILED : ST_SUCCESS);
     }
     out_off[n_parents] = pos;
     if (child_dst) child_dst[offsets[n_parents]] = pos;
     free(keys);
+    free(accepted);
     return OR_OK;
 }
 
@@ -287,6 +330,7 @@ typedef struct {
     int64_t *len;                /* per child: SUCCESS record length, else 0 */
     int32_t *cnt[3];             /* per parent: SUCCESS / FAILED / SKIPPED */
     uint8_t *emitted;            /* per parent */
+    uint8_t *barrier;            /* per parent: group failure seen (the stream is one Call) */
 } oracle_stream;
 
 void oracle_stream_destroy(oracle_stream *s)
@@ -295,6 +339,7 @@ void oracle_stream_destroy(oracle_stream *s)
     free(s->offsets); free(s->seen); free(s->state); free((void *)s->src); free(s->len);
     for (int t = 0; t < 3; ++t) free(s->cnt[t]);
     free(s->emitted);
+    free(s->barrier);
     free(s);
 }
 
@@ -315,8 +360,9 @@ oracle_stream *oracle_stream_create(const int64_t *offsets, int64_t n_parents)
     s->len = (int64_t *)calloc(nc, sizeof(int64_t));
     for (int t = 0; t < 3; ++t) s->cnt[t] = (int32_t *)calloc(np, sizeof(int32_t));
     s->emitted = (uint8_t *)calloc(np, 1);
+    s->barrier = (uint8_t *)calloc(np, 1);
     if (!s->offsets || !s->seen || !s->state || !s->src || !s->len ||
-        !s->cnt[0] || !s->cnt[1] || !s->cnt[2] || !s->emitted) {
+        !s->cnt[0] || !s->cnt[1] || !s->cnt[2] || !s->emitted || !s->barrier) {
         oracle_stream_destroy(s);
         return NULL;
     }
@@ -324,12 +370,19 @@ oracle_stream *oracle_stream_create(const int64_t *offsets, int64_t n_parents)
     return s;
 }
 
-/* Record one wave of reports.  A child reported in an earlier wave, or twice
- * in this one, is a conflicting publication.  The bytes stay in the caller's
- * buffer until the parent is emitted. */
+/* The stream's group-failure barrier (read it to drop the suppressed
+ * siblings of the next wave's queue). */
+const uint8_t *oracle_stream_barrier(const oracle_stream *s) { return s ? s->barrier : NULL; }
+
+/* Record one wave of reports, committed in the order given.  A child
+ * reported in an earlier wave, or twice in this one, is a conflicting
+ * publication.  A report of a barred parent is rejected; a GROUP_FAILED
+ * report commits as a failed member and bars its parent.  The bytes stay in
+ * the caller's buffer until the parent is emitted. */
 int oracle_stream_report(oracle_stream *s, const uint32_t *rep_parent,
                          const uint32_t *rep_ordinal, const uint8_t *rep_state,
-                         const int64_t *rep_off, const uint8_t *data, int64_t n_reports)
+                         const int64_t *rep_off, const uint8_t *data, int64_t n_reports,
+                         int64_t *n_rejected)
 {
     if (!s || n_reports < 0)
         return OR_EINVAL;
@@ -339,30 +392,40 @@ int oracle_stream_report(oracle_stream *s, const uint32_t *rep_parent,
         return OR_EINVAL;
     for (int64_t i = 0; i < n_reports; ++i) {      /* validate first */
         if (rep_off[i + 1] < rep_off[i]) return OR_EINVAL;
-        if (rep_state[i] > ST_PENDING) return OR_ESTATE;
+        if (rep_state[i] > ST_GROUP_FAILED) return OR_ESTATE;
         if (rep_state[i] == ST_PENDING) continue;
         uint32_t p = rep_parent[i];
         if ((int64_t)p >= s->n_parents) return OR_ERANGE;
         if ((int64_t)rep_ordinal[i] >= s->offsets[p + 1] - s->offsets[p]) return OR_ERANGE;
     }
+    int64_t rejected = 0;
     for (int64_t i = 0; i < n_reports; ++i) {
         if (rep_state[i] == ST_PENDING) continue;
         uint32_t p = rep_parent[i];
+        if (s->barrier[p]) {                           /* cannot commit */
+            ++rejected;
+            continue;
+        }
         int64_t c = s->offsets[p] + rep_ordinal[i];
         if (s->seen[c])
             return OR_EDUP;
+        int st = rep_state[i] == ST_GROUP_FAILED ? ST_FAILED : rep_state[i];
         s->seen[c] = 1;
-        s->state[c] = rep_state[i];
+        s->state[c] = (uint8_t)st;
         s->src[c] = data != NULL ? data + rep_off[i] : NULL;   /* NULL: metadata only */
-        s->len[c] = rep_state[i] == ST_SUCCESS ? rep_off[i + 1] - rep_off[i] : 0;
-        s->cnt[rep_state[i]][p] += 1;
+        s->len[c] = st == ST_SUCCESS ? rep_off[i + 1] - rep_off[i] : 0;
+        s->cnt[st][p] += 1;
+        if (rep_state[i] == ST_GROUP_FAILED)
+            s->barrier[p] = 1;
     }
+    if (n_rejected) *n_rejected = rejected;
     return OR_OK;
 }
 
-/* Emit every parent that is complete now and was not emitted before, in
- * ascending parent order: its id, its slot offset inside emit_data, its
- * counts, its derived state and its SUCCESS bytes in ordinal order. */
+/* Emit every parent that is complete now (or barred) and was not emitted
+ * before, in ascending parent order: its id, its slot offset inside
+ * emit_data, its counts, its derived state and its SUCCESS bytes in ordinal
+ * order. */
 int oracle_stream_emit(oracle_stream *s, uint32_t *emit_parent, int64_t *emit_off,
                        uint8_t *emit_data, int64_t cap_parents, int64_t cap_bytes,
                        int32_t *n_success, int32_t *n_failed, int32_t *n_skipped,
@@ -374,7 +437,7 @@ int oracle_stream_emit(oracle_stream *s, uint32_t *emit_parent, int64_t *emit_of
     /* first pass: sizes, checked against the capacities */
     for (int64_t p = 0; p < s->n_parents; ++p) {
         int64_t k = s->offsets[p + 1] - s->offsets[p];
-        if (s->emitted[p] || (int64_t)s->cnt[0][p] + s->cnt[1][p] + s->cnt[2][p] != k)
+        if (s->emitted[p] || (!s->barrier[p] && (int64_t)s->cnt[0][p] + s->cnt[1][p] + s->cnt[2][p] != k))
             continue;
         ++e;
         for (int64_t c = s->offsets[p]; c < s->offsets[p + 1]; ++c)
@@ -386,7 +449,7 @@ int oracle_stream_emit(oracle_stream *s, uint32_t *emit_parent, int64_t *emit_of
     pos = 0;
     for (int64_t p = 0; p < s->n_parents; ++p) {
         int64_t k = s->offsets[p + 1] - s->offsets[p];
-        if (s->emitted[p] || (int64_t)s->cnt[0][p] + s->cnt[1][p] + s->cnt[2][p] != k)
+        if (s->emitted[p] || (!s->barrier[p] && (int64_t)s->cnt[0][p] + s->cnt[1][p] + s->cnt[2][p] != k))
             continue;
         if (emit_parent) emit_parent[e] = (uint32_t)p;
         emit_off[e] = pos;
@@ -398,7 +461,7 @@ int oracle_stream_emit(oracle_stream *s, uint32_t *emit_parent, int64_t *emit_of
         if (n_success) n_success[e] = s->cnt[0][p];
         if (n_failed)  n_failed[e] = s->cnt[1][p];
         if (n_skipped) n_skipped[e] = s->cnt[2][p];
-        if (parent_state) parent_state[e] = s->cnt[1][p] > 0 ? ST_FAILED : ST_SUCCESS;
+        if (parent_state) parent_state[e] = (s->barrier[p] || s->cnt[1][p] > 0) ? ST_FAILED : ST_SUCCESS;
         s->emitted[p] = 1;
         ++e;
     }

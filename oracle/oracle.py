@@ -17,10 +17,10 @@ import numpy as np
 
 __all__ = ["build", "lib", "OracleError", "expand", "batch", "gather", "nested", "Stream",
            "OK", "EINVAL", "ERANGE", "EDUP", "ECAP", "EOVERFLOW", "ESTATE",
-           "SUCCESS", "FAILED", "SKIPPED", "PENDING"]
+           "SUCCESS", "FAILED", "SKIPPED", "PENDING", "GROUP_FAILED"]
 
 OK, EINVAL, ERANGE, EDUP, ECAP, EOVERFLOW, ESTATE = 0, -1, -2, -3, -4, -5, -6
-SUCCESS, FAILED, SKIPPED, PENDING = 0, 1, 2, 3
+SUCCESS, FAILED, SKIPPED, PENDING, GROUP_FAILED = 0, 1, 2, 3, 4
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
@@ -49,12 +49,14 @@ def _load(path):
     P = C.c_void_p
     i64 = C.c_int64
     L.oracle_expand.argtypes = [P, i64, P, P, P, i64]
-    L.oracle_batch.argtypes = [P, P, i64, P, i64, C.c_int32, P, P, P, i64, P, P, P]
-    L.oracle_gather.argtypes = [P, P, P, P, P, i64, P, i64, P, P, i64, P, P, P, P, P, P]
+    L.oracle_batch.argtypes = [P, P, i64, P, i64, C.c_int32, P, P, P, i64, P, P, P, P]
+    L.oracle_gather.argtypes = [P, P, P, P, P, i64, P, i64, P, P, i64, P, P, P, P, P, P, P, P]
     L.oracle_stream_create.argtypes = [P, i64]
     L.oracle_stream_create.restype = P
     L.oracle_stream_destroy.argtypes = [P]
-    L.oracle_stream_report.argtypes = [P, P, P, P, P, P, i64]
+    L.oracle_stream_report.argtypes = [P, P, P, P, P, P, i64, P]
+    L.oracle_stream_barrier.argtypes = [P]
+    L.oracle_stream_barrier.restype = C.POINTER(C.c_uint8)
     L.oracle_stream_emit.argtypes = [P, P, P, P, i64, i64, P, P, P, P, P, P]
     for f in ("oracle_expand", "oracle_batch", "oracle_gather", "oracle_stream_report",
               "oracle_stream_emit"):
@@ -100,8 +102,9 @@ def expand(counts, tags=True, L=None):
     return offsets, parent[:n], ordinal[:n]
 
 
-def batch(queue, keep, offsets, batch_size, L=None):
-    """FIFO batches: returns (child, parent, ordinal, batch_sizes)."""
+def batch(queue, keep, offsets, batch_size, barrier=None, L=None):
+    """FIFO batches: returns (child, parent, ordinal, batch_sizes).  With a
+    barrier (uint8 per parent), children of barred parents are dropped."""
     L = L or lib()
     queue = np.ascontiguousarray(queue, dtype=np.uint32)
     keep = None if keep is None else np.ascontiguousarray(keep, dtype=np.uint8)
@@ -114,16 +117,22 @@ def batch(queue, keep, offsets, batch_size, L=None):
     sizes = np.zeros(cap, np.int64)
     n_out = np.zeros(1, np.int64)
     n_b = np.zeros(1, np.int64)
+    barrier = None if barrier is None else np.ascontiguousarray(barrier, dtype=np.uint8)
     _check(L.oracle_batch(_p(queue), _p(keep), Q, _p(offsets), len(offsets) - 1, int(batch_size),
-                          _p(child), _p(parent), _p(ordinal), Q, _p(n_out), _p(n_b), _p(sizes)),
+                          _p(child), _p(parent), _p(ordinal), Q, _p(n_out), _p(n_b), _p(sizes),
+                          _p(barrier)),
            "batch")
     m, nb = int(n_out[0]), int(n_b[0])
     return child[:m], parent[:m], ordinal[:m], sizes[:nb]
 
 
-def gather(parent, ordinal, state, off, data, offsets, with_data=True, child_dst=False, L=None):
+def gather(parent, ordinal, state, off, data, offsets, with_data=True, child_dst=False, barrier=None,
+           L=None):
     """Ordered gather; returns a dict of per-parent outputs (and, with
-    child_dst, every child's output start position, N+1 entries)."""
+    child_dst, every child's output start position, N+1 entries).  With a
+    barrier (uint8 per parent, the Call's group-failure state before this
+    call) the result also holds the updated barrier and the number of
+    rejected reports."""
     L = L or lib()
     parent = np.ascontiguousarray(parent, dtype=np.uint32)
     ordinal = np.ascontiguousarray(ordinal, dtype=np.uint32)
@@ -142,14 +151,20 @@ def gather(parent, ordinal, state, off, data, offsets, with_data=True, child_dst
     comp = np.zeros(max(P, 1), np.uint8)
     pst = np.zeros(max(P, 1), np.uint8)
     cdst = np.zeros(int(offsets[-1]) + 1, np.int64) if child_dst else None
+    bar = None if barrier is None else np.array(barrier, dtype=np.uint8, copy=True)
+    nrej = np.zeros(1, np.int64)
     _check(L.oracle_gather(_p(parent), _p(ordinal), _p(state), _p(off),
                            _p(data) if with_data else None, n, _p(offsets), P,
                            _p(out_off), _p(out_data), cap, _p(ns), _p(nf), _p(nk),
-                           _p(comp), _p(pst), _p(cdst) if child_dst else None), "gather")
+                           _p(comp), _p(pst), _p(cdst) if child_dst else None, _p(bar), _p(nrej)),
+           "gather")
     res = dict(out_off=out_off, n_success=ns[:P], n_failed=nf[:P], n_skipped=nk[:P],
                complete=comp[:P], parent_state=pst[:P])
     if child_dst:
         res["child_dst_off"] = cdst
+    if barrier is not None:
+        res["barrier"] = bar
+        res["n_rejected"] = int(nrej[0])
     if with_data:
         res["out_data"] = out_data[:int(out_off[-1])]
     return res
@@ -197,8 +212,16 @@ class Stream:
         off = np.ascontiguousarray(off, dtype=np.int64)
         data = None if data is None else np.ascontiguousarray(data, dtype=np.uint8)
         self._keep.append((parent, ordinal, state, off, data))
+        nrej = np.zeros(1, np.int64)
         _check(self.L.oracle_stream_report(self.h, _p(parent), _p(ordinal), _p(state), _p(off),
-                                           _p(data), len(parent)), "stream_report")
+                                           _p(data), len(parent), _p(nrej)), "stream_report")
+        return int(nrej[0])
+
+    def barrier(self):
+        """Copy of the stream's group-failure barrier (uint8 per parent)."""
+        P = len(self.offsets) - 1
+        ptr = self.L.oracle_stream_barrier(self.h)
+        return np.ctypeslib.as_array(ptr, shape=(max(P, 1),))[:P].copy()
 
     def emit(self, cap_parents=None, cap_bytes=None, with_data=True):
         P = len(self.offsets) - 1

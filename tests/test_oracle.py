@@ -472,3 +472,164 @@ def test_stream_duplicate_across_waves():
                   np.zeros(1, np.uint8))
     assert e.value.code == O.EDUP
     st.close()
+
+
+# ---------------------------------------------------------------- group failure
+def test_group_failure_figure():
+    """Fig. recovery-protocol: B1's group failure rejects the in-flight B2,
+    suppresses the queued B3, keeps B0 committed earlier, and leaves A and C
+    to pass on their own."""
+    fx = json.load(open(os.path.join(GOLDEN, "failure_group.json")))
+    names = {n: i for i, n in enumerate("ABC")}
+    codes = {"SUCCESS": O.SUCCESS, "GROUP_FAILED": O.GROUP_FAILED}
+    counts = np.array(fx["counts"], np.int32)
+    offs = O.expand(counts, tags=False)
+    st = O.Stream(offs)
+
+    def wave(reports):
+        par = np.array([names[r[0]] for r in reports], np.uint32)
+        ordi = np.array([r[1] for r in reports], np.uint32)
+        state = np.array([codes[r[2]] for r in reports], np.uint8)
+        data = np.array([16 * names[r[0]] + r[1] for r in reports], np.uint8)
+        off = np.arange(len(reports) + 1, dtype=np.int64)
+        return st.report(par, ordi, state, off, data)
+
+    ex = fx["expect"]
+    assert wave(fx["wave1"]["reports"]) == 0
+    assert len(st.emit()["parent"]) == len(ex["wave1_emitted"]) == 0
+    queue = np.array([offs[names[p]] + o for p, o in fx["queue"]], np.uint32)
+    child, par, ordi, sizes = O.batch(queue, None, offs, fx["reserve"], barrier=st.barrier())
+    assert [(int(p), int(o)) for p, o in zip(par[:sizes[0]], ordi[:sizes[0]])] == \
+        [(names[p], o) for p, o, _ in fx["wave2"]["reports"]]
+    assert wave(fx["wave2"]["reports"]) == ex["wave2_rejected"]
+    e = st.emit()
+    assert [("ABC"[p]) for p in e["parent"]] == ex["wave2_emitted"]
+    for j, p in enumerate(e["parent"]):
+        n = "ABC"[p]
+        assert e["parent_state"][j] == codes.get(ex["states"][n], O.FAILED)
+        assert e["n_success"][j] == ex["n_success"][n] and e["n_failed"][j] == ex["n_failed"][n]
+        assert list(e["data"][e["off"][j]:e["off"][j + 1]]) == ex["bytes"][n]
+    # the next reservation over what is left (B3) suppresses it
+    left = queue[sizes[0]:]
+    assert len(O.batch(left, None, offs, fx["reserve"], barrier=st.barrier())[0]) == len(ex["next_reservation"])
+    st.close()
+
+
+def _gf_expected(reports, counts, barrier_in):
+    """Group failure from its first-failure form: a report of parent p is
+    accepted iff p was not barred before the call and no group failure of p
+    comes earlier in report order."""
+    P = len(counts)
+    first = {}
+    for i, (p, o, s, b) in enumerate(reports):
+        if s == O.GROUP_FAILED and p not in first and not barrier_in[p]:
+            first[p] = i
+    acc = [s != O.PENDING and not barrier_in[p] and (p not in first or i <= first[p])
+           for i, (p, o, s, b) in enumerate(reports)]
+    bar = np.array([1 if barrier_in[p] or p in first else 0 for p in range(P)], np.uint8)
+    out = []
+    for p in range(P):
+        mine = sorted((o, s, b) for (pp, o, s, b), a in zip(reports, acc) if a and pp == p)
+        ns = sum(1 for _, s, _ in mine if s == O.SUCCESS)
+        nf = sum(1 for _, s, _ in mine if s in (O.FAILED, O.GROUP_FAILED))
+        nk = sum(1 for _, s, _ in mine if s == O.SKIPPED)
+        done = bool(bar[p]) or ns + nf + nk == counts[p]
+        state = O.PENDING if not done else (O.FAILED if bar[p] or nf else O.SUCCESS)
+        slot = b"".join(b for _, s, b in mine if s == O.SUCCESS)
+        out.append((ns, nf, nk, int(done), state, slot))
+    n_rej = sum(1 for (p, o, s, b), a in zip(reports, acc) if s != O.PENDING and not a)
+    return out, bar, n_rej
+
+
+def test_group_failure_vs_first_failure_form():
+    rng = np.random.default_rng(31)
+    for trial in range(400):
+        P = int(rng.integers(1, 6))
+        counts = [int(x) for x in rng.integers(0, 5, P)]
+        reports = _random_reports(rng, counts, p_report=float(rng.choice([1.0, 0.7])),
+                                  states=(0, 0, 1, 2, 3, 4, 4), max_len=4)
+        barrier_in = (rng.random(P) < 0.2).astype(np.uint8)
+        offsets = O.expand(np.array(counts, np.int32), tags=False)
+        par = np.array([r[0] for r in reports], np.uint32)
+        ordi = np.array([r[1] for r in reports], np.uint32)
+        st = np.array([r[2] for r in reports], np.uint8)
+        lens = np.array([len(r[3]) for r in reports], np.int64)
+        off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+        data = np.frombuffer(b"".join(r[3] for r in reports) or b"\0", np.uint8)
+        g = O.gather(par, ordi, st, off, data, offsets, barrier=barrier_in)
+        want, bar, n_rej = _gf_expected([tuple(r) for r in reports], counts, barrier_in)
+        _compare_brute(g, want)
+        assert np.array_equal(g["barrier"], bar) and g["n_rejected"] == n_rej, trial
+
+
+def test_group_failure_rejected_repeat_is_not_a_duplicate():
+    """A repeat of a committed child that arrives after its parent's group
+    failure is rejected before any duplicate check."""
+    offs = O.expand(np.array([3], np.int32), tags=False)
+    par = np.zeros(3, np.uint32)
+    ordi = np.array([0, 1, 0], np.uint32)
+    st = np.array([O.SUCCESS, O.GROUP_FAILED, O.SUCCESS], np.uint8)
+    off = np.array([0, 1, 1, 2], np.int64)
+    g = O.gather(par, ordi, st, off, np.array([7, 9], np.uint8), offs, barrier=np.zeros(1, np.uint8))
+    assert g["n_rejected"] == 1 and g["complete"][0] == 1 and g["parent_state"][0] == O.FAILED
+    assert list(g["out_data"]) == [7]
+    with pytest.raises(O.OracleError) as e:           # without a barrier array the state is bad
+        O.gather(par, ordi, st, off, np.array([7, 9], np.uint8), offs)
+    assert e.value.code == O.ESTATE
+
+
+def test_batch_barrier_is_a_filter():
+    """Dropping barred parents' children is the same as filtering the queue
+    first (suppressed before dispatch), order kept."""
+    rng = np.random.default_rng(37)
+    for trial in range(200):
+        counts = rng.integers(0, 6, int(rng.integers(1, 9))).astype(np.int32)
+        offs, cpar, _ = O.expand(counts)
+        N = int(offs[-1])
+        q = rng.permutation(N).astype(np.uint32)
+        keep = (rng.random(N) < 0.8).astype(np.uint8)
+        bar = (rng.random(len(counts)) < 0.3).astype(np.uint8)
+        B = int(rng.integers(1, 6))
+        got = O.batch(q, keep, offs, B, barrier=bar)
+        k2 = keep & (1 - bar[cpar[q]]) if N else keep
+        want = O.batch(q, k2, offs, B)
+        for a, b in zip(got, want):
+            assert np.array_equal(a, b), trial
+
+
+def test_stream_group_failure_emits_at_barrier():
+    """Waves committed in order equal one gather over all reports with the
+    barrier carried along; each parent is emitted once, in the wave where it
+    completes or is barred."""
+    rng = np.random.default_rng(41)
+    for trial in range(60):
+        counts = rng.integers(0, 6, int(rng.integers(1, 12))).astype(np.int32)
+        offs = O.expand(counts, tags=False)
+        N = int(offs[-1])
+        reports = _random_reports(rng, list(counts), states=(0, 0, 1, 2, 4), max_len=3)
+        cuts = np.sort(rng.integers(0, len(reports) + 1, 3))
+        waves = np.split(np.arange(len(reports)), cuts)
+        st = O.Stream(offs)
+        emitted_in = {}
+        got_bytes = {}
+        for w, idx in enumerate(waves):
+            rs = [reports[i] for i in idx]
+            par = np.array([r[0] for r in rs], np.uint32)
+            ordi = np.array([r[1] for r in rs], np.uint32)
+            stt = np.array([r[2] for r in rs], np.uint8)
+            off = np.concatenate([[0], np.cumsum([len(r[3]) for r in rs])]).astype(np.int64)
+            data = np.frombuffer(b"".join(r[3] for r in rs) or b"\0", np.uint8)
+            st.report(par, ordi, stt, off, data)
+            e = st.emit()
+            for j, p in enumerate(e["parent"]):
+                assert p not in emitted_in
+                emitted_in[int(p)] = w
+                got_bytes[int(p)] = bytes(e["data"][e["off"][j]:e["off"][j + 1]])
+        want, bar, _ = _gf_expected([tuple(r) for r in reports], list(counts),
+                                    np.zeros(len(counts), np.uint8))
+        for p in range(len(counts)):
+            if want[p][3]:
+                assert p in emitted_in and got_bytes[p] == want[p][5], (trial, p)
+            else:
+                assert p not in emitted_in
+        st.close()

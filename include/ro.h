@@ -39,7 +39,16 @@
  *     2^32 - 1 children (RO_EOVERFLOW otherwise).  Byte offsets are int64.
  *   * Terminal states are uint8: RO_SUCCESS (Present), RO_FAILED (Failed, or
  *     Suppressed handed up from a lower level), RO_SKIPPED (Dropped) and
- *     RO_PENDING (no report yet).
+ *     RO_PENDING (no report yet).  A report may also carry RO_GROUP_FAILED,
+ *     a typed group failure (Sec. 4 "Commit, Failure, and Recovery"): it
+ *     commits as a failed member and bars its parent for the rest of the
+ *     Call.  Barriers live in a caller-owned uint8 array per Call, one byte
+ *     per parent; reports commit in the order given, call after call, so a
+ *     later report of a barred parent is rejected (not committed, not
+ *     counted, its bytes never copied), reports committed earlier stay, and
+ *     ro_batch drops the barred parent's queued children before dispatch.
+ *     A barred parent is complete and RO_FAILED.  RO_GROUP_FAILED without a
+ *     barrier array is RO_ESTATE.
  *
  * A context is bound to one stream and is not thread safe.
  */
@@ -63,7 +72,7 @@ enum {
     RO_EHIP = -7        /* a HIP runtime call failed                                   */
 };
 
-enum { RO_SUCCESS = 0, RO_FAILED = 1, RO_SKIPPED = 2, RO_PENDING = 3 };
+enum { RO_SUCCESS = 0, RO_FAILED = 1, RO_SKIPPED = 2, RO_PENDING = 3, RO_GROUP_FAILED = 4 };
 
 typedef struct ro_ctx ro_ctx;
 
@@ -120,11 +129,13 @@ int ro_expand(ro_ctx *ctx, const int32_t *counts, int64_t n_parents, int64_t *of
  * (out_ordinal); any of the three may be NULL.  M must be <= out_cap
  * (RO_ECAP).  A ready id >= N (N = offsets[n_parents]) is RO_ERANGE.  M and
  * ceil(M/B) are written to the device scalars *n_out_dev and *n_batches_dev
- * (either may be NULL). */
+ * (either may be NULL).  With a group-failure barrier ([n_parents], may be
+ * NULL), an entry whose parent is barred is not ready: it is suppressed
+ * before dispatch and takes no slot. */
 int ro_batch(ro_ctx *ctx, const uint32_t *queue, const uint8_t *keep, int64_t q_len,
              const int64_t *offsets, int64_t n_parents, int32_t batch_size,
              uint32_t *out_child, uint32_t *out_parent, uint32_t *out_ordinal, int64_t out_cap,
-             int64_t *n_out_dev, int64_t *n_batches_dev);
+             int64_t *n_out_dev, int64_t *n_batches_dev, const uint8_t *barrier);
 
 /* One terminal report per child, in any order.  Report i is the child
  * (parent[i], ordinal[i]) with state[i]; its value is the byte range
@@ -155,6 +166,9 @@ typedef struct ro_gather_out {
                                  canonical order; child c's bytes (none unless it has a
                                  SUCCESS report) are [child_dst_off[c],
                                  child_dst_off[c+1]), child_dst_off[N] = out_off[P]     */
+    uint8_t *barrier;         /* [P] or NULL: the Call's group-failure barrier, read and
+                                 updated (a parent barred by this call's reports is set) */
+    int64_t *n_rejected;      /* device scalar or NULL: reports rejected by a barrier    */
 } ro_gather_out;
 
 /* F.reduce: ordered gather of reports into parent slots.  Slot p holds the
@@ -175,18 +189,25 @@ int ro_gather(ro_ctx *ctx, const ro_reports *reports, const int64_t *offsets, in
 
 /* Streaming gather over one expansion (offsets[P+1] on the device, kept by
  * reference until ro_stream_destroy).  The stream's own state lives in
- * device memory allocated here (about 32 bytes per child and 34 per parent). */
+ * device memory allocated here (about 32 bytes per child and 42 per parent).
+ * A stream is one Call: `barrier` ([P], zeroed by the caller, may be NULL)
+ * is its group-failure barrier, kept by reference; pass the same array to
+ * ro_batch for each wave so that barred parents' queued children are
+ * dropped. */
 typedef struct ro_stream ro_stream;
 int ro_stream_create(ro_ctx *ctx, const int64_t *offsets, int64_t n_parents, int64_t n_children,
-                     ro_stream **out);
+                     uint8_t *barrier, ro_stream **out);
 
 /* Record one wave of reports (same validation as ro_gather; a child already
- * reported in an earlier wave is RO_EDUP).  The report bytes are read when
- * their parent is emitted, so `data` must stay valid until then. */
-int ro_stream_report(ro_ctx *ctx, ro_stream *s, const ro_reports *wave);
+ * reported in an earlier wave is RO_EDUP).  Reports commit in the order
+ * given, after every earlier wave: one of a barred parent is rejected and
+ * added to *n_rejected_dev (device scalar, may be NULL).  The report bytes
+ * are read when their parent is emitted, so `data` must stay valid until
+ * then. */
+int ro_stream_report(ro_ctx *ctx, ro_stream *s, const ro_reports *wave, int64_t *n_rejected_dev);
 
-/* Emit every parent that is complete now and was not emitted before, in
- * ascending parent order: emit_parent[e], its slot
+/* Emit every parent that is complete now (a barred parent is complete) and
+ * was not emitted before, in ascending parent order: emit_parent[e], its slot
  * emit_data[emit_off[e], emit_off[e+1]), its counts and its state.  Needs
  * room for cap_parents parents (emit_off: cap_parents + 1) and cap_bytes
  * bytes (RO_ECAP).  The number of parents and bytes go to the device
@@ -199,7 +220,7 @@ int ro_stream_emit(ro_ctx *ctx, ro_stream *s, uint32_t *emit_parent, int64_t *em
 
 /* Start the stream over for a new run on the same expansion (same offsets
  * buffer, same P and N; the offsets may be rewritten in between): every
- * report, count and emission is forgotten, the allocation is kept.
+ * report, count, emission and barrier is forgotten, the allocation is kept.
  * Stream-ordered like the other calls, allocates nothing and enqueues no
  * memset node.  A new Call over a parent batch of the same shape (Sec. 4,
  * per-Call queue) then reuses the state instead of creating it again.

@@ -6,7 +6,9 @@
 // one after another until the queue is empty is a stable compaction of the
 // ready entries cut into consecutive chunks of B, which is what this kernel
 // computes in one pass: a workgroup scan of the ready flags and a decoupled
-// look-back across tiles give every ready entry its FIFO slot.
+// look-back across tiles give every ready entry its FIFO slot.  A barred
+// parent's entries (Sec. 4 "Commit, Failure, and Recovery": queued siblings
+// of a group failure are suppressed before dispatch) are simply not ready.
 #include "ro_device.h"
 
 namespace ro {
@@ -43,7 +45,8 @@ __global__ __launch_bounds__(kBlock) void k_batch(
     const int64_t *__restrict__ offsets, int64_t P, const uint32_t *__restrict__ cmap, int64_t cmap_cap,
     int32_t B, uint32_t *__restrict__ out_child, uint32_t *__restrict__ out_parent,
     uint32_t *__restrict__ out_ordinal, int64_t out_cap, int64_t *n_out, int64_t *n_batches,
-    Ctl *ctl, uint64_t *desc, int64_t desc_cap, int64_t ntiles, int vec_ok)
+    const uint8_t *__restrict__ barrier, Ctl *ctl, uint64_t *desc, int64_t desc_cap, int64_t ntiles,
+    int vec_ok)
 {
     const uint32_t epoch = scan_epoch(ctl);
     __shared__ uint32_t s_out[kTile];          // one output array of a tile, in slot order
@@ -88,7 +91,8 @@ __global__ __launch_bounds__(kBlock) void k_batch(
                 }
             }
         }
-        // lineage tags of the ready entries (independent lookups, all in flight)
+        // lineage tags of the ready entries (independent lookups, all in
+        // flight); an entry of a barred parent is not ready
         uint32_t par[kItems], ord[kItems];
         bool bad_range = false;
 #pragma unroll
@@ -99,10 +103,14 @@ __global__ __launch_bounds__(kBlock) void k_batch(
                 const int64_t c = q[k];
                 if (c >= N) {
                     bad_range = true;
-                } else if (want_tags) {
+                } else if (want_tags || barrier) {
                     const int64_t p = parent_of(cmap, nmap, offsets, P, c);
-                    par[k] = (uint32_t)p;
-                    ord[k] = (uint32_t)(c - offsets[p]);
+                    if (barrier && barrier[p]) {
+                        kmask &= ~(1u << k);
+                    } else {
+                        par[k] = (uint32_t)p;
+                        ord[k] = (uint32_t)(c - offsets[p]);
+                    }
                 }
             }
         }
@@ -197,13 +205,13 @@ hipError_t launch_batch(const Launch &L, const uint32_t *queue, const uint8_t *k
                         int64_t Q, const int64_t *offsets, int64_t P, int32_t B,
                         uint32_t *out_child, uint32_t *out_parent, uint32_t *out_ordinal,
                         int64_t out_cap, int64_t *n_out, int64_t *n_batches, uint32_t *cmap,
-                        int64_t cmap_cap)
+                        int64_t cmap_cap, const uint8_t *barrier)
 {
     // The coarse map costs a search per 64 children; a short unmasked queue
     // (fewer entries than parents, such as one wave of a stream) searches
     // the offsets directly instead and skips the extra launch.
     const bool tags = out_parent != nullptr || out_ordinal != nullptr;
-    const bool use_map = tags && !(keep == nullptr && Q < P);
+    const bool use_map = (tags || barrier != nullptr) && !(keep == nullptr && barrier == nullptr && Q < P);
     if (use_map) {
         const int64_t grid_m = (int64_t)L.num_cus * 4;
         RO_LAUNCH(L, RO_K_BATCH_SAMPLES, k_batch_cmap, dim3((unsigned)grid_m), dim3(256), 0, L.stream,
@@ -211,7 +219,7 @@ hipError_t launch_batch(const Launch &L, const uint32_t *queue, const uint8_t *k
     } else {
         cmap_cap = 0;
     }
-    if (keep == nullptr) {
+    if (keep == nullptr && barrier == nullptr) {
         int64_t grid_a = (Q + kBlock * kAllPer - 1) / (kBlock * kAllPer);
         grid_a = grid_a < 1 ? 1 : (grid_a > (int64_t)L.num_cus * 8 ? (int64_t)L.num_cus * 8 : grid_a);
         RO_LAUNCH(L, RO_K_BATCH, k_batch_all, dim3((unsigned)grid_a), dim3(kBlock), 0, L.stream, queue, Q,
@@ -225,7 +233,7 @@ hipError_t launch_batch(const Launch &L, const uint32_t *queue, const uint8_t *k
     const bool aligned = ((reinterpret_cast<uintptr_t>(queue) | reinterpret_cast<uintptr_t>(keep)) & 15u) == 0;
     RO_LAUNCH(L, RO_K_BATCH, k_batch, dim3((unsigned)grid), dim3(kBlock), 0, L.stream, queue, keep, Q,
               offsets, P, cmap, cmap_cap, B, out_child, out_parent, out_ordinal, out_cap, n_out, n_batches,
-              L.ctl, L.desc, L.desc_cap, ntiles, aligned ? 1 : 0);
+              barrier, L.ctl, L.desc, L.desc_cap, ntiles, aligned ? 1 : 0);
     return hipGetLastError();
 }
 

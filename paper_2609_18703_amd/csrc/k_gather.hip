@@ -24,12 +24,59 @@
 
 namespace ro {
 
+// ---------------------------------------------------------------- group failure
+__global__ void k_first_gf(const uint8_t *__restrict__ rs, const uint32_t *__restrict__ rp, int64_t n,
+                           int64_t P, const uint8_t *__restrict__ barrier, uint64_t *__restrict__ gkey,
+                           uint32_t epoch)
+{
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        if (rs[i] != RO_GROUP_FAILED) continue;
+        const uint32_t p = rp[i];
+        if ((int64_t)p >= P || barrier[p]) continue;
+        __hip_atomic_fetch_max(&gkey[p], gf_key(epoch, i), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+__global__ void k_gf_fold(const uint8_t *__restrict__ rs, const uint32_t *__restrict__ rp, int64_t n, int64_t P,
+                          uint8_t *__restrict__ barrier, const uint64_t *__restrict__ gkey, uint32_t epoch)
+{
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        if (rs[i] != RO_GROUP_FAILED) continue;
+        const uint32_t p = rp[i];
+        if ((int64_t)p < P && gkey[p] == gf_key(epoch, i)) barrier[p] = 1;
+    }
+}
+
+hipError_t launch_first_gf(const Launch &L, const uint8_t *rs, const uint32_t *rp, int64_t n, int64_t P,
+                           const uint8_t *barrier, uint64_t *gkey, uint32_t epoch)
+{
+    int64_t grid = (n + kBlock - 1) / kBlock;
+    grid = grid < 1 ? 1 : (grid > (int64_t)L.num_cus * 8 ? (int64_t)L.num_cus * 8 : grid);
+    RO_LAUNCH(L, RO_K_GATHER_SCATTER, k_first_gf, dim3((unsigned)grid), dim3(kBlock), 0, L.stream, rs, rp, n, P,
+              barrier, gkey, epoch);
+    return hipGetLastError();
+}
+
+hipError_t launch_gf_fold(const Launch &L, const uint8_t *rs, const uint32_t *rp, int64_t n, int64_t P,
+                          uint8_t *barrier, const uint64_t *gkey, uint32_t epoch)
+{
+    int64_t grid = (n + kBlock - 1) / kBlock;
+    grid = grid < 1 ? 1 : (grid > (int64_t)L.num_cus * 8 ? (int64_t)L.num_cus * 8 : grid);
+    RO_LAUNCH(L, RO_K_STREAM_REPORT, k_gf_fold, dim3((unsigned)grid), dim3(kBlock), 0, L.stream, rs, rp, n, P,
+              barrier, gkey, epoch);
+    return hipGetLastError();
+}
+
 // ---------------------------------------------------------------- scatter
+// With a group-failure barrier, reports commit in report order: one of a
+// barred parent, or one after its parent's first group failure in this
+// call, is rejected; an accepted group failure is a failed member.
 __global__ __launch_bounds__(kBlock) void k_gather_scatter(
     const uint32_t *__restrict__ rp, const uint32_t *__restrict__ ro_, const uint8_t *__restrict__ rs,
     const int64_t *__restrict__ roff, const uint8_t *data, int64_t n,
     const int64_t *__restrict__ offsets, int64_t P, Canon *__restrict__ canon, int64_t canon_cap,
-    int32_t *__restrict__ ns, int32_t *__restrict__ nf, int32_t *__restrict__ nk, Ctl *ctl)
+    int32_t *__restrict__ ns, int32_t *__restrict__ nf, int32_t *__restrict__ nk,
+    const uint8_t *__restrict__ barrier, const uint64_t *__restrict__ gkey, Ctl *ctl)
 {
     __shared__ int64_t s_wave[kBlock / 64];
     const uint32_t epoch = ctl->canon_epoch;
@@ -50,12 +97,12 @@ __global__ __launch_bounds__(kBlock) void k_gather_scatter(
         if (nk) nk[p] = 0;
         if (offsets[p + 1] < offsets[p]) err = RO_EINVAL;
     }
-    int64_t cnt = 0;
+    int64_t cnt = 0, rej = 0;
     for (int64_t i = gtid; i < n; i += gstride) {
-        const uint32_t s = rs[i];
+        uint32_t s = rs[i];
         const int64_t o0 = roff[i], o1 = roff[i + 1];
         if (o1 < o0) { err = RO_EINVAL; continue; }
-        if (s > RO_PENDING) { err = RO_ESTATE; continue; }
+        if (s > RO_PENDING && !(s == RO_GROUP_FAILED && barrier)) { err = RO_ESTATE; continue; }
         if (s == RO_PENDING) continue;
         const uint32_t p = rp[i];
         if ((int64_t)p >= P) { err = RO_ERANGE; continue; }
@@ -66,6 +113,8 @@ __global__ __launch_bounds__(kBlock) void k_gather_scatter(
         if (st < 0 || c >= N) { err = RO_EINVAL; continue; }     // offsets not an Expansion
         const int64_t len = s == RO_SUCCESS ? o1 - o0 : 0;
         if (len >= ((int64_t)1 << 32)) { err = RO_EOVERFLOW; continue; }
+        if (gf_rejected(barrier, gkey, epoch, p, i)) { ++rej; continue; }
+        if (s == RO_GROUP_FAILED) s = RO_FAILED;
         ++cnt;
         if (cap_ok) {
             Canon e;
@@ -79,6 +128,11 @@ __global__ __launch_bounds__(kBlock) void k_gather_scatter(
     const int64_t tot = block_sum(cnt, s_wave);
     if (threadIdx.x == 0 && tot)
         __hip_atomic_fetch_add(&ctl->n_valid, tot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (barrier) {
+        const int64_t r = block_sum(rej, s_wave);
+        if (threadIdx.x == 0 && r)
+            __hip_atomic_fetch_add(&ctl->n_rejected, r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
 }
 
 // ---------------------------------------------------------------- scan
@@ -282,8 +336,10 @@ __global__ __launch_bounds__(kBlock) void k_gather_finalize(
     const int64_t *__restrict__ offsets, int64_t P, int64_t canon_cap, int64_t *__restrict__ out_off,
     int64_t out_cap, int has_data, const int32_t *__restrict__ ns, const int32_t *__restrict__ nf,
     const int32_t *__restrict__ nk, uint8_t *__restrict__ complete, uint8_t *__restrict__ pstate,
-    int64_t *__restrict__ cdst, Ctl *ctl)
+    int64_t *__restrict__ cdst, uint8_t *__restrict__ barrier, const uint64_t *__restrict__ gkey,
+    int64_t *n_rejected, Ctl *ctl)
 {
+    const uint32_t epoch = ctl->canon_epoch;
     const int64_t N0 = offsets[P];
     const int64_t N = N0 <= canon_cap ? N0 : 0;
     const int64_t total = N > 0 ? ctl->total : 0;
@@ -291,6 +347,7 @@ __global__ __launch_bounds__(kBlock) void k_gather_finalize(
     if (gtid == 0) {
         if (out_off) out_off[P] = total;
         if (cdst && N0 <= canon_cap) cdst[N0] = total;
+        if (n_rejected) *n_rejected = ctl->n_rejected;
         if (ctl->n_filled != ctl->n_valid) raise_err(ctl, RO_EDUP);
         if (has_data && total > out_cap) raise_err(ctl, RO_ECAP);
     }
@@ -299,9 +356,15 @@ __global__ __launch_bounds__(kBlock) void k_gather_finalize(
         const int64_t k = offsets[p + 1] - st;
         if (st >= N && out_off) out_off[p] = total;       // no child at or after its start
         const int64_t a = ns ? ns[p] : 0, b = nf ? nf[p] : 0, c = nk ? nk[p] : 0;
-        const bool done = (a + b + c) == k;
+        // a barred parent's uncommitted children are suppressed: it is done
+        bool barred = false;
+        if (barrier) {
+            barred = barrier[p] || (uint32_t)(gkey[p] >> 32) == epoch;
+            if (barred) barrier[p] = 1;
+        }
+        const bool done = barred || (a + b + c) == k;
         if (complete) complete[p] = done ? 1 : 0;
-        if (pstate) pstate[p] = !done ? RO_PENDING : (b > 0 ? RO_FAILED : RO_SUCCESS);
+        if (pstate) pstate[p] = !done ? RO_PENDING : ((barred || b > 0) ? RO_FAILED : RO_SUCCESS);
     }
 }
 
@@ -315,6 +378,7 @@ __global__ void k_gather_reset(Ctl *ctl)
         ctl->n_valid = 0;
         ctl->n_filled = 0;
         ctl->total = 0;
+        ctl->n_rejected = 0;
         ctl->canon_epoch = ctl->canon_epoch + 1;
     }
 }
@@ -416,12 +480,16 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_
     }
 }
 
-hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w)
+hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w, uint32_t epoch)
 {
+    if (a.barrier != nullptr && a.n > 0) {
+        const hipError_t e = launch_first_gf(L, a.rs, a.rp, a.n, a.P, a.barrier, w.gkey, epoch);
+        if (e != hipSuccess) return e;
+    }
     const int64_t grid_r = (int64_t)L.num_cus * 8;
     RO_LAUNCH(L, RO_K_GATHER_SCATTER, k_gather_scatter, dim3((unsigned)grid_r), dim3(kBlock), 0, L.stream,
               a.rp, a.ro, a.rs, a.roff, a.data, a.n, a.offsets, a.P, w.canon, w.canon_cap, a.ns, a.nf,
-              a.nk, L.ctl);
+              a.nk, a.barrier, w.gkey, L.ctl);
     const int64_t grid_s = (int64_t)L.num_cus * 4;
     RO_LAUNCH(L, RO_K_GATHER_SCAN, k_gather_scan, dim3((unsigned)grid_s), dim3(kBlock), 0, L.stream, a.offsets, a.P,
               w.canon, w.canon_cap, a.out_off, a.ns, a.nf, a.nk, a.cdst, w.sub_base, L.ctl, L.desc, L.desc_cap);
@@ -429,7 +497,7 @@ hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w
     grid_f = grid_f < 1 ? 1 : (grid_f > (int64_t)L.num_cus * 8 ? (int64_t)L.num_cus * 8 : grid_f);
     RO_LAUNCH(L, RO_K_GATHER_FINALIZE, k_gather_finalize, dim3((unsigned)grid_f), dim3(kBlock), 0, L.stream, a.offsets,
                        a.P, w.canon_cap, a.out_off, a.out_cap, a.out_data != nullptr ? 1 : 0, a.ns, a.nf,
-                       a.nk, a.complete, a.pstate, a.cdst, L.ctl);
+                       a.nk, a.complete, a.pstate, a.cdst, a.barrier, w.gkey, a.n_rejected, L.ctl);
     if (a.out_data != nullptr) {
         const int64_t grid_c = (int64_t)L.num_cus * 8;
         RO_LAUNCH(L, RO_K_GATHER_COPY, k_gather_copy, dim3((unsigned)grid_c), dim3(kBlock), 0, L.stream, a.offsets,

@@ -23,8 +23,6 @@
 
 namespace ro {
 
-constexpr uint32_t kStreamEpoch = 1;      // slot tag epoch of an accepted stream report
-
 // How many children of a parent have reported, by its size k:
 //   k < kMid   the seen bits of its children (at most three words), no counter;
 //   k < kBig   one counter, indexed by its first child >> kMidShift;
@@ -77,22 +75,29 @@ __global__ void k_stream_check(const int64_t *__restrict__ offsets, int64_t P, i
     if (bad) raise_err(ctl, RO_EINVAL);
 }
 
+// One wave of reports.  Accepted slots are tagged with the run's epoch.
+// With a group-failure barrier, reports commit in order after every earlier
+// wave: one of a barred parent, or one after its parent's first group
+// failure in this wave, is rejected (counted into *n_rejected).
 __global__ __launch_bounds__(kBlock) void k_stream_report(
     const uint32_t *__restrict__ rp, const uint32_t *__restrict__ ro_, const uint8_t *__restrict__ rs,
     const int64_t *__restrict__ roff, const uint8_t *data, int64_t n, const int64_t *__restrict__ offsets,
     int64_t P, int64_t N, Canon *__restrict__ canon, uint32_t *__restrict__ seen, int32_t *__restrict__ mid,
-    int32_t *__restrict__ big, int64_t nslots, Ctl *ctl)
+    int32_t *__restrict__ big, int64_t nslots, uint32_t run_epoch, const uint8_t *__restrict__ barrier,
+    const uint64_t *__restrict__ gkey, uint32_t gf_epoch, int64_t *n_rejected, Ctl *ctl)
 {
+    __shared__ int64_t s_wave[kBlock / 64];
     const int64_t gtid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     const int64_t gstride = (int64_t)gridDim.x * kBlock;
     const int64_t spread = (int64_t)(((blockIdx.x << 2) + (threadIdx.x >> 6)) & (kSpread - 1)) * nslots;
     int err = 0;
+    int64_t rej = 0;
     if (gtid == 0 && n > 0 && roff[0] < 0) err = RO_EINVAL;
     for (int64_t i = gtid; i < n; i += gstride) {
-        const uint32_t s = rs[i];
+        uint32_t s = rs[i];
         const int64_t o0 = roff[i], o1 = roff[i + 1];
         if (o1 < o0) { err = RO_EINVAL; continue; }
-        if (s > RO_PENDING) { err = RO_ESTATE; continue; }
+        if (s > RO_PENDING && !(s == RO_GROUP_FAILED && barrier)) { err = RO_ESTATE; continue; }
         if (s == RO_PENDING) continue;
         const uint32_t p = rp[i];
         if ((int64_t)p >= P) { err = RO_ERANGE; continue; }
@@ -104,6 +109,8 @@ __global__ __launch_bounds__(kBlock) void k_stream_report(
         if (st < 0 || c >= N) { err = RO_EINVAL; continue; }
         const int64_t len = s == RO_SUCCESS ? o1 - o0 : 0;
         if (len >= ((int64_t)1 << 32)) { err = RO_EOVERFLOW; continue; }
+        if (gf_rejected(barrier, gkey, gf_epoch, p, i)) { ++rej; continue; }
+        if (s == RO_GROUP_FAILED) s = RO_FAILED;
         // first report of this child, in this wave or any earlier one
         const uint32_t bit = 1u << (c & 31);
         const uint32_t old = atomicOr(&seen[c >> 5], bit);
@@ -111,12 +118,17 @@ __global__ __launch_bounds__(kBlock) void k_stream_report(
         Canon e;
         e.src = reinterpret_cast<uint64_t>(data) + (uint64_t)o0;
         e.len = (uint32_t)len;
-        e.tag = (kStreamEpoch << 2) | s;
+        e.tag = (run_epoch << 2) | s;
         canon[c] = e;
         if (k >= kBig) atomicAdd(&big[spread + (st >> kBigShift)], 1);
         else if (k >= kMid) atomicAdd(&mid[st >> kMidShift], 1);
     }
     if (err) raise_err(ctl, err);
+    if (barrier) {
+        const int64_t r = block_sum(rej, s_wave);
+        if (threadIdx.x == 0 && r && n_rejected)
+            __hip_atomic_fetch_add(n_rejected, r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
 }
 
 // Newly complete parents, compacted in ascending order (one tile = 2048
@@ -128,7 +140,7 @@ constexpr int kSItems = kSTile / kBlock;
 __global__ __launch_bounds__(kBlock) void k_stream_select(
     const int64_t *__restrict__ offsets, int64_t P, const uint32_t *__restrict__ seen,
     const int32_t *__restrict__ mid, const int32_t *__restrict__ big, int64_t nslots,
-    uint8_t *__restrict__ emitted,
+    const uint8_t *__restrict__ barrier, uint8_t *__restrict__ ebar, uint8_t *__restrict__ emitted,
     int64_t *__restrict__ ebase, int64_t *__restrict__ evoff, uint32_t *__restrict__ emit_parent,
     int32_t *__restrict__ ecnt, int64_t ecnt_stride, int64_t cap_parents, int64_t *n_emitted, Ctl *ctl,
     uint64_t *desc, uint64_t *desc_kids, int64_t desc_cap, int64_t ntiles)
@@ -152,7 +164,8 @@ __global__ __launch_bounds__(kBlock) void k_stream_select(
             if (p < P && !emitted[p]) {
                 const int64_t st = offsets[p];
                 const int64_t kp = offsets[p + 1] - st;
-                if (reported(seen, mid, big, nslots, st, kp) == kp) {
+                // a barred parent is complete: its uncommitted children are suppressed
+                if ((barrier && barrier[p]) || reported(seen, mid, big, nslots, st, kp) == kp) {
                     fmask |= 1u << k;
                     kk[k] = (uint32_t)kp;
                     kids += kp;
@@ -174,6 +187,7 @@ __global__ __launch_bounds__(kBlock) void k_stream_select(
             if (e < cap_parents) {
                 ebase[e] = offsets[p] - run;      // canonical slot of virtual child v: ebase[e] + v
                 evoff[e] = run;
+                ebar[e] = (barrier && barrier[p]) ? 1 : 0;
                 if (emit_parent) emit_parent[e] = (uint32_t)p;
                 ecnt[e] = 0;
                 ecnt[ecnt_stride + e] = 0;
@@ -218,7 +232,8 @@ constexpr int kECntLds = 256;
 __global__ __launch_bounds__(kBlock) void k_emit_scan(
     const int64_t *__restrict__ evoff, const int64_t *__restrict__ ebase, const Canon *__restrict__ canon,
     int64_t *__restrict__ edst, uint64_t *__restrict__ esrc, int64_t *__restrict__ emit_off,
-    int32_t *__restrict__ ecnt, int64_t ecnt_stride, Ctl *ctl, uint64_t *desc, int64_t desc_cap)
+    int32_t *__restrict__ ecnt, int64_t ecnt_stride, uint32_t run_epoch, Ctl *ctl, uint64_t *desc,
+    int64_t desc_cap)
 {
     const int64_t E = ctl->n_items;
     const int64_t V = ctl->n_virtual;
@@ -291,7 +306,7 @@ __global__ __launch_bounds__(kBlock) void k_emit_scan(
                 }
                 const int64_t c = (lds_ok ? s_base[e - pf] : ebase[e]) + v;
                 const Canon x = canon[c];
-                if ((x.tag >> 2) == kStreamEpoch) {
+                if ((x.tag >> 2) == run_epoch) {
                     stv[k] = x.tag & 3u;
                     len[k] = stv[k] == RO_SUCCESS ? x.len : 0;
                     src[k] = x.src;
@@ -368,8 +383,8 @@ constexpr int64_t kEmitMinUnit = 1024;
 
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_WAVES))) void k_emit_out(
     int64_t *__restrict__ emit_off, const int64_t *__restrict__ evoff, const int32_t *__restrict__ ecnt,
-    int64_t ecnt_stride, int32_t *__restrict__ ns, int32_t *__restrict__ nf, int32_t *__restrict__ nk,
-    uint8_t *__restrict__ pstate, int64_t *n_bytes, const int64_t *__restrict__ edst,
+    int64_t ecnt_stride, const uint8_t *__restrict__ ebar, int32_t *__restrict__ ns, int32_t *__restrict__ nf,
+    int32_t *__restrict__ nk, uint8_t *__restrict__ pstate, int64_t *n_bytes, const int64_t *__restrict__ edst,
     const uint64_t *__restrict__ esrc, uint8_t *__restrict__ out, int64_t cap_bytes, Ctl *ctl)
 {
     constexpr int kWaves = kBlock / 64;
@@ -390,7 +405,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_
         if (ns) ns[e] = a;
         if (nf) nf[e] = f;
         if (nk) nk[e] = k;
-        if (pstate) pstate[e] = f > 0 ? RO_FAILED : RO_SUCCESS;
+        if (pstate) pstate[e] = (f > 0 || ebar[e]) ? RO_FAILED : RO_SUCCESS;
     }
     if (out == nullptr || T <= 0 || T > cap_bytes || read_err(ctl) != 0) return;
     const uint64_t outa = reinterpret_cast<uint64_t>(out);
@@ -438,20 +453,24 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_
 // for children of emitted parents, and those were all reported.
 __global__ void k_stream_clear(uint32_t *__restrict__ seen, int64_t n_seen, int32_t *__restrict__ mid,
                                int64_t n_mid, int32_t *__restrict__ big, int64_t n_big,
-                               uint8_t *__restrict__ emitted, int64_t n_emitted)
+                               uint8_t *__restrict__ emitted, uint8_t *__restrict__ barrier, int64_t n_emitted)
 {
     const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = g; i < n_seen; i += stride) seen[i] = 0;
     for (int64_t i = g; i < n_mid; i += stride) mid[i] = 0;
     for (int64_t i = g; i < n_big; i += stride) big[i] = 0;
-    for (int64_t i = g; i < n_emitted; i += stride) emitted[i] = 0;
+    for (int64_t i = g; i < n_emitted; i += stride) {
+        emitted[i] = 0;
+        if (barrier) barrier[i] = 0;
+    }
 }
 
 hipError_t launch_stream_reset(const Launch &L, StreamState &s)
 {
     RO_LAUNCH(L, RO_K_MISC, k_stream_clear, dim3((unsigned)L.num_cus * 4), dim3(256), 0, L.stream, s.seen,
-              (s.N + 31) / 32 + 1, s.mid, stream_mid_size(s.N), s.big, stream_big_size(s.N), s.emitted, s.P + 1);
+              (s.N + 31) / 32 + 1, s.mid, stream_mid_size(s.N), s.big, stream_big_size(s.N), s.emitted,
+              s.barrier, s.P);
     return launch_stream_init(L, s);
 }
 
@@ -463,13 +482,19 @@ hipError_t launch_stream_init(const Launch &L, StreamState &s)
 }
 
 hipError_t launch_stream_report(const Launch &L, StreamState &s, const uint32_t *rp, const uint32_t *ro,
-                                const uint8_t *rs, const int64_t *roff, const uint8_t *data, int64_t n)
+                                const uint8_t *rs, const int64_t *roff, const uint8_t *data, int64_t n,
+                                int64_t *n_rejected)
 {
+    if (s.barrier) {
+        const hipError_t e = launch_first_gf(L, rs, rp, n, s.P, s.barrier, s.gkey, s.gf_epoch);
+        if (e != hipSuccess) return e;
+    }
     int64_t grid = (n + kBlock - 1) / kBlock;
     grid = grid < 1 ? 1 : (grid > (int64_t)L.num_cus * 8 ? (int64_t)L.num_cus * 8 : grid);
     RO_LAUNCH(L, RO_K_STREAM_REPORT, k_stream_report, dim3((unsigned)grid), dim3(kBlock), 0, L.stream, rp, ro,
               rs, roff, data, n, s.offsets, s.P, s.N, s.canon, s.seen, s.mid, s.big, stream_big_slots(s.N),
-              L.ctl);
+              s.run_epoch, s.barrier, s.gkey, s.gf_epoch, n_rejected, L.ctl);
+    if (s.barrier) return launch_gf_fold(L, rs, rp, n, s.P, s.barrier, s.gkey, s.gf_epoch);
     return hipGetLastError();
 }
 
@@ -489,14 +514,15 @@ hipError_t launch_stream_emit(const Launch &L, StreamState &s, uint32_t *emit_pa
     const int64_t grid = ntiles < (int64_t)L.num_cus * 4 ? ntiles : (int64_t)L.num_cus * 4;
     const int64_t es = s.P + 1;
     RO_LAUNCH(L, RO_K_STREAM_SELECT, k_stream_select, dim3((unsigned)grid), dim3(kBlock), 0, L.stream,
-              s.offsets, s.P, s.seen, s.mid, s.big, stream_big_slots(s.N), s.emitted, s.ebase, s.evoff, emit_parent,
+              s.offsets, s.P, s.seen, s.mid, s.big, stream_big_slots(s.N), s.barrier, s.ebar, s.emitted, s.ebase,
+              s.evoff, emit_parent,
               s.ecnt, es, cap_parents, n_emitted, L.ctl, L.desc, L.desc + ntiles, L.desc_cap, ntiles);
     const int64_t grid_s = (int64_t)L.num_cus * 2;
     RO_LAUNCH(L, RO_K_STREAM_SCAN, k_emit_scan, dim3((unsigned)grid_s), dim3(kBlock), 0, L.stream, s.evoff,
-              s.ebase, s.canon, s.edst, s.esrc, emit_off, s.ecnt, es, L.ctl, L.desc, L.desc_cap);
+              s.ebase, s.canon, s.edst, s.esrc, emit_off, s.ecnt, es, s.run_epoch, L.ctl, L.desc, L.desc_cap);
     const int64_t grid_c = (int64_t)L.num_cus * 8;
     RO_LAUNCH(L, RO_K_STREAM_COPY, k_emit_out, dim3((unsigned)grid_c), dim3(kBlock), 0, L.stream, emit_off,
-              s.evoff, s.ecnt, es, ns, nf, nk, pstate, n_bytes, s.edst, s.esrc, emit_data, cap_bytes, L.ctl);
+              s.evoff, s.ecnt, es, s.ebar, ns, nf, nk, pstate, n_bytes, s.edst, s.esrc, emit_data, cap_bytes, L.ctl);
     return hipGetLastError();
 }
 

@@ -66,6 +66,7 @@ struct ro_ctx {
     uint32_t *cmap;           // coarse child -> parent map used by ro_batch
     int64_t cmap_cap;
     int32_t *cnt;             // [3 * cnt_cap] counters used when the caller passes none
+    uint64_t *gkey;           // [cnt_cap] first group failure per parent (gather)
     int64_t cnt_cap;
     int64_t gathers;          // host shadow of the device canonical epoch
     Tracer *tracer;
@@ -148,10 +149,14 @@ int ensure_cnt(ro_ctx *c, int64_t parents)
     if (parents <= c->cnt_cap && c->cnt) return RO_OK;
     if (hipStreamSynchronize(c->stream) != hipSuccess) return RO_EHIP;
     (void)hipFree(c->cnt);
+    (void)hipFree(c->gkey);
     c->cnt = nullptr;
+    c->gkey = nullptr;
     c->cnt_cap = 0;
     const int64_t n = parents > 0 ? parents : 1;
     if (dev_alloc(&c->cnt, 3 * n) != hipSuccess) return RO_EHIP;
+    if (dev_alloc(&c->gkey, n) != hipSuccess) return RO_EHIP;
+    if (hipMemset(c->gkey, 0, (size_t)n * sizeof(uint64_t)) != hipSuccess) return RO_EHIP;
     c->cnt_cap = n;
     return RO_OK;
 }
@@ -160,6 +165,8 @@ int before_gather(ro_ctx *c)
 {
     if (c->gathers + 1 > (int64_t)kMaxCanonEpoch) {
         if (launch_reset_canon(launch_of(c), c->canon, c->canon_cap) != hipSuccess) return RO_EHIP;
+        // group-failure keys carry the same epoch
+        if (c->gkey && launch_zero_u64(launch_of(c), c->gkey, c->cnt_cap) != hipSuccess) return RO_EHIP;
         c->gathers = 1;
     }
     c->gathers += 1;
@@ -240,6 +247,7 @@ int ro_ctx_destroy(ro_ctx *c)
     (void)hipFree(c->sub_base);
     (void)hipFree(c->cmap);
     (void)hipFree(c->cnt);
+    (void)hipFree(c->gkey);
     if (c->tracer) {
         for (hipEvent_t e : c->tracer->pool) (void)hipEventDestroy(e);
         delete c->tracer;
@@ -285,7 +293,7 @@ int ro_expand(ro_ctx *c, const int32_t *counts, int64_t n_parents, int64_t *offs
 int ro_batch(ro_ctx *c, const uint32_t *queue, const uint8_t *keep, int64_t q_len,
              const int64_t *offsets, int64_t n_parents, int32_t batch_size,
              uint32_t *out_child, uint32_t *out_parent, uint32_t *out_ordinal, int64_t out_cap,
-             int64_t *n_out_dev, int64_t *n_batches_dev)
+             int64_t *n_out_dev, int64_t *n_batches_dev, const uint8_t *barrier)
 {
     if (!c || !offsets || q_len < 0 || n_parents < 0 || batch_size <= 0 || out_cap < 0 ||
         (q_len > 0 && !queue))
@@ -294,7 +302,7 @@ int ro_batch(ro_ctx *c, const uint32_t *queue, const uint8_t *keep, int64_t q_le
     if (rc) return rc;
     return hip_fail(launch_batch(launch_of(c), queue, keep, q_len, offsets, n_parents, batch_size,
                                  out_child, out_parent, out_ordinal, out_cap, n_out_dev, n_batches_dev,
-                                 c->cmap, c->cmap_cap));
+                                 c->cmap, c->cmap_cap, barrier));
 }
 
 int ro_gather(ro_ctx *c, const ro_reports *r, const int64_t *offsets, int64_t n_parents,
@@ -304,6 +312,7 @@ int ro_gather(ro_ctx *c, const ro_reports *r, const int64_t *offsets, int64_t n_
         return RO_EINVAL;
     if (r->n > 0 && (!r->parent || !r->ordinal || !r->state || !r->off)) return RO_EINVAL;
     if (o->out_data != nullptr && r->n > 0 && !r->data) return RO_EINVAL;
+    if (o->barrier != nullptr && r->n >= ((int64_t)1 << 32)) return RO_EINVAL;   // report index is 32-bit
     // the canonical workspace must cover the expansion; its size is on the
     // device, so the report count is the host's best lower bound
     int rc = ensure_canon(c, c->canon_cap > r->n ? c->canon_cap : r->n);
@@ -328,6 +337,9 @@ int ro_gather(ro_ctx *c, const ro_reports *r, const int64_t *offsets, int64_t n_
     a.complete = o->complete;
     a.pstate = o->parent_state;
     a.cdst = o->child_dst_off;
+    a.barrier = o->barrier;
+    a.n_rejected = o->n_rejected;
+    if (a.barrier && (rc = ensure_cnt(c, n_parents))) return rc;
     if (!a.ns || !a.nf || !a.nk) {
         if ((rc = ensure_cnt(c, n_parents))) return rc;
         if (!a.ns) a.ns = c->cnt;
@@ -339,12 +351,13 @@ int ro_gather(ro_ctx *c, const ro_reports *r, const int64_t *offsets, int64_t n_
     w.canon_cap = c->canon_cap;
     w.sub_base = c->sub_base;
     w.sub_cap = c->sub_cap;
+    w.gkey = c->gkey;
     if ((rc = before_gather(c))) return rc;
-    return hip_fail(launch_gather(launch_of(c), a, w));
+    return hip_fail(launch_gather(launch_of(c), a, w, (uint32_t)(c->gathers - 1)));
 }
 
 int ro_stream_create(ro_ctx *c, const int64_t *offsets, int64_t n_parents, int64_t n_children,
-                     ro_stream **out)
+                     uint8_t *barrier, ro_stream **out)
 {
     if (out) *out = nullptr;
     if (!c || !offsets || !out || n_parents < 0 || n_children < 0 || n_children >= ((int64_t)1 << 32))
@@ -364,6 +377,8 @@ int ro_stream_create(ro_ctx *c, const int64_t *offsets, int64_t n_parents, int64
         (size_t)(3 * (P + 1)) * sizeof(int32_t),            // ecnt
         (size_t)(N + 1) * sizeof(int64_t),                  // edst
         (size_t)(N + 1) * sizeof(uint64_t),                 // esrc
+        (size_t)(P + 1) * sizeof(uint64_t),                 // gkey
+        (size_t)(P + 1),                                    // ebar
     };
     constexpr int kArrays = (int)(sizeof(sizes) / sizeof(sizes[0]));
     size_t offs[kArrays], total = 0;
@@ -399,6 +414,11 @@ int ro_stream_create(ro_ctx *c, const int64_t *offsets, int64_t n_parents, int64
     st.ecnt = (int32_t *)(block + offs[7]);
     st.edst = (int64_t *)(block + offs[8]);
     st.esrc = (uint64_t *)(block + offs[9]);
+    st.gkey = (uint64_t *)(block + offs[10]);
+    st.ebar = (uint8_t *)(block + offs[11]);
+    st.barrier = barrier;
+    st.run_epoch = 1;
+    st.gf_epoch = 0;
     if (launch_stream_init(launch_of(c), st) != hipSuccess) {
         (void)hipFree(block);
         free(s);
@@ -408,13 +428,22 @@ int ro_stream_create(ro_ctx *c, const int64_t *offsets, int64_t n_parents, int64
     return RO_OK;
 }
 
-int ro_stream_report(ro_ctx *c, ro_stream *s, const ro_reports *r)
+int ro_stream_report(ro_ctx *c, ro_stream *s, const ro_reports *r, int64_t *n_rejected_dev)
 {
     if (!c || !s || !r || s->ctx != c || r->n < 0) return RO_EINVAL;
     if (r->n > 0 && (!r->parent || !r->ordinal || !r->state || !r->off)) return RO_EINVAL;
+    if (s->st.barrier != nullptr && r->n >= ((int64_t)1 << 32)) return RO_EINVAL;
     if (r->n == 0) return RO_OK;
+    if (s->st.barrier != nullptr) {
+        // a new epoch for this call's first group failures
+        if (s->st.gf_epoch == 0xffffffffu) {
+            if (launch_zero_u64(launch_of(c), s->st.gkey, s->st.P + 1) != hipSuccess) return RO_EHIP;
+            s->st.gf_epoch = 0;
+        }
+        s->st.gf_epoch += 1;
+    }
     return hip_fail(launch_stream_report(launch_of(c), s->st, r->parent, r->ordinal, r->state, r->off, r->data,
-                                         r->n));
+                                         r->n, n_rejected_dev));
 }
 
 int ro_stream_emit(ro_ctx *c, ro_stream *s, uint32_t *emit_parent, int64_t *emit_off,
@@ -431,6 +460,12 @@ int ro_stream_emit(ro_ctx *c, ro_stream *s, uint32_t *emit_parent, int64_t *emit
 int ro_stream_reset(ro_ctx *c, ro_stream *s)
 {
     if (!c || !s || s->ctx != c) return RO_EINVAL;
+    // a new slot epoch, so that the slots of the previous run read as unreported
+    if (s->st.run_epoch + 1 > kMaxCanonEpoch) {
+        if (launch_clear_tags(launch_of(c), s->st.canon, s->st.N) != hipSuccess) return RO_EHIP;
+        s->st.run_epoch = 0;
+    }
+    s->st.run_epoch += 1;
     return hip_fail(launch_stream_reset(launch_of(c), s->st));
 }
 

@@ -288,6 +288,26 @@ __device__ __forceinline__ int lds_first_ge(const int16_t *a, int lo, int hi, in
     return lo;
 }
 
+// Group-failure commit rule (Sec. 4 "Commit, Failure, and Recovery"), for
+// report i of parent p in a call whose first group failure per parent is
+// recorded in gkey as (epoch << 32 | ~index): the report is rejected if p was
+// barred before this call or if p's first group failure comes earlier in
+// this call's report order.
+__device__ __forceinline__ bool gf_rejected(const uint8_t *barrier, const uint64_t *gkey, uint32_t epoch,
+                                            uint32_t p, int64_t i)
+{
+    if (barrier == nullptr) return false;
+    if (barrier[p]) return true;
+    const uint64_t k = gkey[p];
+    if ((uint32_t)(k >> 32) != epoch) return false;
+    return i > (int64_t)(0xffffffffu - (uint32_t)k);
+}
+
+__device__ __forceinline__ uint64_t gf_key(uint32_t epoch, int64_t i)
+{
+    return ((uint64_t)epoch << 32) | (uint64_t)(0xffffffffu - (uint32_t)i);
+}
+
 __device__ __forceinline__ int64_t min64(int64_t a, int64_t b) { return a < b ? a : b; }
 __device__ __forceinline__ int64_t max64(int64_t a, int64_t b) { return a > b ? a : b; }
 

@@ -35,9 +35,10 @@ struct Ctl {
     int64_t total;           // gather / emit: total bytes
     int64_t n_items;         // emit: emitted parents
     int64_t n_virtual;       // emit: children of emitted parents
+    int64_t n_rejected;      // gather: reports rejected by a group-failure barrier
     uint32_t scan_epoch;     // look-back descriptor epoch of the next ticketed launch (1..65535)
     uint32_t canon_epoch;    // canonical-slot epoch of the next gather (1..2^30-1)
-    int64_t pad[8];
+    int64_t pad[7];
 };
 
 struct Tracer;
@@ -69,6 +70,8 @@ constexpr uint32_t kMaxCanonEpoch = (1u << 30) - 1;
 hipError_t launch_reset_scan_epoch(const Launch &L);
 hipError_t launch_reset_canon(const Launch &L, Canon *canon, int64_t n);
 hipError_t launch_ctl_init(const Launch &L);
+hipError_t launch_zero_u64(const Launch &L, uint64_t *p, int64_t n);
+hipError_t launch_clear_tags(const Launch &L, Canon *canon, int64_t n);
 
 // ---- launchers (defined in the kernel sources) ----------------------------
 hipError_t launch_expand(const Launch &L, const int32_t *counts, int64_t P,
@@ -79,7 +82,7 @@ hipError_t launch_batch(const Launch &L, const uint32_t *queue, const uint8_t *k
                         int64_t Q, const int64_t *offsets, int64_t P, int32_t B,
                         uint32_t *out_child, uint32_t *out_parent, uint32_t *out_ordinal,
                         int64_t out_cap, int64_t *n_out, int64_t *n_batches, uint32_t *cmap,
-                        int64_t cmap_cap);
+                        int64_t cmap_cap, const uint8_t *barrier);
 
 struct GatherArgs {
     const uint32_t *rp, *ro;
@@ -95,6 +98,8 @@ struct GatherArgs {
     int32_t *ns, *nf, *nk;
     uint8_t *complete, *pstate;
     int64_t *cdst;           // per-child output positions (or null)
+    uint8_t *barrier;        // group-failure barrier of the Call (or null)
+    int64_t *n_rejected;     // device scalar (or null)
 };
 
 struct GatherWs {
@@ -102,9 +107,12 @@ struct GatherWs {
     int64_t canon_cap;
     int64_t *sub_base;       // per copy sub-tile: first output byte
     int64_t sub_cap;
+    uint64_t *gkey;          // [P] first group failure per parent (epoch << 32 | ~report index)
 };
 
-hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w);
+// epoch: the canonical epoch of this gather (the host's shadow of the device
+// one), which also tags its group-failure keys
+hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w, uint32_t epoch);
 
 // streaming
 struct StreamState {
@@ -120,7 +128,21 @@ struct StreamState {
     int32_t *ecnt;           // [3*(P+1)] SUCCESS / FAILED / SKIPPED counts per emitted parent
     int64_t *edst;           // [N+1] output position of each virtual child
     uint64_t *esrc;          // [N] source address of each virtual child's bytes
+    uint8_t *barrier;        // [P] the Call's group-failure barrier (caller's, or null)
+    uint64_t *gkey;          // [P] first group failure per parent in the current report call
+    uint8_t *ebar;           // [P] per emitted parent: barred
+    uint32_t run_epoch;      // slot tag epoch of this run (advanced by each reset)
+    uint32_t gf_epoch;       // epoch of the current report call in gkey
 };
+
+// First group-failure report of each parent among reports [0, n), as the
+// largest key (epoch << 32 | ~i); reports of parents already barred are
+// skipped.  Then, after the commit pass, set the barrier of every parent
+// whose first group failure is in this call.
+hipError_t launch_first_gf(const Launch &L, const uint8_t *rs, const uint32_t *rp, int64_t n, int64_t P,
+                           const uint8_t *barrier, uint64_t *gkey, uint32_t epoch);
+hipError_t launch_gf_fold(const Launch &L, const uint8_t *rs, const uint32_t *rp, int64_t n, int64_t P,
+                          uint8_t *barrier, const uint64_t *gkey, uint32_t epoch);
 
 int64_t stream_mid_size(int64_t N);
 int64_t stream_big_size(int64_t N);
@@ -129,7 +151,7 @@ hipError_t launch_stream_init(const Launch &L, StreamState &s);
 hipError_t launch_stream_reset(const Launch &L, StreamState &s);
 hipError_t launch_stream_report(const Launch &L, StreamState &s, const uint32_t *rp,
                                 const uint32_t *ro, const uint8_t *rs, const int64_t *roff,
-                                const uint8_t *data, int64_t n);
+                                const uint8_t *data, int64_t n, int64_t *n_rejected);
 hipError_t launch_stream_emit(const Launch &L, StreamState &s,
                               uint32_t *emit_parent, int64_t *emit_off, uint8_t *emit_data,
                               int64_t cap_parents, int64_t cap_bytes, int32_t *ns, int32_t *nf,

@@ -11,10 +11,11 @@ import ctypes as C
 import os
 
 __all__ = ["RoError", "load", "Context", "Stream", "KERNELS", "OK", "EINVAL", "ERANGE", "EDUP", "ECAP",
-           "EOVERFLOW", "ESTATE", "EHIP", "SUCCESS", "FAILED", "SKIPPED", "PENDING", "LIB_PATH"]
+           "EOVERFLOW", "ESTATE", "EHIP", "SUCCESS", "FAILED", "SKIPPED", "PENDING", "GROUP_FAILED",
+           "LIB_PATH"]
 
 OK, EINVAL, ERANGE, EDUP, ECAP, EOVERFLOW, ESTATE, EHIP = 0, -1, -2, -3, -4, -5, -6, -7
-SUCCESS, FAILED, SKIPPED, PENDING = 0, 1, 2, 3
+SUCCESS, FAILED, SKIPPED, PENDING, GROUP_FAILED = 0, 1, 2, 3, 4
 
 # kernel kinds reported by Context.trace_read, in the C enum's order
 KERNELS = ["expand_scan", "expand_tags", "batch_samples", "batch", "gather_scatter", "gather_scan",
@@ -38,7 +39,8 @@ class ReportsT(C.Structure):
 class GatherOutT(C.Structure):
     _fields_ = [("out_off", C.c_void_p), ("out_data", C.c_void_p), ("out_cap", C.c_int64),
                 ("n_success", C.c_void_p), ("n_failed", C.c_void_p), ("n_skipped", C.c_void_p),
-                ("complete", C.c_void_p), ("parent_state", C.c_void_p), ("child_dst_off", C.c_void_p)]
+                ("complete", C.c_void_p), ("parent_state", C.c_void_p), ("child_dst_off", C.c_void_p),
+                ("barrier", C.c_void_p), ("n_rejected", C.c_void_p)]
 
 
 _lib = None
@@ -61,10 +63,10 @@ def load(path=None):
     L.ro_ctx_status.argtypes = [P]
     L.ro_ctx_destroy.argtypes = [P]
     L.ro_expand.argtypes = [P, P, i64, P, P, P, i64]
-    L.ro_batch.argtypes = [P, P, P, i64, P, i64, i32, P, P, P, i64, P, P]
+    L.ro_batch.argtypes = [P, P, P, i64, P, i64, i32, P, P, P, i64, P, P, P]
     L.ro_gather.argtypes = [P, C.POINTER(ReportsT), P, i64, C.POINTER(GatherOutT)]
-    L.ro_stream_create.argtypes = [P, P, i64, i64, pp]
-    L.ro_stream_report.argtypes = [P, P, C.POINTER(ReportsT)]
+    L.ro_stream_create.argtypes = [P, P, i64, i64, P, pp]
+    L.ro_stream_report.argtypes = [P, P, C.POINTER(ReportsT), P]
     L.ro_stream_emit.argtypes = [P, P, P, P, P, i64, i64, P, P, P, P, P, P]
     L.ro_stream_reset.argtypes = [P, P]
     L.ro_stream_destroy.argtypes = [P]
@@ -143,29 +145,30 @@ class Context:
                                 _ptr(child_parent), _ptr(child_ordinal), cap), "ro_expand")
 
     def batch(self, queue, keep, offsets, batch_size, out_child=None, out_parent=None,
-              out_ordinal=None, n_out=None, n_batches=None, q_len=None, out_cap=None):
+              out_ordinal=None, n_out=None, n_batches=None, q_len=None, out_cap=None, barrier=None):
         q_len = queue.numel() if q_len is None else q_len
         if out_cap is None:
             outs = [t.numel() for t in (out_child, out_parent, out_ordinal) if t is not None]
             out_cap = min(outs) if outs else q_len
         _check(self.L.ro_batch(self.h, _ptr(queue), _ptr(keep), q_len, _ptr(offsets),
                                offsets.numel() - 1, int(batch_size), _ptr(out_child), _ptr(out_parent),
-                               _ptr(out_ordinal), int(out_cap), _ptr(n_out), _ptr(n_batches)),
+                               _ptr(out_ordinal), int(out_cap), _ptr(n_out), _ptr(n_batches), _ptr(barrier)),
                "ro_batch")
 
     def gather(self, parent, ordinal, state, off, data, offsets, out_off, out_data=None,
                n_success=None, n_failed=None, n_skipped=None, complete=None, parent_state=None,
-               n=None, out_cap=None, child_dst_off=None):
+               n=None, out_cap=None, child_dst_off=None, barrier=None, n_rejected=None):
         rep = _reports(parent, ordinal, state, off, data, n)
         if out_cap is None:
             out_cap = out_data.numel() if out_data is not None else 0
         out = GatherOutT(_ptr(out_off), _ptr(out_data), int(out_cap), _ptr(n_success), _ptr(n_failed),
-                         _ptr(n_skipped), _ptr(complete), _ptr(parent_state), _ptr(child_dst_off))
+                         _ptr(n_skipped), _ptr(complete), _ptr(parent_state), _ptr(child_dst_off),
+                         _ptr(barrier), _ptr(n_rejected))
         _check(self.L.ro_gather(self.h, C.byref(rep), _ptr(offsets), offsets.numel() - 1, C.byref(out)),
                "ro_gather")
 
-    def stream(self, offsets, n_children):
-        return Stream(self, offsets, n_children)
+    def stream(self, offsets, n_children, barrier=None):
+        return Stream(self, offsets, n_children, barrier)
 
     def close(self):
         if getattr(self, "h", None):
@@ -182,17 +185,19 @@ class Context:
 class Stream:
     """Streaming gather over one expansion."""
 
-    def __init__(self, ctx, offsets, n_children):
+    def __init__(self, ctx, offsets, n_children, barrier=None):
         self.ctx = ctx
         self.offsets = offsets
+        self.barrier = barrier          # kept alive: the library holds it by reference
         h = C.c_void_p()
         _check(ctx.L.ro_stream_create(ctx.h, _ptr(offsets), offsets.numel() - 1, int(n_children),
-                                      C.byref(h)), "ro_stream_create")
+                                      _ptr(barrier), C.byref(h)), "ro_stream_create")
         self.h = h
 
-    def report(self, parent, ordinal, state, off, data, n=None):
+    def report(self, parent, ordinal, state, off, data, n=None, n_rejected=None):
         rep = _reports(parent, ordinal, state, off, data, n)
-        _check(self.ctx.L.ro_stream_report(self.ctx.h, self.h, C.byref(rep)), "ro_stream_report")
+        _check(self.ctx.L.ro_stream_report(self.ctx.h, self.h, C.byref(rep), _ptr(n_rejected)),
+               "ro_stream_report")
 
     def emit(self, emit_parent, emit_off, emit_data, n_success=None, n_failed=None, n_skipped=None,
              parent_state=None, n_emitted=None, n_bytes=None, cap_parents=None, cap_bytes=None):

@@ -633,3 +633,39 @@ def test_stream_group_failure_emits_at_barrier():
             else:
                 assert p not in emitted_in
         st.close()
+
+
+def test_group_failure_trace_schedule():
+    """The failure-containment analog on the oracle: every page is either
+    dispatched or suppressed, every dispatched report either commits or is
+    rejected, the 99 poisoned first pages all commit, only poisoned documents
+    lose pages, and every document is emitted once (poisoned ones FAILED with
+    the pages committed before their barrier)."""
+    from failure_sched import oracle_waves
+    t = W.failure_trace()
+    N, P = t.n_children, t.n_parents
+    assert (N, P, len(t.poisoned)) == (45_507, 1_885, 99)
+    assert N - len(t.poisoned) == 45_408                       # non-trigger pages
+    assert int(t.counts[t.poisoned].sum()) - len(t.poisoned) == 23_514
+    offs, waves = oracle_waves(t)
+    disp = np.concatenate([w["dispatched"] for w in waves])
+    supp = sum(w["suppressed"] for w in waves)
+    rej = sum(w["rejected"] for w in waves)
+    assert len(disp) + supp == N and len(np.unique(disp)) == len(disp)
+    parent_of = np.repeat(np.arange(P), t.counts)
+    poisoned = np.zeros(P, bool)
+    poisoned[t.poisoned] = True
+    assert poisoned[parent_of[np.setdiff1d(np.arange(N), disp)]].all()   # only their pages are suppressed
+    trig = offs[t.poisoned]
+    assert np.isin(trig, disp).all()
+    emitted = np.concatenate([w["emitted"]["parent"] for w in waves])
+    states = np.concatenate([w["emitted"]["parent_state"] for w in waves])
+    assert np.array_equal(np.sort(emitted), np.arange(P))
+    assert (states[poisoned[emitted]] == O.FAILED).all() and (states[~poisoned[emitted]] == O.SUCCESS).all()
+    ns = np.concatenate([w["emitted"]["n_success"] for w in waves])
+    nf = np.concatenate([w["emitted"]["n_failed"] for w in waves])
+    assert (nf[poisoned[emitted]] == 1).all()
+    committed = len(disp) - rej
+    assert int(ns.sum() + nf.sum()) == committed
+    print(f"group-failure trace: {len(waves)} waves, {len(disp)} dispatched, {supp} suppressed, "
+          f"{rej} rejected, {committed} committed")

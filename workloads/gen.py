@@ -19,19 +19,19 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-SUCCESS, FAILED, SKIPPED, PENDING = 0, 1, 2, 3
+SUCCESS, FAILED, SKIPPED, PENDING, GROUP_FAILED = 0, 1, 2, 3, 4
 
 _GAMMA = np.uint64(0x9E3779B97F4A7C15)
 _M1 = np.uint64(0xBF58476D1CE4E5B9)
 _M2 = np.uint64(0x94D049BB133111EB)
 
 __all__ = [
-    "SUCCESS", "FAILED", "SKIPPED", "PENDING",
+    "SUCCESS", "FAILED", "SKIPPED", "PENDING", "GROUP_FAILED",
     "splitmix64_words", "record_bytes", "content_seed",
     "trunc_zipf", "lognormal_int", "pareto_int", "rank_zipf_counts",
     "Reports", "SingleLevel", "Nested", "Streaming",
     "single_level", "config1", "config2", "config3", "config4", "config5",
-    "nested", "streaming", "CONFIG_NAMES",
+    "nested", "streaming", "CONFIG_NAMES", "FailureTrace", "failure_trace",
 ]
 
 
@@ -129,7 +129,14 @@ def rank_zipf_counts(rng, n_parents, n_children, s, lo, hi):
     unclamped ranks whose rounding moved them furthest.  Ranks are assigned to
     parents by a seeded permutation.
     """
-    w = np.arange(1, n_parents + 1, dtype=np.float64) ** (-s)
+    counts = _rank_counts(np.arange(1, n_parents + 1), n_children, s, lo, hi)
+    perm = rng.permutation(n_parents)
+    return counts[perm]
+
+
+def _rank_counts(ranks, n_children, s, lo, hi):
+    """clip(rint(C * r^-s), lo, hi) over the given ranks, summing to n_children."""
+    w = np.asarray(ranks, dtype=np.float64) ** (-s)
     lo_c, hi_c = 0.0, float(n_children) / w[-1] + 1.0
 
     def total(c):
@@ -153,8 +160,7 @@ def rank_zipf_counts(rng, n_parents, n_children, s, lo, hi):
         order = cand[np.argsort(-(counts[cand] - x[cand]), kind="stable")]
         counts[order[:-resid]] -= 1
     assert int(counts.sum()) == n_children
-    perm = rng.permutation(n_parents)
-    return counts[perm]
+    return counts
 
 
 # --------------------------------------------------------------------------
@@ -398,6 +404,66 @@ def config5(n_parents=500_000, n_children=10_000_000, n_waves=50, seed=4):
         lambda r: rank_zipf_counts(r, n_parents, n_children, 1.1, 1, 100_000),
         lambda r, n: r.integers(64, 513, n),
         n_waves, 1024)
+
+
+@dataclass
+class FailureTrace:
+    """A Call whose ready queue holds every child of a long-tailed document
+    set, pages of one document in page order and documents interleaved; the
+    first page of each of the largest documents reports a group failure."""
+    name: str
+    seed: int
+    counts: np.ndarray      # int32[P]
+    queue: np.ndarray       # uint32[N] ready order (canonical child ids)
+    states: np.ndarray      # uint8[N] canonical report state
+    lengths: np.ndarray     # int64[N] record length
+    poisoned: np.ndarray    # int64[n_poisoned] parent ids
+    wave: int               # entries reserved per wave (actors x batch)
+    batch_size: int
+
+    @property
+    def n_parents(self):
+        return len(self.counts)
+
+    @property
+    def n_children(self):
+        return len(self.lengths)
+
+
+def failure_trace(seed=5, n_parents=1_885, n_children=45_507, n_poisoned=99, poisoned_children=23_613,
+                  max_pages=427, actors=4, batch_size=48):
+    """Group-failure workload shaped by the paper's failure-containment
+    numbers (1,885 documents, 45,507 pages, the 99 largest documents poisoned
+    at page 0, 23,514 of their other pages; 1-427 pages per document; 4
+    actors with batches of 48).  Rank-frequency counts: the 99 largest
+    follow r^-0.5 and hold 23,613 pages, the rest follow r^-1 below the
+    smallest of them.  The ready queue is a seeded interleaving that keeps
+    each document's pages in page order.  Records are uniform in
+    [64, 512] bytes; every report succeeds except the poisoned first pages."""
+    rng = np.random.default_rng(seed)
+    top = _rank_counts(np.arange(1, n_poisoned + 1), poisoned_children, 0.5, 1, max_pages)
+    rest = _rank_counts(np.arange(n_poisoned + 1, n_parents + 1), n_children - poisoned_children, 1.0, 1,
+                        int(top.min()) - 1)
+    by_rank = np.concatenate([top, rest])
+    perm = rng.permutation(n_parents)            # parent perm[r] gets rank r
+    counts = np.empty(n_parents, np.int64)
+    counts[perm] = by_rank
+    poisoned = np.sort(perm[:n_poisoned])
+    # interleave documents, pages in order: draw a position for every page,
+    # then hand each document's positions to its pages in ascending order
+    n = int(counts.sum())
+    parent = np.repeat(np.arange(n_parents), counts)
+    pos = rng.permutation(n)
+    idx = np.lexsort((pos, parent))
+    pos_of_child = pos[idx]
+    queue = np.argsort(pos_of_child, kind="stable")
+    offsets = np.concatenate([[0], np.cumsum(counts)])
+    states = np.full(n, SUCCESS, np.uint8)
+    states[offsets[poisoned]] = GROUP_FAILED
+    lengths = rng.integers(64, 513, n).astype(np.int64)
+    return FailureTrace(name="group-failure trace", seed=seed, counts=counts.astype(np.int32),
+                        queue=queue.astype(np.uint32), states=states, lengths=lengths, poisoned=poisoned,
+                        wave=actors * batch_size, batch_size=batch_size)
 
 
 CONFIG_NAMES = {

@@ -21,6 +21,10 @@
  *   - Sec. 4 "Scheduling Ready Grains": one FIFO Ready Queue per Call holds
  *     ready Grains in enqueue order; elastic reservation removes at most B
  *     entries from its head and may mix parents.
+ *   - Sec. 4 input propagation and Table "primitives": F.filter keeps or
+ *     drops an Item in its own Domain, F.broadcast makes an ancestor's Item
+ *     available in a descendant Domain, both under the precedence failed /
+ *     suppressed, then unresolved, then dropped, then ready.
  *   - Sec. 4 "Commit, Failure, and Recovery": a typed GroupFailure puts a
  *     suppression barrier on one (Call, parent): queued siblings are
  *     suppressed before dispatch, in-flight siblings may finish but cannot
@@ -468,5 +472,66 @@ int oracle_stream_emit(oracle_stream *s, uint32_t *emit_parent, int64_t *emit_of
     emit_off[e] = pos;
     if (n_emitted) *n_emitted = e;
     if (n_bytes) *n_bytes = pos;
+    return OR_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* F.filter and F.broadcast, with the input propagation rule.                */
+/* ------------------------------------------------------------------------ */
+/* Sec. 4, input propagation: a failed or suppressed input suppresses the
+ * output; otherwise an unresolved input makes it wait; otherwise a dropped
+ * required input drops it; otherwise the output is ready.  In states:
+ * FAILED before PENDING before SKIPPED before SUCCESS. */
+static int propagate(int a, int b)
+{
+    if (a == ST_FAILED || b == ST_FAILED) return ST_FAILED;
+    if (a == ST_PENDING || b == ST_PENDING) return ST_PENDING;
+    if (a == ST_SKIPPED || b == ST_SKIPPED) return ST_SKIPPED;
+    return ST_SUCCESS;
+}
+
+/* F.filter(x, mask) (Table "primitives"): same Domain; the output passes x
+ * when the mask is true and is dropped when it is false, after the
+ * propagation rule over both inputs.  mask_state may be NULL (mask present). */
+int oracle_filter(const uint8_t *x_state, const uint8_t *mask_state, const uint8_t *mask, int64_t n,
+                  uint8_t *out_state)
+{
+    if (n < 0 || (n > 0 && (!x_state || !mask || !out_state)))
+        return OR_EINVAL;
+    for (int64_t i = 0; i < n; ++i) {
+        int ms = mask_state ? mask_state[i] : ST_SUCCESS;
+        if (x_state[i] > ST_PENDING || ms > ST_PENDING)
+            return OR_ESTATE;
+        int s = propagate(x_state[i], ms);
+        if (s == ST_SUCCESS && mask[i] == 0)
+            s = ST_SKIPPED;
+        out_state[i] = (uint8_t)s;
+    }
+    return OR_OK;
+}
+
+/* F.broadcast(x, like=y) (Table "primitives"): ancestor x made available in
+ * y's Domain.  maps[0] takes a descendant to its parent, maps[1] that parent
+ * to its own parent, and so on for `levels` levels; the last index is the
+ * ancestor.  The output state follows the propagation rule over x at the
+ * ancestor and y (like_state, NULL = present). */
+int oracle_broadcast(const uint32_t *const *maps, int32_t levels, int64_t n, const uint8_t *x_state,
+                     int64_t n_ancestors, const uint8_t *like_state, uint32_t *out_ancestor,
+                     uint8_t *out_state)
+{
+    if (n < 0 || levels < 1 || (n > 0 && (!maps || !x_state || !out_ancestor || !out_state)))
+        return OR_EINVAL;
+    for (int64_t d = 0; d < n; ++d) {
+        uint32_t a = (uint32_t)d;
+        for (int32_t l = 0; l < levels; ++l)
+            a = maps[l][a];
+        if ((int64_t)a >= n_ancestors)
+            return OR_ERANGE;
+        int ls = like_state ? like_state[d] : ST_SUCCESS;
+        if (x_state[a] > ST_PENDING || ls > ST_PENDING)
+            return OR_ESTATE;
+        out_ancestor[d] = a;
+        out_state[d] = (uint8_t)propagate(x_state[a], ls);
+    }
     return OR_OK;
 }

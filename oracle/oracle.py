@@ -15,7 +15,7 @@ import subprocess
 
 import numpy as np
 
-__all__ = ["build", "lib", "OracleError", "expand", "batch", "gather", "nested", "Stream",
+__all__ = ["build", "lib", "OracleError", "expand", "batch", "gather", "nested", "Stream", "filter", "broadcast",
            "OK", "EINVAL", "ERANGE", "EDUP", "ECAP", "EOVERFLOW", "ESTATE",
            "SUCCESS", "FAILED", "SKIPPED", "PENDING", "GROUP_FAILED"]
 
@@ -55,11 +55,13 @@ def _load(path):
     L.oracle_stream_create.restype = P
     L.oracle_stream_destroy.argtypes = [P]
     L.oracle_stream_report.argtypes = [P, P, P, P, P, P, i64, P]
+    L.oracle_filter.argtypes = [P, P, P, i64, P]
+    L.oracle_broadcast.argtypes = [P, C.c_int32, i64, P, i64, P, P, P]
     L.oracle_stream_barrier.argtypes = [P]
     L.oracle_stream_barrier.restype = C.POINTER(C.c_uint8)
     L.oracle_stream_emit.argtypes = [P, P, P, P, i64, i64, P, P, P, P, P, P]
     for f in ("oracle_expand", "oracle_batch", "oracle_gather", "oracle_stream_report",
-              "oracle_stream_emit"):
+              "oracle_stream_emit", "oracle_filter", "oracle_broadcast"):
         getattr(L, f).restype = C.c_int
     return L
 
@@ -192,6 +194,33 @@ def nested(counts1, queue1, keep1, batch1, counts2, queue2, keep2, batch2,
     return dict(offsets1=off1, parent1=par1, ordinal1=ord1, batch1=b1,
                 offsets2=off2, parent2=par2, ordinal2=ord2, batch2=b2,
                 low=low, up=up)
+
+
+def filter(x_state, mask, mask_state=None, L=None):
+    """F.filter: output state per item (SKIPPED where a present mask is false)."""
+    L = L or lib()
+    x_state = np.ascontiguousarray(x_state, dtype=np.uint8)
+    mask = np.ascontiguousarray(mask, dtype=np.uint8)
+    ms = None if mask_state is None else np.ascontiguousarray(mask_state, dtype=np.uint8)
+    out = np.zeros(max(len(x_state), 1), np.uint8)
+    _check(L.oracle_filter(_p(x_state), _p(ms), _p(mask), len(x_state), _p(out)), "filter")
+    return out[:len(x_state)]
+
+
+def broadcast(maps, x_state, like_state=None, L=None):
+    """F.broadcast: (ancestor index, output state) per descendant; maps[0]
+    is the descendant level's child->parent array, maps[1] the next, ..."""
+    L = L or lib()
+    maps = [np.ascontiguousarray(m, dtype=np.uint32) for m in maps]
+    n = len(maps[0])
+    x_state = np.ascontiguousarray(x_state, dtype=np.uint8)
+    ls = None if like_state is None else np.ascontiguousarray(like_state, dtype=np.uint8)
+    arr = (C.c_void_p * len(maps))(*[m.ctypes.data for m in maps])
+    anc = np.zeros(max(n, 1), np.uint32)
+    out = np.zeros(max(n, 1), np.uint8)
+    _check(L.oracle_broadcast(C.cast(arr, C.c_void_p), len(maps), n, _p(x_state), len(x_state), _p(ls),
+                              _p(anc), _p(out)), "broadcast")
+    return anc[:n], out[:n]
 
 
 class Stream:

@@ -669,3 +669,78 @@ def test_group_failure_trace_schedule():
     assert int(ns.sum() + nf.sum()) == committed
     print(f"group-failure trace: {len(waves)} waves, {len(disp)} dispatched, {supp} suppressed, "
           f"{rej} rejected, {committed} committed")
+
+
+# ---------------------------------------------------------------- filter / broadcast
+S, F, K, Pd = O.SUCCESS, O.FAILED, O.SKIPPED, O.PENDING
+
+
+def test_filter_mask_table_and_precedence():
+    """Table "primitives": on a present x and a present mask the output passes
+    x on true and is dropped on false; Sec. 4 propagation: a failed input
+    suppresses, an unresolved one waits (even next to a dropped one), a
+    dropped one drops; the two inputs play symmetric roles."""
+    xs, ms, mv = [], [], []
+    for x in (S, F, K, Pd):
+        for m in (S, F, K, Pd):
+            for v in (0, 1):
+                xs.append(x); ms.append(m); mv.append(v)
+    out = O.filter(np.array(xs), np.array(mv), np.array(ms))
+    got = {(x, m, v): o for x, m, v, o in zip(xs, ms, mv, out)}
+    assert got[(S, S, 1)] == S and got[(S, S, 0)] == K
+    for v in (0, 1):
+        for a in (S, F, K, Pd):
+            assert got[(F, a, v)] == F and got[(a, F, v)] == F
+            assert got[(a, S, 1)] == a                         # a true mask is the identity
+        assert got[(Pd, K, v)] == Pd and got[(K, Pd, v)] == Pd
+        assert got[(K, S, v)] == K and got[(S, K, v)] == K
+        for a in (S, F, K, Pd):
+            for b in (S, F, K, Pd):
+                if a != S and b != S:
+                    assert got[(a, b, v)] == got[(b, a, v)]
+    assert O.filter(np.zeros(0, np.uint8), np.zeros(0, np.uint8)).size == 0
+
+
+def test_filter_then_reduce_drops_masked_members():
+    """Filtered-out members are dropped, so the parent's slot is its
+    surviving members' bytes in ordinal order and they count as skipped."""
+    rng = np.random.default_rng(43)
+    counts = rng.integers(0, 6, 200).astype(np.int32)
+    offs, cp, co = O.expand(counts)
+    N = int(offs[-1])
+    lens = rng.integers(0, 9, N)
+    off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    data = rng.integers(0, 256, int(off[-1]) + 1, dtype=np.uint8)
+    mask = (rng.random(N) < 0.6).astype(np.uint8)
+    st = O.filter(np.zeros(N, np.uint8), mask)
+    g = O.gather(cp, co, st, off, data, offs)
+    for p in range(len(counts)):
+        cs = range(int(offs[p]), int(offs[p + 1]))
+        want = b"".join(bytes(data[off[c]:off[c + 1]]) for c in cs if mask[c])
+        assert bytes(g["out_data"][g["out_off"][p]:g["out_off"][p + 1]]) == want
+        assert g["n_skipped"][p] == sum(1 for c in cs if not mask[c])
+
+
+def test_broadcast_ancestor_by_composed_offsets():
+    """The ancestor of a leaf two levels down, by searching the two offset
+    arrays, equals the chained child->parent maps; its state follows x at
+    the ancestor and the leaf's own state."""
+    rng = np.random.default_rng(47)
+    for trial in range(20):
+        c1 = rng.integers(0, 5, int(rng.integers(1, 40))).astype(np.int32)
+        o1, p1, _ = O.expand(c1)
+        c2 = rng.integers(0, 5, int(o1[-1])).astype(np.int32)
+        o2, p2, _ = O.expand(c2)
+        n = int(o2[-1])
+        x = rng.choice(np.array([S, S, F, K, Pd], np.uint8), len(c1))
+        like = rng.choice(np.array([S, S, S, F, K, Pd], np.uint8), n)
+        anc, st = O.broadcast([p2, p1], x, like)
+        mid = np.searchsorted(o2, np.arange(n), side="right") - 1
+        top = np.searchsorted(o1, mid, side="right") - 1
+        assert np.array_equal(anc, top), trial
+        for d in range(n):
+            a, b = x[top[d]], like[d]
+            want = F if F in (a, b) else (Pd if Pd in (a, b) else (K if K in (a, b) else S))
+            assert st[d] == want
+    anc, st = O.broadcast([np.zeros(0, np.uint32)], np.zeros(1, np.uint8))
+    assert anc.size == 0 and st.size == 0

@@ -15,6 +15,8 @@ untimed by the generator's device fill):
   videos-nested two levels: 2,000 videos -> clips -> frames, 1,024-B frames.
   stream-waves  10^7 children under 500,000 parents turning terminal over 50
                 waves: per wave ro_batch, ro_stream_report, ro_stream_emit.
+  docs-ops      F.filter over the ~2.7M regions of the documents workload and
+                F.broadcast of a document-level Item to every region.
 
 Prints one JSON line.  Children/s counts every child entity created at every
 level (pages + regions, clips + frames).
@@ -34,7 +36,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, published
-WORKLOADS = ("zipf-single", "docs-nested", "videos-nested", "stream-waves")
+WORKLOADS = ("zipf-single", "docs-nested", "videos-nested", "stream-waves", "docs-ops")
 
 
 def parse():
@@ -310,6 +312,46 @@ def stage_stream(ctx, parents):
     return Job("stream-waves", step, N, alg_stream(P, N, total, len(s.waves), ew), cfg, check)
 
 
+def stage_ops(ctx, parents):
+    import torch
+    import workloads as W
+    from workloads import device as D
+    n = W.config3(n_docs=parents or 20_000)
+    P1, N1, N2 = len(n.counts1), len(n.queue1), len(n.queue2)
+    log(f"[bench] docs-ops: docs={P1} pages={N1} regions={N2}")
+    rng = np.random.default_rng(7)
+    st = np.array([0, 0, 0, 1, 2, 3], np.uint8)
+    xs = D.to_dev(rng.choice(st, N2))
+    ms = D.to_dev(rng.choice(st, N2))
+    mv = D.to_dev((rng.random(N2) < 0.5).astype(np.uint8))
+    doc_x = D.to_dev(rng.choice(st, P1))
+    like = D.to_dev(n.states)
+    o1 = torch.empty(P1 + 1, dtype=torch.int64, device="cuda")
+    o2 = torch.empty(N1 + 1, dtype=torch.int64, device="cuda")
+    p1 = torch.empty(N1, dtype=torch.int32, device="cuda")
+    p2 = torch.empty(N2, dtype=torch.int32, device="cuda")
+    ctx.reserve(N2, max(N1, P1), N2)
+    ctx.expand(D.to_dev(n.counts1), o1, p1, None)
+    ctx.expand(D.to_dev(n.counts2), o2, p2, None)
+    fout = torch.empty(N2, dtype=torch.uint8, device="cuda")
+    bst = torch.empty(N2, dtype=torch.uint8, device="cuda")
+    banc = torch.empty(N2, dtype=torch.int32, device="cuda")
+
+    def step():
+        ctx.filter(xs, mv, fout, mask_state=ms)
+        ctx.broadcast([p2, p1], doc_x, bst, banc, like)
+
+    def check():
+        assert int(fout.max().item()) <= 3 and int(bst.max().item()) <= 3
+
+    cfg = {"workload": f"F.filter over {N2} regions (state, mask state, mask) and F.broadcast of a document "
+                       f"Item to every region through two child->parent levels; documents workload, seed 2",
+           "regions": N2, "pages": N1, "documents": P1}
+    # filter: three state bytes in, one out; broadcast: region map, region state, ancestor and state out
+    # (the page map and document states stay in cache)
+    return Job("docs-ops", step, N2, {"misc": 4 * N2 + 10 * N2}, cfg, check)
+
+
 # ---------------------------------------------------------------- main
 
 def main():
@@ -346,6 +388,8 @@ def run(args):
         job = stage_zipf(ctx, args.parents)
     elif args.workload == "stream-waves":
         job = stage_stream(ctx, args.parents)
+    elif args.workload == "docs-ops":
+        job = stage_ops(ctx, args.parents)
     else:
         job = stage_nested(ctx, args.workload, args.parents)
     torch.cuda.synchronize()

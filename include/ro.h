@@ -187,6 +187,27 @@ typedef struct ro_gather_out {
 int ro_gather(ro_ctx *ctx, const ro_reports *reports, const int64_t *offsets, int64_t n_parents,
               const ro_gather_out *out);
 
+/* F.filter (Table "primitives"; Sec. 4 input propagation): for n Items of
+ * one Domain, out_state[i] derives from x_state[i] and the mask's state
+ * mask_state[i] (NULL = all present) by the propagation precedence (a
+ * FAILED input gives FAILED, else a PENDING one PENDING, else a SKIPPED one
+ * SKIPPED, else SUCCESS); a SUCCESS output whose mask[i] is 0 is dropped
+ * (SKIPPED).  The value of a passing Item is x's own record, so no bytes
+ * move.  A state above RO_PENDING is RO_ESTATE. */
+int ro_filter(ro_ctx *ctx, const uint8_t *x_state, const uint8_t *mask_state, const uint8_t *mask, int64_t n,
+              uint8_t *out_state);
+
+/* F.broadcast (Table "primitives"): make the ancestor Item x available in
+ * a descendant Domain of n Items.  maps[0] is the descendant level's
+ * child -> parent array (as ro_expand's child_parent), maps[1] the level
+ * above, ..., `levels` arrays in all (1..8); the last index reached is the
+ * ancestor (out_ancestor[d], may be NULL; >= n_ancestors is RO_ERANGE).
+ * out_state[d] combines x_state[ancestor] with like_state[d] (the
+ * descendant's own state, NULL = present) by the same precedence as
+ * ro_filter.  `maps` is a host array of device pointers. */
+int ro_broadcast(ro_ctx *ctx, const uint32_t *const *maps, int32_t levels, int64_t n, const uint8_t *x_state,
+                 int64_t n_ancestors, const uint8_t *like_state, uint32_t *out_ancestor, uint8_t *out_state);
+
 /* Streaming gather over one expansion (offsets[P+1] on the device, kept by
  * reference until ro_stream_destroy).  The stream's own state lives in
  * device memory allocated here (about 32 bytes per child and 42 per parent).

@@ -114,6 +114,13 @@ struct GatherWs {
 // one), which also tags its group-failure keys
 hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w, uint32_t epoch);
 
+// filter / broadcast
+constexpr int kMaxBroadcastLevels = 8;
+hipError_t launch_filter(const Launch &L, const uint8_t *xs, const uint8_t *ms, const uint8_t *mv, int64_t n,
+                         uint8_t *out);
+hipError_t launch_broadcast(const Launch &L, const uint32_t *const *maps, int32_t levels, int64_t n,
+                            const uint8_t *xs, int64_t n_anc, const uint8_t *ls, uint32_t *anc, uint8_t *out);
+
 // streaming
 struct StreamState {
     const int64_t *offsets;

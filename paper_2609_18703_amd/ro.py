@@ -69,12 +69,15 @@ def load(path=None):
     L.ro_stream_report.argtypes = [P, P, C.POINTER(ReportsT), P]
     L.ro_stream_emit.argtypes = [P, P, P, P, P, i64, i64, P, P, P, P, P, P]
     L.ro_stream_reset.argtypes = [P, P]
+    L.ro_filter.argtypes = [P, P, P, P, i64, P]
+    L.ro_broadcast.argtypes = [P, P, i32, i64, P, i64, P, P, P]
     L.ro_stream_destroy.argtypes = [P]
     L.ro_ctx_trace.argtypes = [P, C.c_int]
     L.ro_ctx_trace_read.argtypes = [P, P, P, i32]
     for name in ("ro_ctx_trace", "ro_ctx_trace_read", "ro_ctx_create", "ro_ctx_set_stream", "ro_ctx_reserve", "ro_ctx_status",
                  "ro_ctx_destroy", "ro_expand", "ro_batch", "ro_gather", "ro_stream_create",
-                 "ro_stream_report", "ro_stream_emit", "ro_stream_reset", "ro_stream_destroy"):
+                 "ro_stream_report", "ro_stream_emit", "ro_stream_reset", "ro_stream_destroy", "ro_filter",
+                 "ro_broadcast"):
         getattr(L, name).restype = C.c_int
     if path == LIB_PATH:
         _lib = L
@@ -166,6 +169,19 @@ class Context:
                          _ptr(barrier), _ptr(n_rejected))
         _check(self.L.ro_gather(self.h, C.byref(rep), _ptr(offsets), offsets.numel() - 1, C.byref(out)),
                "ro_gather")
+
+    def filter(self, x_state, mask, out_state, mask_state=None, n=None):
+        n = x_state.numel() if n is None else n
+        _check(self.L.ro_filter(self.h, _ptr(x_state), _ptr(mask_state), _ptr(mask), int(n), _ptr(out_state)),
+               "ro_filter")
+
+    def broadcast(self, maps, x_state, out_state, out_ancestor=None, like_state=None, n=None):
+        """maps: device tensors, the descendant level's child->parent first."""
+        n = maps[0].numel() if n is None else n
+        arr = (C.c_void_p * len(maps))(*[m.data_ptr() for m in maps])
+        _check(self.L.ro_broadcast(self.h, C.cast(arr, C.c_void_p), len(maps), int(n), _ptr(x_state),
+                                   x_state.numel(), _ptr(like_state), _ptr(out_ancestor), _ptr(out_state)),
+               "ro_broadcast")
 
     def stream(self, offsets, n_children, barrier=None):
         return Stream(self, offsets, n_children, barrier)

@@ -25,6 +25,9 @@
  *     drops an Item in its own Domain, F.broadcast makes an ancestor's Item
  *     available in a descendant Domain, both under the precedence failed /
  *     suppressed, then unresolved, then dropped, then ready.
+ *   - Sec. 4, Eq. (grain-phase) and Eq. (generation-fence): a report commits
+ *     only while its Grain is in flight at the report's generation; a retry
+ *     returns the Grain to READY at the next generation.
  *   - Sec. 4 "Commit, Failure, and Recovery": a typed GroupFailure puts a
  *     suppression barrier on one (Call, parent): queued siblings are
  *     suppressed before dispatch, in-flight siblings may finish but cannot
@@ -533,5 +536,130 @@ int oracle_broadcast(const uint32_t *const *maps, int32_t levels, int64_t n, con
         out_ancestor[d] = a;
         out_state[d] = (uint8_t)propagate(x_state[a], ls);
     }
+    return OR_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Grain phases and the generation fence.                                    */
+/* ------------------------------------------------------------------------ */
+/* Sec. 4, Eq. (grain-phase): WAITING -> READY -> IN-FLIGHT -> SEALED, and a
+ * retry takes IN-FLIGHT back to READY; Eq. (generation-fence): a report
+ * commits only if its Grain is in flight and the report's generation is the
+ * Grain's current one; publication rules: a repeat of a committed fact is
+ * idempotent, a conflicting one is rejected.  One Grain per child of an
+ * expansion, all READY at generation 0 to start with. */
+enum { PH_WAITING = 0, PH_READY = 1, PH_IN_FLIGHT = 2, PH_SEALED = 3 };
+
+typedef struct {
+    int64_t n;
+    uint8_t *phase;
+    uint32_t *gen;
+    int64_t *winner;             /* per child: report index accepted in the current commit call, or -1 */
+} oracle_grains;
+
+void oracle_grains_destroy(oracle_grains *g)
+{
+    if (!g) return;
+    free(g->phase); free(g->gen); free(g->winner);
+    free(g);
+}
+
+oracle_grains *oracle_grains_create(int64_t n)
+{
+    if (n < 0) return NULL;
+    oracle_grains *g = (oracle_grains *)calloc(1, sizeof(oracle_grains));
+    if (!g) return NULL;
+    size_t m = (size_t)(n > 0 ? n : 1);
+    g->n = n;
+    g->phase = (uint8_t *)malloc(m);
+    g->gen = (uint32_t *)calloc(m, sizeof(uint32_t));
+    g->winner = (int64_t *)malloc(m * sizeof(int64_t));
+    if (!g->phase || !g->gen || !g->winner) { oracle_grains_destroy(g); return NULL; }
+    for (int64_t c = 0; c < n; ++c) { g->phase[c] = PH_READY; g->winner[c] = -1; }
+    return g;
+}
+
+const uint8_t *oracle_grains_phase(const oracle_grains *g) { return g ? g->phase : NULL; }
+const uint32_t *oracle_grains_gen(const oracle_grains *g) { return g ? g->gen : NULL; }
+
+/* Reserve: READY -> IN-FLIGHT; out_gen[i] = the generation the attempt runs
+ * at.  A child that is not READY is a bad state. */
+int oracle_grains_dispatch(oracle_grains *g, const uint32_t *child, int64_t n, uint32_t *out_gen)
+{
+    if (!g || n < 0 || (n > 0 && !child)) return OR_EINVAL;
+    for (int64_t i = 0; i < n; ++i) {
+        uint32_t c = child[i];
+        if ((int64_t)c >= g->n) return OR_ERANGE;
+        if (g->phase[c] != PH_READY) return OR_ESTATE;
+        g->phase[c] = PH_IN_FLIGHT;
+        if (out_gen) out_gen[i] = g->gen[c];
+    }
+    return OR_OK;
+}
+
+/* Retry: IN-FLIGHT -> READY at the next generation. */
+int oracle_grains_retry(oracle_grains *g, const uint32_t *child, int64_t n)
+{
+    if (!g || n < 0 || (n > 0 && !child)) return OR_EINVAL;
+    for (int64_t i = 0; i < n; ++i) {
+        uint32_t c = child[i];
+        if ((int64_t)c >= g->n) return OR_ERANGE;
+        if (g->phase[c] != PH_IN_FLIGHT) return OR_ESTATE;
+        g->phase[c] = PH_READY;
+        g->gen[c] += 1;
+    }
+    return OR_OK;
+}
+
+/* Commit one call's reports in order.  The first report of an in-flight
+ * Grain at its current generation is accepted and seals it; a later report
+ * of the same call at that generation repeats the accepted one: a duplicate
+ * if its state and bytes are the same, a conflict otherwise; any other
+ * report is stale.  state_out[i] is the report's state if accepted, PENDING
+ * otherwise (so a gather ignores it).  counts[0..3] = accepted, stale,
+ * duplicate, conflict. */
+int oracle_grains_commit(oracle_grains *g, const uint32_t *rep_parent, const uint32_t *rep_ordinal,
+                         const uint8_t *rep_state, const int64_t *rep_off, const uint8_t *data,
+                         const uint32_t *rep_gen, int64_t n, const int64_t *offsets, int64_t n_parents,
+                         uint8_t *state_out, int64_t *counts)
+{
+    if (!g || n < 0 || !offsets || (n > 0 && (!rep_parent || !rep_ordinal || !rep_state || !rep_off || !rep_gen ||
+                                              !state_out)))
+        return OR_EINVAL;
+    for (int64_t i = 0; i < n; ++i) {
+        if (rep_off[i + 1] < rep_off[i]) return OR_EINVAL;
+        if (rep_state[i] > ST_GROUP_FAILED) return OR_ESTATE;
+        if (rep_state[i] == ST_PENDING) continue;
+        uint32_t p = rep_parent[i];
+        if ((int64_t)p >= n_parents) return OR_ERANGE;
+        if ((int64_t)rep_ordinal[i] >= offsets[p + 1] - offsets[p]) return OR_ERANGE;
+        if (offsets[p] + rep_ordinal[i] >= g->n) return OR_ERANGE;
+    }
+    int64_t acc = 0, stale = 0, dup = 0, conf = 0;
+    for (int64_t i = 0; i < n; ++i) {
+        state_out[i] = ST_PENDING;
+        if (rep_state[i] == ST_PENDING) continue;
+        int64_t c = offsets[rep_parent[i]] + rep_ordinal[i];
+        if (g->phase[c] == PH_IN_FLIGHT && rep_gen[i] == g->gen[c]) {
+            g->phase[c] = PH_SEALED;
+            g->winner[c] = i;
+            state_out[i] = rep_state[i];
+            ++acc;
+        } else if (g->winner[c] >= 0 && rep_gen[i] == g->gen[c]) {
+            int64_t w = g->winner[c];
+            int same = rep_state[w] == rep_state[i];
+            if (same && rep_state[i] == ST_SUCCESS) {
+                int64_t lw = rep_off[w + 1] - rep_off[w], li = rep_off[i + 1] - rep_off[i];
+                same = lw == li && (lw == 0 || data == NULL ||
+                                    memcmp(data + rep_off[w], data + rep_off[i], (size_t)lw) == 0);
+            }
+            if (same) ++dup; else ++conf;
+        } else {
+            ++stale;
+        }
+    }
+    for (int64_t i = 0; i < n; ++i)          /* winners are per call */
+        if (rep_state[i] != ST_PENDING) g->winner[offsets[rep_parent[i]] + rep_ordinal[i]] = -1;
+    if (counts) { counts[0] = acc; counts[1] = stale; counts[2] = dup; counts[3] = conf; }
     return OR_OK;
 }

@@ -16,6 +16,7 @@ import subprocess
 import numpy as np
 
 __all__ = ["build", "lib", "OracleError", "expand", "batch", "gather", "nested", "Stream", "filter", "broadcast",
+           "Grains", "WAITING", "READY", "IN_FLIGHT", "SEALED",
            "OK", "EINVAL", "ERANGE", "EDUP", "ECAP", "EOVERFLOW", "ESTATE",
            "SUCCESS", "FAILED", "SKIPPED", "PENDING", "GROUP_FAILED"]
 
@@ -57,6 +58,18 @@ def _load(path):
     L.oracle_stream_report.argtypes = [P, P, P, P, P, P, i64, P]
     L.oracle_filter.argtypes = [P, P, P, i64, P]
     L.oracle_broadcast.argtypes = [P, C.c_int32, i64, P, i64, P, P, P]
+    L.oracle_grains_create.argtypes = [i64]
+    L.oracle_grains_create.restype = P
+    L.oracle_grains_destroy.argtypes = [P]
+    L.oracle_grains_dispatch.argtypes = [P, P, i64, P]
+    L.oracle_grains_retry.argtypes = [P, P, i64]
+    L.oracle_grains_commit.argtypes = [P, P, P, P, P, P, P, i64, P, i64, P, P]
+    L.oracle_grains_phase.argtypes = [P]
+    L.oracle_grains_phase.restype = C.POINTER(C.c_uint8)
+    L.oracle_grains_gen.argtypes = [P]
+    L.oracle_grains_gen.restype = C.POINTER(C.c_uint32)
+    for f in ("oracle_grains_dispatch", "oracle_grains_retry", "oracle_grains_commit"):
+        getattr(L, f).restype = C.c_int
     L.oracle_stream_barrier.argtypes = [P]
     L.oracle_stream_barrier.restype = C.POINTER(C.c_uint8)
     L.oracle_stream_emit.argtypes = [P, P, P, P, i64, i64, P, P, P, P, P, P]
@@ -221,6 +234,63 @@ def broadcast(maps, x_state, like_state=None, L=None):
     _check(L.oracle_broadcast(C.cast(arr, C.c_void_p), len(maps), n, _p(x_state), len(x_state), _p(ls),
                               _p(anc), _p(out)), "broadcast")
     return anc[:n], out[:n]
+
+
+WAITING, READY, IN_FLIGHT, SEALED = 0, 1, 2, 3
+
+
+class Grains:
+    """Grain phases and generations of one Call's children (oracle side)."""
+
+    def __init__(self, n, L=None):
+        self.L = L or lib()
+        self.n = int(n)
+        self.h = self.L.oracle_grains_create(self.n)
+        if not self.h:
+            raise OracleError(EINVAL, "grains_create")
+
+    def dispatch(self, child):
+        child = np.ascontiguousarray(child, dtype=np.uint32)
+        gen = np.zeros(max(len(child), 1), np.uint32)
+        _check(self.L.oracle_grains_dispatch(self.h, _p(child), len(child), _p(gen)), "grains_dispatch")
+        return gen[:len(child)]
+
+    def retry(self, child):
+        child = np.ascontiguousarray(child, dtype=np.uint32)
+        _check(self.L.oracle_grains_retry(self.h, _p(child), len(child)), "grains_retry")
+
+    def commit(self, parent, ordinal, state, off, data, gen, offsets):
+        """Returns (state_out, (accepted, stale, duplicate, conflict))."""
+        parent = np.ascontiguousarray(parent, dtype=np.uint32)
+        ordinal = np.ascontiguousarray(ordinal, dtype=np.uint32)
+        state = np.ascontiguousarray(state, dtype=np.uint8)
+        off = np.ascontiguousarray(off, dtype=np.int64)
+        data = None if data is None else np.ascontiguousarray(data, dtype=np.uint8)
+        gen = np.ascontiguousarray(gen, dtype=np.uint32)
+        offsets = np.ascontiguousarray(offsets, dtype=np.int64)
+        out = np.zeros(max(len(parent), 1), np.uint8)
+        counts = np.zeros(4, np.int64)
+        _check(self.L.oracle_grains_commit(self.h, _p(parent), _p(ordinal), _p(state), _p(off), _p(data), _p(gen),
+                                           len(parent), _p(offsets), len(offsets) - 1, _p(out), _p(counts)),
+               "grains_commit")
+        return out[:len(parent)], tuple(int(x) for x in counts)
+
+    def phase(self):
+        return np.ctypeslib.as_array(self.L.oracle_grains_phase(self.h), shape=(max(self.n, 1),))[:self.n].copy()
+
+    def gen(self):
+        return np.ctypeslib.as_array(self.L.oracle_grains_gen(self.h), shape=(max(self.n, 1),))[:self.n].copy()
+
+    def close(self):
+        if self.h:
+            self.L.oracle_grains_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 class Stream:

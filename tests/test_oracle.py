@@ -744,3 +744,127 @@ def test_broadcast_ancestor_by_composed_offsets():
             assert st[d] == want
     anc, st = O.broadcast([np.zeros(0, np.uint32)], np.zeros(1, np.uint8))
     assert anc.size == 0 and st.size == 0
+
+
+# ---------------------------------------------------------------- generation fence
+def test_generation_fence_cases():
+    """Eq. (generation-fence) case by case: a report commits only while its
+    Grain is in flight at the report's generation; a repeat of the committed
+    report in the same call is a duplicate, a different one a conflict; a
+    retry moves the Grain to the next generation, after which the old
+    attempt's report is stale."""
+    offs = O.expand(np.array([3], np.int32), tags=False)
+    g = O.Grains(3)
+    assert list(g.phase()) == [O.READY] * 3
+    gen = g.dispatch([0, 1, 2])
+    assert list(gen) == [0, 0, 0] and list(g.phase()) == [O.IN_FLIGHT] * 3
+    data = np.array([5, 6, 7, 9], np.uint8)
+    # child 0: committed, then an identical repeat and a conflicting one
+    # child 1: a report at a wrong generation (stale) and a right one
+    par = np.zeros(5, np.uint32)
+    ordi = np.array([0, 0, 0, 1, 1], np.uint32)
+    st = np.array([O.SUCCESS, O.SUCCESS, O.SUCCESS, O.SUCCESS, O.FAILED], np.uint8)
+    off = np.array([0, 1, 1, 2, 3, 3], np.int64)            # bytes 5 | - | 6 | 7 | -
+    data = np.array([5, 6, 7], np.uint8)
+    out, counts = g.commit(par, ordi, st, off, data, np.array([0, 0, 0, 7, 0], np.uint32), offs)
+    # report 1 has no bytes while report 0 has one: conflict; report 2 has a different byte: conflict
+    assert list(out) == [O.SUCCESS, O.PENDING, O.PENDING, O.PENDING, O.FAILED]
+    assert counts == (2, 1, 0, 2)
+    assert list(g.phase()) == [O.SEALED, O.SEALED, O.IN_FLIGHT]
+    # an identical repeat in one call is a duplicate
+    g2 = O.Grains(1)
+    g2.dispatch([0])
+    o1 = O.expand(np.array([1], np.int32), tags=False)
+    out, counts = g2.commit(np.zeros(2, np.uint32), np.zeros(2, np.uint32), np.zeros(2, np.uint8),
+                            np.array([0, 2, 4], np.int64), np.array([1, 2, 1, 2], np.uint8), np.zeros(2, np.uint32), o1)
+    assert list(out) == [O.SUCCESS, O.PENDING] and counts == (1, 0, 1, 0)
+    # child 2 retried: the old attempt's report is stale, the new one commits
+    g.retry([2])
+    assert g.phase()[2] == O.READY and g.gen()[2] == 1
+    assert list(g.dispatch([2])) == [1]
+    out, counts = g.commit(np.zeros(2, np.uint32), np.array([2, 2], np.uint32), np.zeros(2, np.uint8),
+                           np.array([0, 1, 2], np.int64), np.array([8, 9], np.uint8), np.array([0, 1], np.uint32), offs)
+    assert list(out) == [O.PENDING, O.SUCCESS] and counts == (1, 1, 0, 0)
+    # phase errors: dispatching a sealed Grain, retrying one not in flight
+    with pytest.raises(O.OracleError) as e:
+        g.dispatch([0])
+    assert e.value.code == O.ESTATE
+    with pytest.raises(O.OracleError) as e:
+        g.retry([1])
+    assert e.value.code == O.ESTATE
+    g.close(); g2.close()
+
+
+def _fenced_run(rng, counts, outcomes, lens, payload, B, retry_p=0.3, stale_p=0.3, dup_p=0.2):
+    """A legal schedule with retries, stale and repeated reports; returns the
+    gather of everything the fence accepted."""
+    offs, cp, co = O.expand(counts)
+    N = int(offs[-1])
+    g = O.Grains(N)
+    ready = list(rng.permutation(N))
+    committed = np.zeros(N, bool)
+    old_attempts = []                    # (child, generation) of retried attempts
+    all_par, all_ord, all_st, all_gen, all_data, all_len = [], [], [], [], [], []
+    while not committed.all():
+        batch = ready[:B]
+        ready = ready[B:]
+        gens = g.dispatch(np.array(batch, np.uint32)) if batch else []
+        par, ordi, st, gn, blobs = [], [], [], [], []
+        for c, gen in zip(batch, gens):
+            if rng.random() < retry_p:               # the attempt is lost: retried later
+                old_attempts.append((c, gen))
+                continue
+            reps = 2 if rng.random() < dup_p else 1
+            for _ in range(reps):
+                par.append(cp[c]); ordi.append(co[c]); st.append(outcomes[c]); gn.append(gen)
+                blobs.append(payload[c] if outcomes[c] == O.SUCCESS else b"")
+        # stale reports of earlier lost attempts arrive late
+        for c, gen in list(old_attempts):
+            if rng.random() < stale_p:
+                par.append(cp[c]); ordi.append(co[c]); st.append(outcomes[c]); gn.append(gen)
+                blobs.append(payload[c] if outcomes[c] == O.SUCCESS else b"")
+        order = rng.permutation(len(par))
+        par = np.array(par, np.uint32)[order] if par else np.zeros(0, np.uint32)
+        ordi = np.array(ordi, np.uint32)[order] if len(order) else np.zeros(0, np.uint32)
+        st = np.array(st, np.uint8)[order] if len(order) else np.zeros(0, np.uint8)
+        gn = np.array(gn, np.uint32)[order] if len(order) else np.zeros(0, np.uint32)
+        blobs = [blobs[i] for i in order]
+        off = np.concatenate([[0], np.cumsum([len(b) for b in blobs])]).astype(np.int64)
+        data = np.frombuffer(b"".join(blobs) or b"\0", np.uint8)
+        out, cnt = g.commit(par, ordi, st, off, data, gn, offs)
+        acc = out != O.PENDING
+        committed[offs[par[acc]] + ordi[acc]] = True
+        all_par.append(par[acc]); all_ord.append(ordi[acc]); all_st.append(st[acc])
+        all_data += [blobs[i] for i in np.flatnonzero(acc)]
+        # lost attempts go back to the queue at the next generation
+        lost = [c for c in batch if not committed[c] and g.phase()[c] == O.IN_FLIGHT]
+        if lost:
+            g.retry(np.array(lost, np.uint32))
+            ready += lost
+    par = np.concatenate(all_par); ordi = np.concatenate(all_ord); st = np.concatenate(all_st)
+    off = np.concatenate([[0], np.cumsum([len(b) for b in all_data])]).astype(np.int64)
+    data = np.frombuffer(b"".join(all_data) or b"\0", np.uint8)
+    g.close()
+    return O.gather(par, ordi, st, off, data, offs)
+
+
+def test_generation_fence_schedule_invariance():
+    """Eq. (schedule-invariance) under retries: whatever the batches, lost
+    attempts, late stale reports and repeats, the fence commits each Grain
+    exactly once with its fixed outcome, so the gather equals the one-shot
+    gather of one report per child."""
+    rng = np.random.default_rng(53)
+    for trial in range(25):
+        counts = rng.integers(0, 6, int(rng.integers(1, 30))).astype(np.int32)
+        offs, cp, co = O.expand(counts)
+        N = int(offs[-1])
+        outcomes = rng.choice(np.array([0, 0, 0, 1, 2], np.uint8), N)
+        payload = [bytes(rng.integers(0, 256, int(rng.integers(0, 6)), dtype=np.uint8)) for _ in range(N)]
+        lens = np.array([len(p) if o == 0 else 0 for p, o in zip(payload, outcomes)], np.int64)
+        off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+        data = np.frombuffer(b"".join(p for p, o in zip(payload, outcomes) if o == 0) or b"\0", np.uint8)
+        want = O.gather(cp, co, outcomes, off, data, offs)
+        for B in (1, 3, 7):
+            got = _fenced_run(rng, counts, outcomes, lens, payload, B)
+            for k in ("out_off", "n_success", "n_failed", "n_skipped", "complete", "parent_state", "out_data"):
+                assert np.array_equal(got[k], want[k]), (trial, B, k)

@@ -17,6 +17,11 @@ untimed by the generator's device fill):
                 waves: per wave ro_batch, ro_stream_report, ro_stream_emit.
   docs-ops      F.filter over the ~2.7M regions of the documents workload and
                 F.broadcast of a document-level Item to every region.
+  zipf-fence    Grain phases and the generation fence over the dispatched
+                children of zipf-single: reset, dispatch at generation 0,
+                commit (with identical and conflicting repeats), retry of the
+                2% lost attempts, dispatch at generation 1, commit (with
+                stale generation-0 reports).
 
 Prints one JSON line.  Children/s counts every child entity created at every
 level (pages + regions, clips + frames).
@@ -36,7 +41,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, published
-WORKLOADS = ("zipf-single", "docs-nested", "videos-nested", "stream-waves", "docs-ops")
+WORKLOADS = ("zipf-single", "docs-nested", "videos-nested", "stream-waves", "docs-ops", "zipf-fence")
 
 
 def parse():
@@ -196,9 +201,10 @@ class Job:
     """A staged workload: step() enqueues one step; alg maps kernel kinds to
     algorithmic bytes per step."""
 
-    def __init__(self, name, step, children, alg, config, check, leaves=None):
+    def __init__(self, name, step, children, alg, config, check, leaves=None, metric=None):
         self.name, self.step, self.children, self.alg = name, step, children, alg
         self.config, self.check, self.leaves = config, check, leaves
+        self.metric = metric or "children/sec through expand+batch+gather; achieved HBM GB/s vs peak"
 
 
 def stage_zipf(ctx, parents):
@@ -349,7 +355,92 @@ def stage_ops(ctx, parents):
            "regions": N2, "pages": N1, "documents": P1}
     # filter: three state bytes in, one out; broadcast: region map, region state, ancestor and state out
     # (the page map and document states stay in cache)
-    return Job("docs-ops", step, N2, {"misc": 4 * N2 + 10 * N2}, cfg, check)
+    return Job("docs-ops", step, N2, {"filter": 4 * N2, "broadcast": 10 * N2}, cfg, check)
+
+
+def alg_fence(P, N, M, L, n0, n1, rep_bytes):
+    """Algorithmic bytes of one fence step: the grain fill (phase, generation
+    and fence key, 16 B a child); dispatch and retry, 20 B an entry (id in,
+    phase read and written, generation in or out); the first fence pass, 45 B
+    a report (key, ordinal, state, generation, the next offset, the grain's
+    phase and generation, the key's read and write) plus the offsets; the
+    deciding pass, 30 B a report (key, ordinal, state, generation, fence key,
+    grain generation, state out, phase out) plus the bytes of compared
+    repeats."""
+    return {"grains": 16 * N + 20 * (M + 2 * L),
+            "fence_first": 45 * (n0 + n1) + 2 * 8 * (P + 1),
+            "fence_decide": 30 * (n0 + n1) + 2 * 8 * (P + 1) + rep_bytes}
+
+
+def stage_fence(ctx, parents):
+    import torch
+    import workloads as W
+    from workloads import device as D
+    c = W.config2(n_parents=parents or 100_000)
+    f = W.fence_trace(c)
+    P, N = c.n_parents, c.n_children
+    M, L = len(f.dispatch0), len(f.lost)
+    r0, r1 = f.rounds
+    log(f"[bench] zipf-fence: P={P} N={N} dispatched={M} lost={L} reports={r0.n}+{r1.n} "
+        f"repeats={f.n_repeat} conflicts={f.n_conflict} stale={f.n_stale}")
+    offs = torch.empty(P + 1, dtype=torch.int64, device="cuda")
+    ctx.expand(D.to_dev(c.counts), offs)
+
+    def dev_round(r):
+        d = dict(parent=D.to_dev(r.parent.view(np.int32)), ordinal=D.to_dev(r.ordinal.view(np.int32)),
+                 state=D.to_dev(r.state), off=D.to_dev(r.off), gen=D.to_dev(r.generation.view(np.int32)),
+                 out=torch.empty(max(r.n, 1), dtype=torch.uint8, device="cuda"),
+                 cnt=torch.zeros(4, dtype=torch.int64, device="cuda"))
+        d["data"] = D.reports_data_dev(r)
+        return d
+
+    d0, d1 = dev_round(r0), dev_round(r1)
+    disp0 = D.to_dev(f.dispatch0.view(np.int32))
+    lost = D.to_dev(f.lost.view(np.int32))
+    gen0 = torch.empty(max(M, 1), dtype=torch.int32, device="cuda")
+    gen1 = torch.empty(max(L, 1), dtype=torch.int32, device="cuda")
+    g = ctx.grains(N)
+    # bytes the deciding pass compares: both copies of every same-state,
+    # same-length successful repeat
+    lens0 = np.diff(r0.off)
+    na = r0.n - f.n_repeat - f.n_conflict
+    first_len = {}
+    rep_bytes = 0
+    key0 = r0.parent.astype(np.int64) << 32 | r0.ordinal
+    pos = dict(zip(key0[:na].tolist(), range(na)))
+    for i in range(na, r0.n):
+        w = pos[int(key0[i])]
+        if r0.state[i] == r0.state[w] == W.SUCCESS and lens0[i] == lens0[w]:
+            rep_bytes += 2 * int(lens0[i])
+
+    def commit(d, n):
+        g.commit(d["parent"], d["ordinal"], d["state"], d["off"], d["data"], d["gen"], offs, d["out"], d["cnt"],
+                 n=n)
+
+    def step():
+        g.reset()
+        g.dispatch(disp0, gen0, n=M)
+        commit(d0, r0.n)
+        g.retry(lost, n=L)
+        g.dispatch(lost, gen1, n=L)
+        commit(d1, r1.n)
+
+    def check():
+        c0 = tuple(int(x) for x in d0["cnt"].cpu().numpy())
+        c1 = tuple(int(x) for x in d1["cnt"].cpu().numpy())
+        assert c0 == (na, 0, f.n_repeat, f.n_conflict), c0
+        assert c1 == (L, f.n_stale, 0, 0), c1
+        assert int(gen1[:L].max().item()) == 1 and int(gen0[:M].max().item()) == 0
+
+    cfg = {"workload": f"generation fence over the dispatched children of the single-level Zipf(1.2) fan-out "
+                       f"({P} parents, {N} children, {M} dispatched): 2% of attempts lost and retried at "
+                       f"generation 1, 1% identical and 0.2% conflicting repeats, stale reports for half of "
+                       f"the lost attempts, seeds 1 and 6",
+           "parents": P, "children": N, "dispatched": M, "lost": L, "reports": [r0.n, r1.n],
+           "repeats": f.n_repeat, "conflicts": f.n_conflict, "stale": f.n_stale}
+    return Job("zipf-fence", step, M, alg_fence(P, N, M, L, r0.n, r1.n, rep_bytes), cfg, check,
+               metric="children/sec through dispatch + generation-fenced commit over two attempts; "
+                      "achieved HBM GB/s vs peak")
 
 
 # ---------------------------------------------------------------- main
@@ -390,6 +481,8 @@ def run(args):
         job = stage_stream(ctx, args.parents)
     elif args.workload == "docs-ops":
         job = stage_ops(ctx, args.parents)
+    elif args.workload == "zipf-fence":
+        job = stage_fence(ctx, args.parents)
     else:
         job = stage_nested(ctx, args.workload, args.parents)
     torch.cuda.synchronize()
@@ -456,7 +549,7 @@ def run(args):
     value = job.children / (ms_step * 1e-3)
 
     result = {
-        "metric": "children/sec through expand+batch+gather; achieved HBM GB/s vs peak",
+        "metric": job.metric,
         "value": round(value, 1),
         "unit": "children/s",
         "n_gpus": 1,
@@ -566,6 +659,41 @@ def cpu_baseline(workload):
         n_child = len(n.queue1) + len(n.queue2)
         sample = (f"{len(n.counts1)} top parents, {len(n.queue1)} + {len(n.queue2)} children, "
                   f"{int(r.off[-1])} leaf bytes; expand, batch, expand, batch, gather, gather")
+    elif workload == "docs-ops":
+        n = W.config3()
+        rng = np.random.default_rng(7)
+        N2, P1 = len(n.queue2), len(n.counts1)
+        stv = np.array([0, 0, 0, 1, 2, 3], np.uint8)
+        xs, ms = rng.choice(stv, N2), rng.choice(stv, N2)
+        mv = (rng.random(N2) < 0.5).astype(np.uint8)
+        doc_x = rng.choice(stv, P1)
+        t = time.perf_counter()
+        _, p1, _ = O.expand(n.counts1, L=L)
+        _, p2, _ = O.expand(n.counts2, L=L)
+        O.filter(xs, mv, ms, L=L)
+        O.broadcast([p2, p1], doc_x, n.states, L=L)
+        dt = time.perf_counter() - t
+        n_child = N2
+        sample = f"the full workload ({N2} regions); two expands for the maps, filter, broadcast"
+    elif workload == "zipf-fence":
+        c = W.config2()
+        f = W.fence_trace(c)
+        datas = [r.repeated_data() for r in f.rounds]
+        t = time.perf_counter()
+        offs = O.expand(c.counts, tags=False, L=L)
+        g = O.Grains(c.n_children, L=L)
+        g.dispatch(f.dispatch0)
+        r0, r1 = f.rounds
+        g.commit(r0.parent, r0.ordinal, r0.state, r0.off, datas[0], r0.generation, offs)
+        g.retry(f.lost)
+        g.dispatch(f.lost)
+        g.commit(r1.parent, r1.ordinal, r1.state, r1.off, datas[1], r1.generation, offs)
+        dt = time.perf_counter() - t
+        g.close()
+        n_child = len(f.dispatch0)
+        sample = (f"the full workload ({c.n_children} children, {n_child} dispatched, the same fence trace; "
+                  f"the oracle holds the bytes of repeated reports only, the rest it never reads); "
+                  f"expand, dispatch, commit, retry, dispatch, commit")
     else:
         s = W.config5(n_parents=100_000, n_children=2_000_000)
         arena = np.concatenate([rep.data() for rep in s.wave_reports] + [np.zeros(1, np.uint8)])

@@ -107,7 +107,8 @@ enum {
     RO_K_EXPAND_SCAN = 0, RO_K_EXPAND_TAGS, RO_K_BATCH_SAMPLES, RO_K_BATCH,
     RO_K_GATHER_SCATTER, RO_K_GATHER_SCAN, RO_K_GATHER_FINALIZE, RO_K_GATHER_COPY,
     RO_K_GATHER_RESET, RO_K_STREAM_REPORT, RO_K_STREAM_SELECT, RO_K_STREAM_SCAN,
-    RO_K_STREAM_COPY, RO_K_STREAM_FINISH, RO_K_MISC, RO_K_COUNT
+    RO_K_STREAM_COPY, RO_K_STREAM_FINISH, RO_K_MISC, RO_K_FILTER, RO_K_BROADCAST,
+    RO_K_GRAINS, RO_K_FENCE_FIRST, RO_K_FENCE_DECIDE, RO_K_COUNT
 };
 int ro_ctx_trace(ro_ctx *ctx, int enable);
 int ro_ctx_trace_read(ro_ctx *ctx, int64_t *launches, double *total_ms, int32_t n);
@@ -207,6 +208,45 @@ int ro_filter(ro_ctx *ctx, const uint8_t *x_state, const uint8_t *mask_state, co
  * ro_filter.  `maps` is a host array of device pointers. */
 int ro_broadcast(ro_ctx *ctx, const uint32_t *const *maps, int32_t levels, int64_t n, const uint8_t *x_state,
                  int64_t n_ancestors, const uint8_t *like_state, uint32_t *out_ancestor, uint8_t *out_state);
+
+/* Grain phases and the generation fence (Sec. 4, Eq. grain-phase and Eq.
+ * generation-fence).  One Grain per child of an expansion: READY at
+ * generation 0 when created or reset; reservation moves it to IN-FLIGHT, a
+ * retry back to READY at the next generation, an accepted report seals it.
+ * The state lives in device memory allocated here (16 bytes per child). */
+enum { RO_WAITING = 0, RO_READY = 1, RO_IN_FLIGHT = 2, RO_SEALED = 3 };
+typedef struct ro_grains ro_grains;
+int ro_grains_create(ro_ctx *ctx, int64_t n_children, ro_grains **out);
+int ro_grains_reset(ro_ctx *ctx, ro_grains *g);
+int ro_grains_destroy(ro_grains *g);
+
+/* Write every child's phase (RO_READY, RO_IN_FLIGHT or RO_SEALED) and
+ * generation into the device arrays phase[n_children] and
+ * generation[n_children] (uint32; either may be NULL), on the context's
+ * stream.  For inspection: the library keeps its own layout. */
+int ro_grains_read(ro_ctx *ctx, ro_grains *g, uint32_t *phase, uint32_t *generation);
+
+/* Reserve child[0..n): READY -> IN-FLIGHT; out_generation[i] (may be NULL)
+ * is the generation the attempt runs at, which its report must carry.  A
+ * child that is not READY (or named twice) is RO_ESTATE. */
+int ro_grains_dispatch(ro_ctx *ctx, ro_grains *g, const uint32_t *child, int64_t n, uint32_t *out_generation);
+
+/* Retry child[0..n): IN-FLIGHT -> READY at the next generation (a lost or
+ * failed physical attempt; Grain identity is unchanged).  A child not in
+ * flight is RO_ESTATE. */
+int ro_grains_retry(ro_ctx *ctx, ro_grains *g, const uint32_t *child, int64_t n);
+
+/* Commit one call's reports through the fence, in report order: the first
+ * report of an in-flight Grain at its current generation (generation[i]) is
+ * accepted and seals the Grain; a later report of this call at that
+ * generation repeats it and is a duplicate (same state and bytes, dropped as
+ * idempotent) or a conflict (rejected); every other report is stale.
+ * state_out[i] is the report's state if accepted and RO_PENDING otherwise,
+ * so a following ro_gather / ro_stream_report with these states commits
+ * exactly the accepted reports.  counts_dev[0..3] (device, may be NULL) =
+ * accepted, stale, duplicate, conflict.  Validation as in ro_gather. */
+int ro_grains_commit(ro_ctx *ctx, ro_grains *g, const ro_reports *reports, const uint32_t *generation,
+                     const int64_t *offsets, int64_t n_parents, uint8_t *state_out, int64_t *counts_dev);
 
 /* Streaming gather over one expansion (offsets[P+1] on the device, kept by
  * reference until ro_stream_destroy).  The stream's own state lives in

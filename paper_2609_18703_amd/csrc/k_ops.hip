@@ -108,7 +108,7 @@ hipError_t launch_filter(const Launch &L, const uint8_t *xs, const uint8_t *ms, 
                        reinterpret_cast<uintptr_t>(mv) | reinterpret_cast<uintptr_t>(out)) & 15u) == 0;
     int64_t grid = (n + kBlock * 16 - 1) / (kBlock * 16);
     grid = grid < 1 ? 1 : (grid > (int64_t)L.num_cus * 8 ? (int64_t)L.num_cus * 8 : grid);
-    RO_LAUNCH(L, RO_K_MISC, k_filter, dim3((unsigned)grid), dim3(kBlock), 0, L.stream, xs, ms, mv, n, out,
+    RO_LAUNCH(L, RO_K_FILTER, k_filter, dim3((unsigned)grid), dim3(kBlock), 0, L.stream, xs, ms, mv, n, out,
               vec ? 1 : 0, L.ctl);
     return hipGetLastError();
 }
@@ -120,7 +120,7 @@ hipError_t launch_broadcast(const Launch &L, const uint32_t *const *maps, int32_
     for (int32_t l = 0; l < levels; ++l) m.m[l] = maps[l];
     int64_t grid = (n + kBlock - 1) / kBlock;
     grid = grid < 1 ? 1 : (grid > (int64_t)L.num_cus * 8 ? (int64_t)L.num_cus * 8 : grid);
-    RO_LAUNCH(L, RO_K_MISC, k_broadcast, dim3((unsigned)grid), dim3(kBlock), 0, L.stream, m, levels, n, xs, n_anc,
+    RO_LAUNCH(L, RO_K_BROADCAST, k_broadcast, dim3((unsigned)grid), dim3(kBlock), 0, L.stream, m, levels, n, xs, n_anc,
               ls, anc, out, L.ctl);
     return hipGetLastError();
 }

@@ -72,6 +72,15 @@ struct ro_ctx {
     Tracer *tracer;
 };
 
+struct ro_grains {
+    ro_ctx *ctx;
+    int64_t n;
+    Grain *g;                 // [max(n, 1)] phase, generation and fence key per child
+    uint32_t epoch;           // of the current commit call
+    uint32_t *tag;            // [tag_cap] per report: epoch of the call in which it met another
+    int64_t tag_cap;
+};
+
 struct ro_stream {
     ro_ctx *ctx;
     StreamState st;
@@ -374,6 +383,98 @@ int ro_broadcast(ro_ctx *c, const uint32_t *const *maps, int32_t levels, int64_t
     if (n == 0) return RO_OK;
     return hip_fail(launch_broadcast(launch_of(c), maps, levels, n, x_state, n_ancestors, like_state, out_ancestor,
                                      out_state));
+}
+
+int ro_grains_create(ro_ctx *c, int64_t n_children, ro_grains **out)
+{
+    if (out) *out = nullptr;
+    if (!c || !out || n_children < 0 || n_children >= ((int64_t)1 << 32)) return RO_EINVAL;
+    const int64_t n = n_children > 0 ? n_children : 1;
+    ro_grains *g = (ro_grains *)calloc(1, sizeof(ro_grains));
+    if (!g) return RO_EINVAL;
+    if (hipMalloc((void **)&g->g, (size_t)n * sizeof(Grain)) != hipSuccess) {
+        free(g);
+        return RO_EHIP;
+    }
+    g->ctx = c;
+    g->n = n_children;
+    g->epoch = 0;
+    if (launch_grains_fill(launch_of(c), g->g, n) != hipSuccess) {
+        (void)hipFree(g->g);
+        free(g);
+        return RO_EHIP;
+    }
+    *out = g;
+    return RO_OK;
+}
+
+int ro_grains_reset(ro_ctx *c, ro_grains *g)
+{
+    if (!c || !g || g->ctx != c) return RO_EINVAL;
+    g->epoch = 0;
+    return hip_fail(launch_grains_fill(launch_of(c), g->g, g->n > 0 ? g->n : 1));
+}
+
+int ro_grains_destroy(ro_grains *g)
+{
+    if (!g) return RO_EINVAL;
+    if (g->ctx) (void)hipStreamSynchronize(g->ctx->stream);
+    (void)hipFree(g->g);
+    if (g->tag) (void)hipFree(g->tag);
+    free(g);
+    return RO_OK;
+}
+
+int ro_grains_read(ro_ctx *c, ro_grains *g, uint32_t *phase, uint32_t *generation)
+{
+    if (!c || !g || g->ctx != c) return RO_EINVAL;
+    if (g->n == 0 || (!phase && !generation)) return RO_OK;
+    return hip_fail(launch_grains_read(launch_of(c), g->g, g->n, phase, generation));
+}
+
+int ro_grains_dispatch(ro_ctx *c, ro_grains *g, const uint32_t *child, int64_t n, uint32_t *out_generation)
+{
+    if (!c || !g || g->ctx != c || n < 0 || (n > 0 && !child)) return RO_EINVAL;
+    if (n == 0) return RO_OK;
+    return hip_fail(launch_grains_dispatch(launch_of(c), child, n, g->n, g->g, out_generation));
+}
+
+int ro_grains_retry(ro_ctx *c, ro_grains *g, const uint32_t *child, int64_t n)
+{
+    if (!c || !g || g->ctx != c || n < 0 || (n > 0 && !child)) return RO_EINVAL;
+    if (n == 0) return RO_OK;
+    return hip_fail(launch_grains_retry(launch_of(c), child, n, g->n, g->g));
+}
+
+int ro_grains_commit(ro_ctx *c, ro_grains *g, const ro_reports *r, const uint32_t *generation,
+                     const int64_t *offsets, int64_t n_parents, uint8_t *state_out, int64_t *counts_dev)
+{
+    if (!c || !g || g->ctx != c || !r || !offsets || n_parents < 0 || r->n < 0) return RO_EINVAL;
+    if (r->n >= ((int64_t)1 << 32)) return RO_EINVAL;                // report index is 32-bit
+    if (r->n > 0 && (!r->parent || !r->ordinal || !r->state || !r->off || !generation || !state_out))
+        return RO_EINVAL;
+    const Launch L = launch_of(c);
+    const int64_t need = r->n > 0 ? r->n : 1;
+    if (need > g->tag_cap) {                  // grows with the largest call; starts untagged
+        const int64_t cap = need > 2 * g->tag_cap ? need : 2 * g->tag_cap;
+        uint32_t *t = nullptr;
+        if (hipMalloc((void **)&t, (size_t)cap * sizeof(uint32_t)) != hipSuccess) return RO_EHIP;
+        if (g->tag) {
+            (void)hipStreamSynchronize(c->stream);
+            (void)hipFree(g->tag);
+        }
+        g->tag = t;
+        g->tag_cap = cap;
+        if (launch_grains_zero_tags(L, g->tag, cap) != hipSuccess) return RO_EHIP;
+    }
+    if (g->epoch == 0xffffffffu) {            // keys and tags of every earlier call must read as old
+        if (launch_grains_rekey(L, g->g, g->n > 0 ? g->n : 1) != hipSuccess) return RO_EHIP;
+        if (launch_grains_zero_tags(L, g->tag, g->tag_cap) != hipSuccess) return RO_EHIP;
+        g->epoch = 0;
+    }
+    g->epoch += 1;
+    return hip_fail(launch_grains_commit(L, r->parent, r->ordinal, r->state, r->off, r->data, generation, r->n,
+                                         offsets, n_parents, g->n, g->g, g->epoch, g->tag, state_out, counts_dev));
 }
 
 int ro_stream_create(ro_ctx *c, const int64_t *offsets, int64_t n_parents, int64_t n_children,

@@ -114,6 +114,28 @@ struct GatherWs {
 // one), which also tags its group-failure keys
 hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w, uint32_t epoch);
 
+// grain phases and the generation fence.  One 16-byte record per Grain:
+// word = phase (READY or IN-FLIGHT) | generation << 32, changed by one 64-bit
+// compare-and-swap; key = the accepted report, epoch << 32 | ~index, of the
+// commit call that sealed the Grain (0 while unsealed).  A report touches one
+// record: one random access.
+struct alignas(16) Grain {
+    uint64_t word;
+    uint64_t key;
+};
+static_assert(sizeof(Grain) == 16, "grain record");
+hipError_t launch_grains_fill(const Launch &L, Grain *g, int64_t n);
+hipError_t launch_grains_rekey(const Launch &L, Grain *g, int64_t n);
+hipError_t launch_grains_read(const Launch &L, const Grain *g, int64_t n, uint32_t *phase, uint32_t *gen);
+hipError_t launch_grains_dispatch(const Launch &L, const uint32_t *child, int64_t n, int64_t N, Grain *g,
+                                  uint32_t *out_gen);
+hipError_t launch_grains_retry(const Launch &L, const uint32_t *child, int64_t n, int64_t N, Grain *g);
+hipError_t launch_grains_commit(const Launch &L, const uint32_t *rp, const uint32_t *ro, const uint8_t *rs,
+                                const int64_t *roff, const uint8_t *data, const uint32_t *rgen, int64_t n,
+                                const int64_t *offsets, int64_t P, int64_t N, Grain *g, uint32_t epoch, uint32_t *tag,
+                                uint8_t *state_out, int64_t *counts);
+hipError_t launch_grains_zero_tags(const Launch &L, uint32_t *tag, int64_t n);
+
 // filter / broadcast
 constexpr int kMaxBroadcastLevels = 8;
 hipError_t launch_filter(const Launch &L, const uint8_t *xs, const uint8_t *ms, const uint8_t *mv, int64_t n,

@@ -9,8 +9,9 @@ from __future__ import annotations
 
 import ctypes as C
 import os
+import weakref
 
-__all__ = ["RoError", "load", "Context", "Stream", "KERNELS", "OK", "EINVAL", "ERANGE", "EDUP", "ECAP",
+__all__ = ["RoError", "load", "Context", "Stream", "Grains", "KERNELS", "OK", "EINVAL", "ERANGE", "EDUP", "ECAP",
            "EOVERFLOW", "ESTATE", "EHIP", "SUCCESS", "FAILED", "SKIPPED", "PENDING", "GROUP_FAILED",
            "LIB_PATH"]
 
@@ -20,7 +21,8 @@ SUCCESS, FAILED, SKIPPED, PENDING, GROUP_FAILED = 0, 1, 2, 3, 4
 # kernel kinds reported by Context.trace_read, in the C enum's order
 KERNELS = ["expand_scan", "expand_tags", "batch_samples", "batch", "gather_scatter", "gather_scan",
            "gather_finalize", "gather_copy", "gather_reset", "stream_report", "stream_select",
-           "stream_scan", "stream_copy", "stream_finish", "misc"]
+           "stream_scan", "stream_copy", "stream_finish", "misc", "filter", "broadcast", "grains",
+           "fence_first", "fence_decide"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libro.so")
 
@@ -70,6 +72,13 @@ def load(path=None):
     L.ro_stream_emit.argtypes = [P, P, P, P, P, i64, i64, P, P, P, P, P, P]
     L.ro_stream_reset.argtypes = [P, P]
     L.ro_filter.argtypes = [P, P, P, P, i64, P]
+    L.ro_grains_create.argtypes = [P, i64, pp]
+    L.ro_grains_reset.argtypes = [P, P]
+    L.ro_grains_destroy.argtypes = [P]
+    L.ro_grains_read.argtypes = [P, P, P, P]
+    L.ro_grains_dispatch.argtypes = [P, P, P, i64, P]
+    L.ro_grains_retry.argtypes = [P, P, P, i64]
+    L.ro_grains_commit.argtypes = [P, P, C.POINTER(ReportsT), P, P, i64, P, P]
     L.ro_broadcast.argtypes = [P, P, i32, i64, P, i64, P, P, P]
     L.ro_stream_destroy.argtypes = [P]
     L.ro_ctx_trace.argtypes = [P, C.c_int]
@@ -77,7 +86,8 @@ def load(path=None):
     for name in ("ro_ctx_trace", "ro_ctx_trace_read", "ro_ctx_create", "ro_ctx_set_stream", "ro_ctx_reserve", "ro_ctx_status",
                  "ro_ctx_destroy", "ro_expand", "ro_batch", "ro_gather", "ro_stream_create",
                  "ro_stream_report", "ro_stream_emit", "ro_stream_reset", "ro_stream_destroy", "ro_filter",
-                 "ro_broadcast"):
+                 "ro_broadcast", "ro_grains_create", "ro_grains_reset", "ro_grains_destroy", "ro_grains_read",
+                 "ro_grains_dispatch", "ro_grains_retry", "ro_grains_commit"):
         getattr(L, name).restype = C.c_int
     if path == LIB_PATH:
         _lib = L
@@ -116,6 +126,7 @@ class Context:
         h = C.c_void_p()
         _check(self.L.ro_ctx_create(C.byref(h), C.c_void_p(stream.cuda_stream)), "ro_ctx_create")
         self.h = h
+        self._owned = weakref.WeakSet()     # grain sets and streams: destroyed before the context
 
     def reserve(self, max_children, max_parents, max_queue=0):
         _check(self.L.ro_ctx_reserve(self.h, int(max_children), int(max_parents), int(max_queue)),
@@ -183,12 +194,65 @@ class Context:
                                    x_state.numel(), _ptr(like_state), _ptr(out_ancestor), _ptr(out_state)),
                "ro_broadcast")
 
+    def grains(self, n_children):
+        g = Grains(self, n_children)
+        self._owned.add(g)
+        return g
+
     def stream(self, offsets, n_children, barrier=None):
-        return Stream(self, offsets, n_children, barrier)
+        st = Stream(self, offsets, n_children, barrier)
+        self._owned.add(st)
+        return st
 
     def close(self):
         if getattr(self, "h", None):
+            for o in list(getattr(self, "_owned", ())):
+                o.close()
             self.L.ro_ctx_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Grains:
+    """Grain phases and generations of one Call's children (device side)."""
+
+    def __init__(self, ctx, n_children):
+        self.ctx = ctx
+        self.n = int(n_children)
+        h = C.c_void_p()
+        _check(ctx.L.ro_grains_create(ctx.h, self.n, C.byref(h)), "ro_grains_create")
+        self.h = h
+
+    def reset(self):
+        _check(self.ctx.L.ro_grains_reset(self.ctx.h, self.h), "ro_grains_reset")
+
+    def read(self, phase=None, generation=None):
+        """Write every child's phase and generation into int32 device tensors
+        of n_children entries (either may be None)."""
+        _check(self.ctx.L.ro_grains_read(self.ctx.h, self.h, _ptr(phase), _ptr(generation)), "ro_grains_read")
+
+    def dispatch(self, child, out_generation=None, n=None):
+        n = child.numel() if n is None else n
+        _check(self.ctx.L.ro_grains_dispatch(self.ctx.h, self.h, _ptr(child), int(n), _ptr(out_generation)),
+               "ro_grains_dispatch")
+
+    def retry(self, child, n=None):
+        n = child.numel() if n is None else n
+        _check(self.ctx.L.ro_grains_retry(self.ctx.h, self.h, _ptr(child), int(n)), "ro_grains_retry")
+
+    def commit(self, parent, ordinal, state, off, data, generation, offsets, state_out, counts=None, n=None):
+        rep = _reports(parent, ordinal, state, off, data, n)
+        _check(self.ctx.L.ro_grains_commit(self.ctx.h, self.h, C.byref(rep), _ptr(generation), _ptr(offsets),
+                                           offsets.numel() - 1, _ptr(state_out), _ptr(counts)), "ro_grains_commit")
+
+    def close(self):
+        if getattr(self, "h", None):
+            self.ctx.L.ro_grains_destroy(self.h)
             self.h = None
 
     def __del__(self):

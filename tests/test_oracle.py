@@ -868,3 +868,46 @@ def test_generation_fence_schedule_invariance():
             got = _fenced_run(rng, counts, outcomes, lens, payload, B)
             for k in ("out_off", "n_success", "n_failed", "n_skipped", "complete", "parent_state", "out_data"):
                 assert np.array_equal(got[k], want[k]), (trial, B, k)
+
+
+def test_generation_fence_trace_outcome():
+    """Sec. 4, Eq. generation-fence with the publication rules, on the fence
+    trace: whatever is lost, repeated or late, every dispatched child ends
+    sealed with exactly one accepted report carrying its own outcome; the
+    first call accepts every first copy, calls the identical repeats
+    duplicates and the altered ones conflicts; the second accepts every
+    retried child and rejects the generation-0 reports as stale."""
+    c = W.config2(n_parents=400)
+    f = W.fence_trace(c, p_repeat=0.05, p_conflict=0.03, p_lost=0.1)
+    offs = O.expand(c.counts, tags=False)
+    g = O.Grains(c.n_children)
+    assert np.array_equal(g.dispatch(f.dispatch0), np.zeros(len(f.dispatch0), np.uint32))
+    r0, r1 = f.rounds
+    out0, cnt0 = g.commit(r0.parent, r0.ordinal, r0.state, r0.off, r0.data(), r0.generation, offs)
+    g.retry(f.lost)
+    assert np.array_equal(g.dispatch(f.lost), np.ones(len(f.lost), np.uint32))
+    out1, cnt1 = g.commit(r1.parent, r1.ordinal, r1.state, r1.off, r1.data(), r1.generation, offs)
+    na = len(f.dispatch0) - len(f.lost)
+    assert f.n_conflict > 0 and f.n_repeat > 0 and f.n_stale > 0
+    assert tuple(cnt0) == (na, 0, f.n_repeat, f.n_conflict)
+    assert tuple(cnt1) == (len(f.lost), f.n_stale, 0, 0)
+    ph = g.phase()
+    assert (ph[f.dispatch0] == O.SEALED).all()
+    assert (ph[c.queue[c.keep == 0]] == O.READY).all()
+    acc_child, acc_state = [], []
+    for r, out in ((r0, out0), (r1, out1)):
+        a = out != O.PENDING
+        acc_child.append(offs[r.parent[a]] + r.ordinal[a])
+        acc_state.append(out[a])
+        assert np.array_equal(out[a], r.state[a])
+    ch = np.concatenate(acc_child)
+    assert len(np.unique(ch)) == len(ch) == len(f.dispatch0)
+    assert np.array_equal(np.concatenate(acc_state), c.states[ch])
+    g.close()
+    # the fence reads the bytes of repeated reports only: the same outcome
+    # from a buffer that holds nothing else
+    g = O.Grains(c.n_children)
+    g.dispatch(f.dispatch0)
+    out0b, cnt0b = g.commit(r0.parent, r0.ordinal, r0.state, r0.off, r0.repeated_data(), r0.generation, offs)
+    assert np.array_equal(out0b, out0) and tuple(cnt0b) == tuple(cnt0)
+    g.close()

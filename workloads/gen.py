@@ -32,6 +32,7 @@ __all__ = [
     "Reports", "SingleLevel", "Nested", "Streaming",
     "single_level", "config1", "config2", "config3", "config4", "config5",
     "nested", "streaming", "CONFIG_NAMES", "FailureTrace", "failure_trace",
+    "FenceRound", "FenceTrace", "fence_trace",
 ]
 
 
@@ -473,3 +474,113 @@ CONFIG_NAMES = {
     4: "2,000 videos -> clips -> frames",
     5: "10M children / 500,000 parents over 50 waves",
 }
+
+
+# --------------------------------------------------------------------------
+# Generation-fence trace: retries, stale and repeated reports
+# --------------------------------------------------------------------------
+
+@dataclass
+class FenceRound:
+    """One commit call: report keys, state, generation and the record layout
+    (``off`` into a shared arena, ``seed`` the content key of each record)."""
+    parent: np.ndarray      # uint32[n]
+    ordinal: np.ndarray     # uint32[n]
+    state: np.ndarray       # uint8[n]
+    generation: np.ndarray  # uint32[n]
+    off: np.ndarray         # int64[n+1]
+    seed: np.ndarray        # uint64[n]
+    base: int = 0
+
+    @property
+    def n(self):
+        return len(self.state)
+
+    def data(self):
+        return record_bytes(self.seed, np.diff(self.off))
+
+    def repeated_data(self):
+        """Host bytes of the records of every report whose child is reported
+        more than once in the call, at their offsets; the rest of the buffer
+        stays zero and its pages are never touched (so never allocated)."""
+        key = self.parent.astype(np.int64) << 32 | self.ordinal.astype(np.int64)
+        _, inv, cnt = np.unique(key, return_inverse=True, return_counts=True)
+        idx = np.flatnonzero(cnt[inv] > 1)
+        host = np.zeros(max(int(self.off[-1]), 1), np.uint8)
+        lens = np.diff(self.off)[idx]
+        if len(idx):
+            starts = self.off[idx] - np.concatenate([[0], np.cumsum(lens)[:-1]])
+            host[np.repeat(starts, lens) + np.arange(int(lens.sum()))] = record_bytes(self.seed[idx], lens)
+        return host
+
+
+@dataclass
+class FenceTrace:
+    """A Call's dispatched children through two attempts.  Attempt 0
+    dispatches them in queue order at generation 0; the reports of a fraction
+    of them never arrive, and those children are retried and dispatched again
+    at generation 1.  Some attempt-0 reports arrive twice (an identical
+    repeat, or a conflicting one: another state, or the same length with other
+    bytes), always after the first copy; in the second call, late reports of
+    lost attempts arrive at generation 0 (stale) among the new ones."""
+    counts: np.ndarray      # int32[P]
+    dispatch0: np.ndarray   # uint32[M] children dispatched at generation 0
+    lost: np.ndarray        # uint32[L] children retried and dispatched at generation 1
+    rounds: list            # [FenceRound, FenceRound]
+    n_repeat: int
+    n_conflict: int
+    n_stale: int
+
+
+def fence_trace(c, seed=6, p_lost=0.02, p_repeat=0.01, p_conflict=0.002, p_stale=0.5):
+    """Fence trace over a single-level workload ``c`` (its dispatched
+    children, canonical states and lengths).  Record bytes follow the content
+    definition: a report's bytes are splitmix64 of its content seed, which is
+    the child's (parent, ordinal) key, with its top bit flipped for a
+    conflicting repeat of the same length."""
+    rng = np.random.default_rng(seed)
+    parent, ordinal = _child_keys(c.counts)
+    disp = np.ascontiguousarray(c.queue[c.keep == 1]).astype(np.int64)
+    M = len(disp)
+    lost_mask = rng.random(M) < p_lost
+    arrived = disp[~lost_mask]
+    u = rng.random(len(arrived))
+    rep = arrived[u < p_repeat]
+    conf = arrived[(u >= p_repeat) & (u < p_repeat + p_conflict)]
+    lost = disp[lost_mask]
+
+    def build(children, state, gen, seed_xor):
+        ln = np.where(state == SUCCESS, c.lengths[children], 0).astype(np.int64)
+        off = np.zeros(len(children) + 1, np.int64)
+        np.cumsum(ln, out=off[1:])
+        sd = content_seed(parent[children], ordinal[children]) ^ seed_xor
+        return FenceRound(parent=parent[children].astype(np.uint32), ordinal=ordinal[children].astype(np.uint32),
+                          state=state.astype(np.uint8), generation=gen.astype(np.uint32), off=off, seed=sd)
+
+    # call 0: first copies in dispatch order, then the repeats in random order
+    rep_all = np.concatenate([rep, conf])
+    perm = rng.permutation(len(rep_all))
+    rep_all = rep_all[perm]
+    is_conf = np.concatenate([np.zeros(len(rep), bool), np.ones(len(conf), bool)])[perm]
+    st_rep = c.states[rep_all].copy()
+    xor_rep = np.zeros(len(rep_all), np.uint64)
+    # a conflict of a successful record keeps its length and changes its bytes;
+    # any other conflict changes the state
+    same_len = is_conf & (st_rep == SUCCESS) & (rng.random(len(rep_all)) < 0.5)
+    xor_rep[same_len] = np.uint64(1 << 63)
+    flip = is_conf & ~same_len
+    st_rep[flip] = np.where(st_rep[flip] == SUCCESS, FAILED, SUCCESS)
+    ch0 = np.concatenate([arrived, rep_all])
+    st0 = np.concatenate([c.states[arrived], st_rep])
+    xor0 = np.concatenate([np.zeros(len(arrived), np.uint64), xor_rep])
+    r0 = build(ch0, st0, np.zeros(len(ch0), np.uint32), xor0)
+    # call 1: every retried child at generation 1, and stale generation-0
+    # reports of some of them, shuffled together
+    stale = lost[rng.random(len(lost)) < p_stale]
+    ch1 = np.concatenate([lost, stale])
+    g1 = np.concatenate([np.ones(len(lost), np.uint32), np.zeros(len(stale), np.uint32)])
+    perm = rng.permutation(len(ch1))
+    ch1, g1 = ch1[perm], g1[perm]
+    r1 = build(ch1, c.states[ch1], g1, np.zeros(len(ch1), np.uint64))
+    return FenceTrace(counts=c.counts, dispatch0=disp.astype(np.uint32), lost=lost.astype(np.uint32),
+                      rounds=[r0, r1], n_repeat=len(rep), n_conflict=len(conf), n_stale=len(stale))

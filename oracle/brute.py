@@ -2,7 +2,7 @@
 
 A second, independent formulation of the same definitions as ``oracle.c``
 (Sec. 4 of the paper: Eq. flat-facts, the Reduce rule, FIFO Ready Queues with
-elastic reservation).  Where the C oracle scans offsets and sorts reports,
+elastic and parent-bound reservation).  Where the C oracle scans offsets and sorts reports,
 this one enumerates the (parent, ordinal) pairs and looks every child up by a
 linear search over all reports, so the two share no algorithm.
 """
@@ -44,6 +44,25 @@ def batch(queue, keep, counts, B):
     while ready:
         batches.append(ready[:B])
         ready = ready[B:]
+    return batches, keys
+
+
+def batch_parent(queue, keep, counts, B):
+    """Literal parent-bound reservations on a list: the head's parent takes
+    its first (at most B) entries found scanning the queue from the head, and
+    the queue is rebuilt without them.  Returns the list of batches of child
+    ids."""
+    keys = children(counts)
+    ready = [c for i, c in enumerate(queue) if keep is None or keep[i]]
+    for c in ready:
+        if c >= len(keys):
+            raise BruteError(-2)
+    batches = []
+    while ready:
+        p = keys[ready[0]][0]
+        take = [c for c in ready if keys[c][0] == p][:B]
+        batches.append(take)
+        ready = [c for c in ready if c not in take]
     return batches, keys
 
 

@@ -169,6 +169,90 @@ done:
 }
 
 /* ------------------------------------------------------------------------ */
+/* FIFO Ready Queue + parent-bound reservation.                              */
+/* ------------------------------------------------------------------------ */
+/* Sec. 4 "Scheduling Ready Grains": a parent-bound reservation takes up to B
+ * siblings of the first ready parent, and every entry it leaves keeps its
+ * place in the queue.  The queue is filled as in oracle_batch (kept entries
+ * in order, barred parents' entries suppressed).  Each reservation looks at
+ * the head, the earliest entry still queued; its parent is the first ready
+ * parent; the reservation takes that parent's queued entries in queue order,
+ * at most B of them, and marks them gone.  Each parent keeps the list of its
+ * queued entries in queue order, so finding the siblings does not rescan the
+ * queue.  Outputs as in oracle_batch, except that batch j starts where batch
+ * j - 1 ends (sizes vary; batch_size_out gives them). */
+int oracle_batch_parent(const uint32_t *queue, const uint8_t *keep, int64_t q_len,
+                        const int64_t *offsets, int64_t n_parents, int32_t batch_size,
+                        uint32_t *out_child, uint32_t *out_parent, uint32_t *out_ordinal,
+                        int64_t out_cap, int64_t *n_out, int64_t *n_batches,
+                        int64_t *batch_size_out, const uint8_t *barrier)
+{
+    if (q_len < 0 || n_parents < 0 || batch_size <= 0 || offsets == NULL ||
+        (q_len > 0 && queue == NULL))
+        return OR_EINVAL;
+    int64_t n = offsets[n_parents];
+    size_t m = (size_t)(q_len > 0 ? q_len : 1);
+    size_t np = (size_t)(n_parents > 0 ? n_parents : 1);
+    uint32_t *par = (uint32_t *)malloc(sizeof(uint32_t) * (size_t)(n > 0 ? n : 1));
+    uint32_t *ord = (uint32_t *)malloc(sizeof(uint32_t) * (size_t)(n > 0 ? n : 1));
+    uint32_t *qc = (uint32_t *)malloc(sizeof(uint32_t) * m);      /* queued children, in order */
+    int64_t *next = (int64_t *)malloc(sizeof(int64_t) * m);       /* next queued sibling */
+    uint8_t *gone = (uint8_t *)calloc(m, 1);
+    int64_t *first = (int64_t *)malloc(sizeof(int64_t) * np);     /* parent's earliest queued entry */
+    int64_t *last = (int64_t *)malloc(sizeof(int64_t) * np);
+    int rc = OR_OK;
+    if (!par || !ord || !qc || !next || !gone || !first || !last) { rc = OR_EINVAL; goto done; }
+    for (int64_t p = 0; p < n_parents; ++p) {
+        first[p] = last[p] = -1;
+        for (int64_t c = offsets[p]; c < offsets[p + 1]; ++c) {
+            par[c] = (uint32_t)p;
+            ord[c] = (uint32_t)(c - offsets[p]);
+        }
+    }
+    int64_t len = 0;
+    for (int64_t i = 0; i < q_len; ++i) {
+        if (keep != NULL && keep[i] == 0)
+            continue;
+        if ((int64_t)queue[i] >= n) { rc = OR_ERANGE; goto done; }
+        uint32_t p = par[queue[i]];
+        if (barrier != NULL && barrier[p])
+            continue;                         /* suppressed: never dispatched */
+        qc[len] = queue[i];
+        next[len] = -1;
+        if (last[p] < 0) first[p] = len; else next[last[p]] = len;
+        last[p] = len;
+        ++len;
+    }
+    if (len > out_cap) { rc = OR_ECAP; goto done; }
+    int64_t slot = 0, nb = 0, head = 0;
+    for (;;) {
+        while (head < len && gone[head]) ++head;
+        if (head == len) break;
+        /* one parent-bound reservation: the head's parent, at most B siblings */
+        uint32_t p = par[qc[head]];
+        int64_t taken = 0;
+        while (taken < batch_size && first[p] >= 0) {
+            int64_t e = first[p];
+            uint32_t c = qc[e];
+            gone[e] = 1;
+            first[p] = next[e];
+            if (out_child)   out_child[slot] = c;
+            if (out_parent)  out_parent[slot] = p;
+            if (out_ordinal) out_ordinal[slot] = ord[c];
+            ++slot;
+            ++taken;
+        }
+        if (batch_size_out) batch_size_out[nb] = taken;
+        ++nb;
+    }
+    if (n_out) *n_out = slot;
+    if (n_batches) *n_batches = nb;
+done:
+    free(par); free(ord); free(qc); free(next); free(gone); free(first); free(last);
+    return rc;
+}
+
+/* ------------------------------------------------------------------------ */
 /* F.reduce: ordered gather of child reports into parent slots.              */
 /* ------------------------------------------------------------------------ */
 typedef struct {

@@ -51,6 +51,7 @@ def _load(path):
     i64 = C.c_int64
     L.oracle_expand.argtypes = [P, i64, P, P, P, i64]
     L.oracle_batch.argtypes = [P, P, i64, P, i64, C.c_int32, P, P, P, i64, P, P, P, P]
+    L.oracle_batch_parent.argtypes = [P, P, i64, P, i64, C.c_int32, P, P, P, i64, P, P, P, P]
     L.oracle_gather.argtypes = [P, P, P, P, P, i64, P, i64, P, P, i64, P, P, P, P, P, P, P, P]
     L.oracle_stream_create.argtypes = [P, i64]
     L.oracle_stream_create.restype = P
@@ -73,7 +74,7 @@ def _load(path):
     L.oracle_stream_barrier.argtypes = [P]
     L.oracle_stream_barrier.restype = C.POINTER(C.c_uint8)
     L.oracle_stream_emit.argtypes = [P, P, P, P, i64, i64, P, P, P, P, P, P]
-    for f in ("oracle_expand", "oracle_batch", "oracle_gather", "oracle_stream_report",
+    for f in ("oracle_expand", "oracle_batch", "oracle_batch_parent", "oracle_gather", "oracle_stream_report",
               "oracle_stream_emit", "oracle_filter", "oracle_broadcast"):
         getattr(L, f).restype = C.c_int
     return L
@@ -117,9 +118,11 @@ def expand(counts, tags=True, L=None):
     return offsets, parent[:n], ordinal[:n]
 
 
-def batch(queue, keep, offsets, batch_size, barrier=None, L=None):
+def batch(queue, keep, offsets, batch_size, barrier=None, L=None, parent_bound=False):
     """FIFO batches: returns (child, parent, ordinal, batch_sizes).  With a
-    barrier (uint8 per parent), children of barred parents are dropped."""
+    barrier (uint8 per parent), children of barred parents are dropped.
+    Elastic reservations by default; parent_bound=True takes up to B siblings
+    of the first ready parent per reservation."""
     L = L or lib()
     queue = np.ascontiguousarray(queue, dtype=np.uint32)
     keep = None if keep is None else np.ascontiguousarray(keep, dtype=np.uint8)
@@ -133,9 +136,9 @@ def batch(queue, keep, offsets, batch_size, barrier=None, L=None):
     n_out = np.zeros(1, np.int64)
     n_b = np.zeros(1, np.int64)
     barrier = None if barrier is None else np.ascontiguousarray(barrier, dtype=np.uint8)
-    _check(L.oracle_batch(_p(queue), _p(keep), Q, _p(offsets), len(offsets) - 1, int(batch_size),
-                          _p(child), _p(parent), _p(ordinal), Q, _p(n_out), _p(n_b), _p(sizes),
-                          _p(barrier)),
+    fn = L.oracle_batch_parent if parent_bound else L.oracle_batch
+    _check(fn(_p(queue), _p(keep), Q, _p(offsets), len(offsets) - 1, int(batch_size),
+              _p(child), _p(parent), _p(ordinal), Q, _p(n_out), _p(n_b), _p(sizes), _p(barrier)),
            "batch")
     m, nb = int(n_out[0]), int(n_b[0])
     return child[:m], parent[:m], ordinal[:m], sizes[:nb]

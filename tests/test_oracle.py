@@ -130,6 +130,83 @@ def test_batch_fifo_order_and_chunking():
     assert np.all(offs[parent] + ordinal == child)
 
 
+def test_batch_parent_exhaustive_vs_brute():
+    """Sec. 4 "Scheduling Ready Grains": parent-bound reservations, the C
+    oracle against the literal list simulation on every queue order, keep
+    mask and batch size of tiny expansions."""
+    for counts in [(2, 1), (0, 3, 1), (1, 0, 0, 2), (4,), (2, 2)]:
+        n = sum(counts)
+        offsets = O.expand(np.array(counts, np.int32), tags=False)
+        keys = brute.children(counts)
+        for perm in itertools.permutations(range(n)):
+            for mask in itertools.product((0, 1), repeat=n):
+                for B in range(1, n + 2):
+                    q = np.array(perm, np.uint32)
+                    keep = np.array(mask, np.uint8)
+                    child, parent, ordinal, sizes = O.batch(q, keep, offsets, B, parent_bound=True)
+                    bb, _ = brute.batch_parent(list(perm), list(mask), counts, B)
+                    assert list(sizes) == [len(b) for b in bb]
+                    flat = [c for b in bb for c in b]
+                    assert list(child) == flat
+                    assert [(int(p), int(o)) for p, o in zip(parent, ordinal)] == [keys[c] for c in flat]
+
+
+def test_batch_parent_teaser_queue():
+    """The teaser figure's ready queue A0 B0 C0 A1 B1 C1 B2 C2 under
+    parent-bound reservations of B = 2 (worked by hand from the definition):
+    A0 A1 | B0 B1 | C0 C1 | B2 | C2."""
+    counts = np.array([2, 3, 3], np.int32)            # A, B, C
+    offs = O.expand(counts, tags=False)
+    A, Bp, Cp = 0, 2, 5
+    q = np.array([A, Bp, Cp, A + 1, Bp + 1, Cp + 1, Bp + 2, Cp + 2], np.uint32)
+    child, parent, ordinal, sizes = O.batch(q, None, offs, 2, parent_bound=True)
+    assert list(sizes) == [2, 2, 2, 1, 1]
+    assert list(zip(parent.tolist(), ordinal.tolist())) == [(0, 0), (0, 1), (1, 0), (1, 1), (2, 0), (2, 1),
+                                                            (1, 2), (2, 2)]
+
+
+def test_batch_parent_closed_form():
+    """An equivalent formulation: rank every kept entry within its parent in
+    queue order; the entries of ranks jB .. jB + B - 1 of a parent form one
+    batch, and batches follow the queue position of their first entry (the
+    head is always the earliest entry left, and batches leave whole)."""
+    for B, seed in [(1, 0), (3, 1), (256, 2), (10_000, 3)]:
+        c = W.config2(n_parents=300, seed=seed)
+        offs = O.expand(c.counts, tags=False)
+        child, parent, ordinal, sizes = O.batch(c.queue, c.keep, offs, B, parent_bound=True)
+        kept = c.queue[c.keep == 1].astype(np.int64)
+        par = np.searchsorted(offs, kept, side="right") - 1
+        rank = np.zeros(len(kept), np.int64)
+        seen = {}
+        for i, p in enumerate(par.tolist()):
+            rank[i] = seen.get(p, 0)
+            seen[p] = rank[i] + 1
+        # queue position of the first entry of each entry's batch
+        pos_by_parent = {}
+        for i, p in enumerate(par.tolist()):
+            pos_by_parent.setdefault(p, []).append(i)
+        first = np.array([pos_by_parent[p][(r // B) * B] for p, r in zip(par.tolist(), rank.tolist())])
+        order = np.lexsort((rank, first))                      # by batch, then rank inside it
+        bounds = np.flatnonzero(np.diff(first[order])) + 1
+        want = np.split(kept[order], bounds)
+        assert list(sizes) == [len(w) for w in want]
+        assert np.array_equal(child, np.concatenate(want))
+        assert np.all(offs[parent] + ordinal == child)
+
+
+def test_batch_parent_barrier_is_a_filter():
+    c = W.config2(n_parents=800, seed=4)
+    offs = O.expand(c.counts, tags=False)
+    rng = np.random.default_rng(4)
+    bar = (rng.random(800) < 0.3).astype(np.uint8)
+    par = np.searchsorted(offs, c.queue.astype(np.int64), side="right") - 1
+    keep2 = c.keep & (bar[par] == 0)
+    a = O.batch(c.queue, c.keep, offs, 7, barrier=bar, parent_bound=True)
+    b = O.batch(c.queue, keep2.astype(np.uint8), offs, 7, parent_bound=True)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
 def test_batch_errors():
     offs = O.expand(np.array([2, 1], np.int32), tags=False)
     with pytest.raises(O.OracleError) as e:

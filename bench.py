@@ -17,6 +17,9 @@ untimed by the generator's device fill):
                 waves: per wave ro_batch, ro_stream_report, ro_stream_emit.
   docs-ops      F.filter over the ~2.7M regions of the documents workload and
                 F.broadcast of a document-level Item to every region.
+  zipf-pbatch   parent-bound reservation of zipf-single's ready queue (41M
+                entries, B = 256): batches of up to B siblings of the first
+                ready parent.
   zipf-fence    Grain phases and the generation fence over the dispatched
                 children of zipf-single: reset, dispatch at generation 0,
                 commit (with identical and conflicting repeats), retry of the
@@ -41,7 +44,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, published
-WORKLOADS = ("zipf-single", "docs-nested", "videos-nested", "stream-waves", "docs-ops", "zipf-fence")
+WORKLOADS = ("zipf-single", "docs-nested", "videos-nested", "stream-waves", "docs-ops", "zipf-fence",
+             "zipf-pbatch")
 
 
 def parse():
@@ -443,6 +447,60 @@ def stage_fence(ctx, parents):
                       "achieved HBM GB/s vs peak")
 
 
+def stage_pbatch(ctx, parents):
+    import torch
+    import workloads as W
+    from workloads import device as D
+    c = W.config2(n_parents=parents or 100_000)
+    P, N, M = c.n_parents, c.n_children, c.n_dispatched
+    Q = len(c.queue)
+    log(f"[bench] zipf-pbatch: P={P} N={N} queue={Q} ready={M} B={c.batch_size}")
+    ctx.reserve(N, P, Q)
+    offs = torch.empty(P + 1, dtype=torch.int64, device="cuda")
+    ctx.expand(D.to_dev(c.counts), offs)
+    q = D.to_dev(c.queue.view(np.int32))
+    keep = D.to_dev(c.keep)
+    oc = torch.empty(M, dtype=torch.int32, device="cuda")
+    op = torch.empty(M, dtype=torch.int32, device="cuda")
+    oo = torch.empty(M, dtype=torch.int32, device="cuda")
+    boff = torch.empty(M + 1, dtype=torch.int64, device="cuda")
+    sc = torch.zeros(2, dtype=torch.int64, device="cuda")
+    # batches: one per started group of B siblings of a parent
+    offs_h = np.concatenate([[0], np.cumsum(c.counts.astype(np.int64))])
+    par = np.searchsorted(offs_h, c.queue[c.keep == 1].astype(np.int64), side="right") - 1
+    n_b = int((-(-np.bincount(par, minlength=P) // c.batch_size)).sum())
+
+    def step():
+        ctx.batch_parent(q, keep, offs, c.batch_size, boff, oc, op, oo, sc[0:1], sc[1:2])
+
+    def check():
+        assert int(sc[0].item()) == M and int(sc[1].item()) == n_b
+
+    cfg = {"workload": f"parent-bound reservation of the single-level Zipf(1.2) fan-out's ready queue: {P} "
+                       f"parents, {N} children in random ready order, {M} ready (sealed ones masked), "
+                       f"B={c.batch_size}, seed 1",
+           "parents": P, "queue": Q, "ready": M, "batches": n_b, "batch_size": c.batch_size}
+    bits = max(int(P - 1).bit_length(), 0)
+    passes = max(-(-bits // 9), 1)
+    tiles = -(-Q // 16384)                 # histogram columns: spans of 8 sort tiles
+    hist = 512 * tiles if passes * 9 == bits or bits > 9 else (1 << bits) * tiles
+    alg = {
+        # compaction: queue id and ready flag in, child and parent out
+        "batch": 5 * Q + 8 * M, "batch_samples": 4 * (N // 64),
+        # radix passes: the histogram reads the keys; the first scatter reads
+        # keys and compacted children and writes keys and (child, position)
+        # values, later ones read and write keys and values
+        "pbatch_sort": passes * 4 * M + 20 * M + (passes - 1) * 24 * M,
+        "expand_scan": passes * 12 * hist,
+        # bounds (keys in, group sizes cleared), group firsts (keys), group
+        # scan (sizes in, batch numbers and offsets out), placement (keys,
+        # values in; child, parent, ordinal out)
+        "pbatch": 8 * M + 4 * M + 4 * M + 12 * n_b + 24 * M,
+    }
+    return Job("zipf-pbatch", step, M, alg, cfg, check,
+               metric="children/sec through parent-bound reservation; achieved HBM GB/s vs peak")
+
+
 # ---------------------------------------------------------------- main
 
 def main():
@@ -483,6 +541,8 @@ def run(args):
         job = stage_ops(ctx, args.parents)
     elif args.workload == "zipf-fence":
         job = stage_fence(ctx, args.parents)
+    elif args.workload == "zipf-pbatch":
+        job = stage_pbatch(ctx, args.parents)
     else:
         job = stage_nested(ctx, args.workload, args.parents)
     torch.cuda.synchronize()
@@ -675,6 +735,15 @@ def cpu_baseline(workload):
         dt = time.perf_counter() - t
         n_child = N2
         sample = f"the full workload ({N2} regions); two expands for the maps, filter, broadcast"
+    elif workload == "zipf-pbatch":
+        c = W.config2()
+        t = time.perf_counter()
+        offs = O.expand(c.counts, tags=False, L=L)
+        _, _, _, sizes = O.batch(c.queue, c.keep, offs, c.batch_size, L=L, parent_bound=True)
+        dt = time.perf_counter() - t
+        n_child = c.n_dispatched
+        sample = (f"the full workload ({len(c.queue)} queue entries, {n_child} ready, {len(sizes)} batches); "
+                  f"expand and parent-bound reservations")
     elif workload == "zipf-fence":
         c = W.config2()
         f = W.fence_trace(c)

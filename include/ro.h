@@ -108,7 +108,7 @@ enum {
     RO_K_GATHER_SCATTER, RO_K_GATHER_SCAN, RO_K_GATHER_FINALIZE, RO_K_GATHER_COPY,
     RO_K_GATHER_RESET, RO_K_STREAM_REPORT, RO_K_STREAM_SELECT, RO_K_STREAM_SCAN,
     RO_K_STREAM_COPY, RO_K_STREAM_FINISH, RO_K_MISC, RO_K_FILTER, RO_K_BROADCAST,
-    RO_K_GRAINS, RO_K_FENCE_FIRST, RO_K_FENCE_DECIDE, RO_K_COUNT
+    RO_K_GRAINS, RO_K_FENCE_FIRST, RO_K_FENCE_DECIDE, RO_K_PBATCH_SORT, RO_K_PBATCH, RO_K_COUNT
 };
 int ro_ctx_trace(ro_ctx *ctx, int enable);
 int ro_ctx_trace_read(ro_ctx *ctx, int64_t *launches, double *total_ms, int32_t n);
@@ -137,6 +137,21 @@ int ro_batch(ro_ctx *ctx, const uint32_t *queue, const uint8_t *keep, int64_t q_
              const int64_t *offsets, int64_t n_parents, int32_t batch_size,
              uint32_t *out_child, uint32_t *out_parent, uint32_t *out_ordinal, int64_t out_cap,
              int64_t *n_out_dev, int64_t *n_batches_dev, const uint8_t *barrier);
+
+/* FIFO Ready Queue + parent-bound reservation (Sec. 4 "Scheduling Ready
+ * Grains"): each reservation takes up to B siblings of the first ready
+ * parent, the parent of the earliest entry still queued, and every other
+ * entry keeps its place.  Ready entries, ids, tags, barrier and errors as in
+ * ro_batch; reservations run until the queue is empty.  Reservation j is
+ * slots [batch_off[j], batch_off[j+1]) (int64, device; batch_off[n_batches]
+ * = M), so it needs n_batches + 1 <= batch_cap (RO_ECAP; n_batches <= M).
+ * M and n_batches go to *n_out_dev and *n_batches_dev (either may be
+ * NULL).  Workspace: about 36 bytes per queue entry and 8 per parent, held
+ * by the context and grown on demand. */
+int ro_batch_parent(ro_ctx *ctx, const uint32_t *queue, const uint8_t *keep, int64_t q_len,
+                    const int64_t *offsets, int64_t n_parents, int32_t batch_size, uint32_t *out_child,
+                    uint32_t *out_parent, uint32_t *out_ordinal, int64_t out_cap, int64_t *batch_off,
+                    int64_t batch_cap, int64_t *n_out_dev, int64_t *n_batches_dev, const uint8_t *barrier);
 
 /* One terminal report per child, in any order.  Report i is the child
  * (parent[i], ordinal[i]) with state[i]; its value is the byte range

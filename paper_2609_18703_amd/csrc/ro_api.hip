@@ -69,6 +69,9 @@ struct ro_ctx {
     uint64_t *gkey;           // [cnt_cap] first group failure per parent (gather)
     int64_t cnt_cap;
     int64_t gathers;          // host shadow of the device canonical epoch
+    PbWs pb;                  // parent-bound reservation workspace
+    int64_t pb_cap, pb_pcap;  // its queue entries and parents
+    void *pb_block;
     Tracer *tracer;
 };
 
@@ -170,6 +173,56 @@ int ensure_cnt(ro_ctx *c, int64_t parents)
     return RO_OK;
 }
 
+// Parent-bound reservation workspace for q queue entries and p parents (one
+// allocation, 256-byte aligned arrays).
+int ensure_pb(ro_ctx *c, int64_t q, int64_t p)
+{
+    if (q <= c->pb_cap && p <= c->pb_pcap && c->pb_block) return RO_OK;
+    q = q > c->pb_cap ? q : c->pb_cap;
+    p = p > c->pb_pcap ? p : c->pb_pcap;
+    const int64_t qn = q > 0 ? q : 1, pn = p > 0 ? p : 1;
+    const int64_t tiles = (qn + kPbTile * kPbSpan - 1) / (kPbTile * kPbSpan);   // histogram columns
+    const size_t sizes[] = {
+        (size_t)qn * 4, (size_t)qn * 4, (size_t)qn * 4, (size_t)qn * 8, (size_t)qn * 8,   // kc, k0, k1, v0, v1
+        (size_t)qn * 4, (size_t)qn * 4,                                                    // fsize, bidx
+        (size_t)pn * 4, (size_t)pn * 4,                                                    // pstart, pend
+        (size_t)(kPbMaxBuckets * tiles) * 4, (size_t)(kPbMaxBuckets * tiles + 1) * 8,      // hist, hoff
+        (size_t)2 * 8,                                                                     // m
+    };
+    constexpr int kArrays = (int)(sizeof(sizes) / sizeof(sizes[0]));
+    size_t offs[kArrays], total = 0;
+    for (int i = 0; i < kArrays; ++i) {
+        offs[i] = total;
+        total += (sizes[i] + 255) & ~(size_t)255;
+    }
+    if (hipStreamSynchronize(c->stream) != hipSuccess) return RO_EHIP;
+    (void)hipFree(c->pb_block);
+    c->pb_block = nullptr;
+    c->pb_cap = c->pb_pcap = 0;
+    char *b = nullptr;
+    if (hipMalloc((void **)&b, total) != hipSuccess) return RO_EHIP;
+    c->pb_block = b;
+    c->pb.kc = (uint32_t *)(b + offs[0]);
+    c->pb.k[0] = (uint32_t *)(b + offs[1]);
+    c->pb.k[1] = (uint32_t *)(b + offs[2]);
+    c->pb.v[0] = (uint64_t *)(b + offs[3]);
+    c->pb.v[1] = (uint64_t *)(b + offs[4]);
+    c->pb.fsize = (uint32_t *)(b + offs[5]);
+    c->pb.bidx = (uint32_t *)(b + offs[6]);
+    c->pb.pstart = (uint32_t *)(b + offs[7]);
+    c->pb.pend = (uint32_t *)(b + offs[8]);
+    c->pb.hist = (int32_t *)(b + offs[9]);
+    c->pb.hoff = (int64_t *)(b + offs[10]);
+    c->pb.m = (int64_t *)(b + offs[11]);
+    c->pb_cap = q;
+    c->pb_pcap = p;
+    // descriptors: the compaction, the histogram scan and the two-chain group scan
+    int64_t need = tiles_for(q);
+    need = need > tiles_for(kPbMaxBuckets * tiles) ? need : tiles_for(kPbMaxBuckets * tiles);
+    need = need > 2 * tiles_for(q) ? need : 2 * tiles_for(q);
+    return ensure_desc(c, need);
+}
+
 int before_gather(ro_ctx *c)
 {
     if (c->gathers + 1 > (int64_t)kMaxCanonEpoch) {
@@ -257,6 +310,7 @@ int ro_ctx_destroy(ro_ctx *c)
     (void)hipFree(c->cmap);
     (void)hipFree(c->cnt);
     (void)hipFree(c->gkey);
+    (void)hipFree(c->pb_block);
     if (c->tracer) {
         for (hipEvent_t e : c->tracer->pool) (void)hipEventDestroy(e);
         delete c->tracer;
@@ -312,6 +366,24 @@ int ro_batch(ro_ctx *c, const uint32_t *queue, const uint8_t *keep, int64_t q_le
     return hip_fail(launch_batch(launch_of(c), queue, keep, q_len, offsets, n_parents, batch_size,
                                  out_child, out_parent, out_ordinal, out_cap, n_out_dev, n_batches_dev,
                                  c->cmap, c->cmap_cap, barrier));
+}
+
+int ro_batch_parent(ro_ctx *c, const uint32_t *queue, const uint8_t *keep, int64_t q_len,
+                    const int64_t *offsets, int64_t n_parents, int32_t batch_size, uint32_t *out_child,
+                    uint32_t *out_parent, uint32_t *out_ordinal, int64_t out_cap, int64_t *batch_off,
+                    int64_t batch_cap, int64_t *n_out_dev, int64_t *n_batches_dev, const uint8_t *barrier)
+{
+    if (!c || !offsets || q_len < 0 || n_parents < 0 || batch_size <= 0 || out_cap < 0 || !batch_off ||
+        batch_cap < 1 || (q_len > 0 && !queue))
+        return RO_EINVAL;
+    if (q_len >= ((int64_t)1 << 32) || n_parents >= ((int64_t)1 << 32)) return RO_EINVAL;
+    int rc = ensure_pb(c, q_len, n_parents);
+    if (rc) return rc;
+    rc = ensure_desc(c, tiles_for(q_len));
+    if (rc) return rc;
+    return hip_fail(launch_batch_parent(launch_of(c), queue, keep, q_len, offsets, n_parents, batch_size,
+                                        out_child, out_parent, out_ordinal, out_cap, batch_off, batch_cap,
+                                        n_out_dev, n_batches_dev, c->cmap, c->cmap_cap, barrier, c->pb));
 }
 
 int ro_gather(ro_ctx *c, const ro_reports *r, const int64_t *offsets, int64_t n_parents,

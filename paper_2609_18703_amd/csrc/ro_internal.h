@@ -84,6 +84,27 @@ hipError_t launch_batch(const Launch &L, const uint32_t *queue, const uint8_t *k
                         int64_t out_cap, int64_t *n_out, int64_t *n_batches, uint32_t *cmap,
                         int64_t cmap_cap, const uint8_t *barrier);
 
+// parent-bound reservation workspace ([cap] queue entries, [pcap] parents)
+struct PbWs {
+    uint32_t *kc;            // ready children in queue order
+    uint32_t *k[2];          // sort keys (parents), double-buffered
+    uint64_t *v[2];          // sort values (child << 32 | queue position), double-buffered
+    uint32_t *fsize;         // per queue position: group size if a group's first entry, else 0
+    uint32_t *bidx;          // per group-first position: batch number
+    uint32_t *pstart, *pend; // per parent: sorted index range
+    int32_t *hist;           // digit histograms, [buckets * tiles]
+    int64_t *hoff;           // their exclusive scan
+    int64_t *m;              // [2] ready count, scratch
+};
+hipError_t launch_batch_parent(const Launch &L, const uint32_t *queue, const uint8_t *keep, int64_t Q,
+                               const int64_t *offsets, int64_t P, int32_t B, uint32_t *out_child,
+                               uint32_t *out_parent, uint32_t *out_ordinal, int64_t out_cap, int64_t *batch_off,
+                               int64_t batch_cap, int64_t *n_out, int64_t *n_batches, uint32_t *cmap,
+                               int64_t cmap_cap, const uint8_t *barrier, const PbWs &w);
+constexpr int64_t kPbTile = 2048;        // sort tile
+constexpr int64_t kPbSpan = 8;           // sort tiles per histogram column
+constexpr int64_t kPbMaxBuckets = 512;
+
 struct GatherArgs {
     const uint32_t *rp, *ro;
     const uint8_t *rs;

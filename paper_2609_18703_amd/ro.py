@@ -22,7 +22,7 @@ SUCCESS, FAILED, SKIPPED, PENDING, GROUP_FAILED = 0, 1, 2, 3, 4
 KERNELS = ["expand_scan", "expand_tags", "batch_samples", "batch", "gather_scatter", "gather_scan",
            "gather_finalize", "gather_copy", "gather_reset", "stream_report", "stream_select",
            "stream_scan", "stream_copy", "stream_finish", "misc", "filter", "broadcast", "grains",
-           "fence_first", "fence_decide"]
+           "fence_first", "fence_decide", "pbatch_sort", "pbatch"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libro.so")
 
@@ -66,6 +66,7 @@ def load(path=None):
     L.ro_ctx_destroy.argtypes = [P]
     L.ro_expand.argtypes = [P, P, i64, P, P, P, i64]
     L.ro_batch.argtypes = [P, P, P, i64, P, i64, i32, P, P, P, i64, P, P, P]
+    L.ro_batch_parent.argtypes = [P, P, P, i64, P, i64, i32, P, P, P, i64, P, i64, P, P, P]
     L.ro_gather.argtypes = [P, C.POINTER(ReportsT), P, i64, C.POINTER(GatherOutT)]
     L.ro_stream_create.argtypes = [P, P, i64, i64, P, pp]
     L.ro_stream_report.argtypes = [P, P, C.POINTER(ReportsT), P]
@@ -84,7 +85,7 @@ def load(path=None):
     L.ro_ctx_trace.argtypes = [P, C.c_int]
     L.ro_ctx_trace_read.argtypes = [P, P, P, i32]
     for name in ("ro_ctx_trace", "ro_ctx_trace_read", "ro_ctx_create", "ro_ctx_set_stream", "ro_ctx_reserve", "ro_ctx_status",
-                 "ro_ctx_destroy", "ro_expand", "ro_batch", "ro_gather", "ro_stream_create",
+                 "ro_ctx_destroy", "ro_expand", "ro_batch", "ro_batch_parent", "ro_gather", "ro_stream_create",
                  "ro_stream_report", "ro_stream_emit", "ro_stream_reset", "ro_stream_destroy", "ro_filter",
                  "ro_broadcast", "ro_grains_create", "ro_grains_reset", "ro_grains_destroy", "ro_grains_read",
                  "ro_grains_dispatch", "ro_grains_retry", "ro_grains_commit"):
@@ -168,6 +169,19 @@ class Context:
                                offsets.numel() - 1, int(batch_size), _ptr(out_child), _ptr(out_parent),
                                _ptr(out_ordinal), int(out_cap), _ptr(n_out), _ptr(n_batches), _ptr(barrier)),
                "ro_batch")
+
+    def batch_parent(self, queue, keep, offsets, batch_size, batch_off, out_child=None, out_parent=None,
+                     out_ordinal=None, n_out=None, n_batches=None, q_len=None, out_cap=None, barrier=None):
+        """Parent-bound reservations; batch j is slots [batch_off[j], batch_off[j+1])."""
+        q_len = queue.numel() if q_len is None else q_len
+        if out_cap is None:
+            outs = [t.numel() for t in (out_child, out_parent, out_ordinal) if t is not None]
+            out_cap = min(outs) if outs else q_len
+        _check(self.L.ro_batch_parent(self.h, _ptr(queue), _ptr(keep), q_len, _ptr(offsets),
+                                      offsets.numel() - 1, int(batch_size), _ptr(out_child), _ptr(out_parent),
+                                      _ptr(out_ordinal), int(out_cap), _ptr(batch_off), batch_off.numel(),
+                                      _ptr(n_out), _ptr(n_batches), _ptr(barrier)),
+               "ro_batch_parent")
 
     def gather(self, parent, ordinal, state, off, data, offsets, out_off, out_data=None,
                n_success=None, n_failed=None, n_skipped=None, complete=None, parent_state=None,

@@ -607,6 +607,7 @@ def run(args):
     dom_bytes = job.alg.get(dom, 0) / dom_launches
     achieved = dom_bytes / (dom_avg_ms * 1e-3) / 1e9
     value = job.children / (ms_step * 1e-3)
+    traffic = traffic_from_profile() if (job.name, dom) == TRAFFIC_WORKLOAD else None
 
     result = {
         "metric": job.metric,
@@ -628,10 +629,13 @@ def run(args):
         "roofline": {
             "bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
             "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": traffic_from_profile() if (job.name, dom) == TRAFFIC_WORKLOAD else None,
+            "traffic": traffic,
             "alg_bytes_per_launch": int(dom_bytes), "avg_launch_ms": round(dom_avg_ms, 4),
             "launches_per_step": dom_launches,
         },
+        # the measured HBM bytes of the dominant kernel (rocprofv3 counters) over its live duration
+        "traffic_GBps": round(traffic / (dom_avg_ms * 1e-3) / 1e9, 1) if traffic else None,
+        "traffic_frac": round(traffic / (dom_avg_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4) if traffic else None,
         "step_alg_GBps": round(total_alg / (ms_step * 1e-3) / 1e9, 1),
         "step_frac_of_peak": round(total_alg / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
         "kernels": per_kernel,

@@ -20,7 +20,9 @@
  *     are emitted in ordinal order, zero survivors give a present empty list.
  *   - Sec. 4 "Scheduling Ready Grains": one FIFO Ready Queue per Call holds
  *     ready Grains in enqueue order; elastic reservation removes at most B
- *     entries from its head and may mix parents.
+ *     entries from its head and may mix parents; parent-bound reservation
+ *     takes up to B siblings of the first ready parent and leaves the rest
+ *     of the queue in order.
  *   - Sec. 4 input propagation and Table "primitives": F.filter keeps or
  *     drops an Item in its own Domain, F.broadcast makes an ancestor's Item
  *     available in a descendant Domain, both under the precedence failed /

@@ -149,6 +149,30 @@ __global__ __launch_bounds__(kBlock) void k_batch(
     ticket_done(ctl, epoch, desc, desc_cap, &s_last);
 }
 
+// First index i in [0, n) with a[i] > x (n if none), for K keys at once
+// (n >= 1, a nondecreasing).  The halving is branch-free and its trip count
+// depends on n only, so the K searches step together and each step's K loads
+// are in flight at the same time.
+template <int K>
+__device__ __forceinline__ void upper_bound_k(const int64_t *a, int64_t n, const int64_t (&x)[K], int64_t (&r)[K])
+{
+    int64_t base[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) base[k] = 0;
+    int64_t len = n;
+    while (len > 1) {
+        const int64_t half = len >> 1;
+        int64_t v[K];
+#pragma unroll
+        for (int k = 0; k < K; ++k) v[k] = a[base[k] + half];
+#pragma unroll
+        for (int k = 0; k < K; ++k) base[k] = v[k] <= x[k] ? base[k] + half : base[k];
+        len -= half;
+    }
+#pragma unroll
+    for (int k = 0; k < K; ++k) r[k] = base[k] + (a[base[k]] <= x[k] ? 1 : 0);
+}
+
 // Every queue entry is ready (no mask): the FIFO compaction is the identity,
 // slot i holds queue[i], so no scan is needed and each entry is independent.
 // A block takes 1024 consecutive entries, lane-contiguous, so every load and
@@ -180,6 +204,20 @@ __global__ __launch_bounds__(kBlock) void k_batch_all(
             const int64_t i = i0 + k * kBlock + threadIdx.x;
             q[k] = i < Q ? queue[i] : 0u;
         }
+        // without the coarse map, the entries' parents come from one
+        // lockstep search of the offsets (ids out of range search for N - 1
+        // and are reported below)
+        int64_t par[kAllPer];
+        if (want_tags && nmap == 0) {
+            int64_t key[kAllPer];
+#pragma unroll
+            for (int k = 0; k < kAllPer; ++k) key[k] = (int64_t)q[k] < N ? (int64_t)q[k] : N - 1;
+            if (N > 0) {
+                upper_bound_k<kAllPer>(offsets, P + 1, key, par);
+#pragma unroll
+                for (int k = 0; k < kAllPer; ++k) par[k] -= 1;
+            }
+        }
 #pragma unroll
         for (int k = 0; k < kAllPer; ++k) {
             const int64_t i = i0 + k * kBlock + threadIdx.x;
@@ -192,7 +230,7 @@ __global__ __launch_bounds__(kBlock) void k_batch_all(
             if (i >= lim) continue;
             if (out_child) out_child[i] = q[k];
             if (want_tags) {
-                const int64_t p = parent_of(cmap, nmap, offsets, P, c);
+                const int64_t p = nmap == 0 ? par[k] : parent_of(cmap, nmap, offsets, P, c);
                 if (out_parent) out_parent[i] = (uint32_t)p;
                 if (out_ordinal) out_ordinal[i] = (uint32_t)(c - offsets[p]);
             }

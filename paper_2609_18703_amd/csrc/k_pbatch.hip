@@ -232,7 +232,7 @@ __global__ __launch_bounds__(kBlock) void k_pb_scan(const uint32_t *__restrict__
 {
     const uint32_t epoch = scan_epoch(ctl);
     __shared__ int64_t s_wave[kBlock / 64];
-    __shared__ uint64_t s_b;
+    __shared__ uint64_t s_b2[2];
     __shared__ int64_t s_t;
     __shared__ int32_t s_last;
     const int64_t M = *m_dev;
@@ -260,8 +260,8 @@ __global__ __launch_bounds__(kBlock) void k_pb_scan(const uint32_t *__restrict__
         int64_t tc, ts;
         const int64_t ec = block_excl_scan(cnt, s_wave, tc);
         const int64_t es = block_excl_scan(sum, s_wave, ts);
-        const uint64_t pc = tile_prefix(desc, t, epoch, (uint64_t)tc, &s_b, ctl);
-        const uint64_t ps = tile_prefix(desc_b, t, epoch, (uint64_t)ts, &s_b, ctl);
+        uint64_t pc, ps;
+        tile_prefix2(desc, (uint64_t)tc, desc_b, (uint64_t)ts, t, epoch, s_b2, pc, ps, ctl);
         int64_t b = (int64_t)pc + ec, o = (int64_t)ps + es;
         bool over = false;
 #pragma unroll

@@ -147,7 +147,7 @@ __global__ __launch_bounds__(kBlock) void k_stream_select(
 {
     const uint32_t epoch = scan_epoch(ctl);
     __shared__ int64_t s_wave[kBlock / 64];
-    __shared__ uint64_t s_b;
+    __shared__ uint64_t s_b2[2];
     __shared__ int64_t s_t;
     __shared__ int32_t s_last;
     for (;;) {
@@ -175,8 +175,8 @@ __global__ __launch_bounds__(kBlock) void k_stream_select(
         int64_t tot, totk;
         const int64_t ex = block_excl_scan(__popc(fmask), s_wave, tot);
         const int64_t exk = block_excl_scan(kids, s_wave, totk);
-        const uint64_t pre = tile_prefix(desc, t, epoch, (uint64_t)tot, &s_b, ctl);
-        const uint64_t prek = tile_prefix(desc_kids, t, epoch, (uint64_t)totk, &s_b, ctl);
+        uint64_t pre, prek;
+        tile_prefix2(desc, (uint64_t)tot, desc_kids, (uint64_t)totk, t, epoch, s_b2, pre, prek, ctl);
         int64_t e = (int64_t)pre + ex;
         int64_t run = (int64_t)prek + exk;
         bool over = false;

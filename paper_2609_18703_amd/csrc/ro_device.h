@@ -153,63 +153,88 @@ __device__ __forceinline__ void desc_put(uint64_t *d, uint64_t w)
 // instead of a hung device.
 constexpr uint32_t kSpinLimit = 1u << 24;
 
+// The look-back of tile t by one wave (all 64 lanes call it): posts the
+// tile's aggregate, sums the predecessors' values back to the nearest
+// inclusive one (64 descriptors a round), posts the tile's inclusive value
+// and returns the exclusive prefix to every lane.
+__device__ __forceinline__ uint64_t lookback_wave(uint64_t *desc, int64_t t, uint32_t epoch, uint64_t agg, Ctl *ctl)
+{
+    const int lane = lane_id();
+    agg = agg < kSat ? agg : kSat;
+    if (t == 0) {
+        if (lane == 0) desc_put(&desc[0], desc_word(epoch, kFlagInc, agg));
+        return 0;
+    }
+    if (lane == 0) desc_put(&desc[t], desc_word(epoch, kFlagAgg, agg));
+    uint64_t excl = 0;
+    int64_t base = t - 1;
+    for (;;) {
+        const int64_t j = base - lane;
+        uint32_t flag = kFlagInc;
+        uint64_t val = 0;
+        if (j >= 0) {
+            uint64_t d = 0;
+            bool ready = false;
+            for (uint32_t spin = 0; spin < kSpinLimit; ++spin) {
+                d = __hip_atomic_load(&desc[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if ((uint32_t)(d >> 48) == epoch && ((d >> 46) & 3u) != 0) {
+                    ready = true;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+            }
+            if (ready) {
+                flag = (uint32_t)((d >> 46) & 3u);
+                val = d & kValMask;
+            } else {
+                raise_err(ctl, RO_EHIP);     // treated as an inclusive zero
+            }
+        }
+        const uint64_t incm = __ballot(flag == kFlagInc);
+        const int first = incm ? (__ffsll((unsigned long long)incm) - 1) : 64;
+        excl += wave_sum<uint64_t>(lane <= first ? val : 0);
+        if (incm) break;
+        base -= 64;
+    }
+    excl = excl < kSat ? excl : kSat;
+    if (lane == 0) {
+        const uint64_t inc = excl + agg;
+        desc_put(&desc[t], desc_word(epoch, kFlagInc, inc < kSat ? inc : kSat));
+    }
+    return excl;
+}
+
 // Exclusive prefix of tile t given its aggregate; called by every thread of
 // the workgroup, returns the same value to all of them.
 __device__ __noinline__ uint64_t tile_prefix(uint64_t *desc, int64_t t, uint32_t epoch,
                                              uint64_t agg, uint64_t *s_b, Ctl *ctl)
 {
-    agg = agg < kSat ? agg : kSat;
-    if (t == 0) {
-        if (threadIdx.x == 0) {
-            desc_put(&desc[0], desc_word(epoch, kFlagInc, agg));
-            *s_b = 0;
-        }
-    } else {
-        if (threadIdx.x == 0) desc_put(&desc[t], desc_word(epoch, kFlagAgg, agg));
-        if (threadIdx.x < 64) {
-            const int lane = lane_id();
-            uint64_t excl = 0;
-            int64_t base = t - 1;
-            for (;;) {
-                const int64_t j = base - lane;
-                uint32_t flag = kFlagInc;
-                uint64_t val = 0;
-                if (j >= 0) {
-                    uint64_t d = 0;
-                    bool ready = false;
-                    for (uint32_t spin = 0; spin < kSpinLimit; ++spin) {
-                        d = __hip_atomic_load(&desc[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        if ((uint32_t)(d >> 48) == epoch && ((d >> 46) & 3u) != 0) {
-                            ready = true;
-                            break;
-                        }
-                        __builtin_amdgcn_s_sleep(1);
-                    }
-                    if (ready) {
-                        flag = (uint32_t)((d >> 46) & 3u);
-                        val = d & kValMask;
-                    } else {
-                        raise_err(ctl, RO_EHIP);     // treated as an inclusive zero
-                    }
-                }
-                const uint64_t incm = __ballot(flag == kFlagInc);
-                const int first = incm ? (__ffsll((unsigned long long)incm) - 1) : 64;
-                excl += wave_sum<uint64_t>(lane <= first ? val : 0);
-                if (incm) break;
-                base -= 64;
-            }
-            excl = excl < kSat ? excl : kSat;
-            if (threadIdx.x == 0) {
-                uint64_t inc = excl + agg;
-                desc_put(&desc[t], desc_word(epoch, kFlagInc, inc < kSat ? inc : kSat));
-                *s_b = excl;
-            }
-        }
+    if (threadIdx.x < 64) {
+        const uint64_t r = lookback_wave(desc, t, epoch, agg, ctl);
+        if (threadIdx.x == 0) *s_b = r;
     }
     __syncthreads();
     uint64_t r = *s_b;
     __syncthreads();
     return r;
+}
+
+// Two independent look-back chains of tile t at once, one wave each;
+// s_b2 holds two entries of LDS.
+__device__ __noinline__ void tile_prefix2(uint64_t *desc_a, uint64_t agg_a, uint64_t *desc_b, uint64_t agg_b,
+                                          int64_t t, uint32_t epoch, uint64_t *s_b2, uint64_t &pa, uint64_t &pb,
+                                          Ctl *ctl)
+{
+    const int w = (int)(threadIdx.x >> 6);
+    if (w < 2) {
+        const uint64_t r = w == 0 ? lookback_wave(desc_a, t, epoch, agg_a, ctl)
+                                  : lookback_wave(desc_b, t, epoch, agg_b, ctl);
+        if (lane_id() == 0) s_b2[w] = r;
+    }
+    __syncthreads();
+    pa = s_b2[0];
+    pb = s_b2[1];
+    __syncthreads();
 }
 
 // ---- searches ---------------------------------------------------------------

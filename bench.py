@@ -680,6 +680,19 @@ def _cpu_info():
     return model, os.cpu_count()
 
 
+def _host_bytes(rep):
+    """A report layout's record bytes on the host, written by the generator's
+    device fill (the same content definition, much faster than numpy)."""
+    import torch
+    from workloads import device as D
+    total = int(rep.off[-1])
+    dev = torch.zeros(max(total, 1), dtype=torch.uint8, device="cuda")
+    D.fill_records_dev(D.to_dev(rep.seed), D.to_dev(rep.off), dev)
+    host = dev.cpu().numpy()[rep.base:total]
+    del dev
+    return host
+
+
 def cpu_baseline(workload):
     """The oracle, single threaded, on a bounded sample of the workload
     (about 10-30 s of one core): the same distributions at a smaller size
@@ -712,9 +725,9 @@ def cpu_baseline(workload):
         sample = (f"the full workload ({n_parents} parents: {n_child} children, {S} surviving bytes); "
                   f"expand + 2 batches + gather")
     elif workload in ("docs-nested", "videos-nested"):
-        n = W.config3() if workload == "docs-nested" else W.config4(n_videos=300)
+        n = W.config3() if workload == "docs-nested" else W.config4()
         r = n.reports
-        data = r.data()
+        data = _host_bytes(r)
         t = time.perf_counter()
         want = O.nested(n.counts1, n.queue1, None, n.batch1, n.counts2, n.queue2, None, n.batch2,
                         r.state, r.off, data, L=L)
@@ -768,8 +781,13 @@ def cpu_baseline(workload):
                   f"the oracle holds the bytes of repeated reports only, the rest it never reads); "
                   f"expand, dispatch, commit, retry, dispatch, commit")
     else:
-        s = W.config5(n_parents=100_000, n_children=2_000_000)
-        arena = np.concatenate([rep.data() for rep in s.wave_reports] + [np.zeros(1, np.uint8)])
+        s = W.config5()
+        total = int(s.wave_reports[-1].off[-1])
+        dev = torch.zeros(total + 1, dtype=torch.uint8, device="cuda")
+        for rep in s.wave_reports:
+            D.fill_records_dev(D.to_dev(rep.seed), D.to_dev(rep.off), dev)
+        arena = dev.cpu().numpy()
+        del dev
         t = time.perf_counter()
         offs = O.expand(s.counts, tags=False, L=L)
         st = O.Stream(offs, L=L)
@@ -780,8 +798,8 @@ def cpu_baseline(workload):
         st.close()
         dt = time.perf_counter() - t
         n_child = s.n_children
-        sample = (f"{s.n_parents} parents, {n_child} children over {len(s.waves)} waves "
-                  f"(same distributions, a fifth of the size); expand + per wave batch, report, emit")
+        sample = (f"the full workload ({s.n_parents} parents, {n_child} children over {len(s.waves)} waves); "
+                  f"expand + per wave batch, report, emit")
     model, ncpu = _cpu_info()
     log(f"[bench] cpu oracle: {n_child} children in {dt:.2f}s")
     return {"value": round(n_child / dt, 1), "unit": "children/s", "cores": 1, "kind": "oracle",

@@ -19,6 +19,12 @@
  *                  soon as all of its children are terminal (Sec. 1 and 4:
  *                  completed parents proceed while others still produce),
  *                  in ascending parent order, exactly once.
+ *   - ro_batch_parent: parent-bound reservation (Sec. 4 "Scheduling Ready
+ *                  Grains"): up to B siblings of the first ready parent.
+ *   - ro_filter, ro_broadcast: F.filter and F.broadcast (Table
+ *                  "primitives") under the input propagation precedence.
+ *   - ro_grains_*: Grain phases and the generation fence (Sec. 4, Eq.
+ *                  grain-phase and Eq. generation-fence).
  *
  * Conventions shared by every entry point:
  *   * Memory.  Every array argument is DEVICE memory owned by the caller
@@ -26,8 +32,11 @@
  *     pointer past the call, except a stream's offsets and the report bytes of
  *     parents not yet emitted (see ro_stream_report).
  *   * Ordering.  Every call enqueues its kernels on the context's HIP stream
- *     and returns at once.  Nothing synchronises except ro_ctx_status,
- *     ro_ctx_reserve (which may allocate) and ro_stream_create/destroy.
+ *     and returns at once.  Nothing synchronises except ro_ctx_status, the
+ *     create/destroy calls, and a call that has to grow a workspace
+ *     (hipMalloc): ro_ctx_reserve, a gather or batch beyond the reservation,
+ *     the first ro_batch_parent of a larger queue, the first
+ *     ro_grains_commit of a larger call.
  *   * Errors.  Errors found on the host (NULL where an array is required, a
  *     negative size, batch_size <= 0, a failing HIP call) are returned
  *     immediately and nothing is enqueued.  Errors that depend on device data
@@ -85,7 +94,9 @@ int ro_ctx_set_stream(ro_ctx *ctx, void *hip_stream);
 
 /* Pre-size the device workspace for expansions of up to `max_children`
  * children and `max_parents` parents, and queues of up to `max_queue`
- * entries, so that later calls never allocate.  Calls whose host-known sizes
+ * entries, so that later expand / batch / gather / stream calls never
+ * allocate (ro_batch_parent and the Grain commit keep workspaces of their
+ * own, sized on first use).  Calls whose host-known sizes
  * (parents, queue length, report count) exceed the reservation grow it
  * (hipMalloc, which synchronises).  An expansion whose child count, known
  * only on the device, exceeds the reservation fails with RO_ECAP. */

@@ -276,7 +276,7 @@ int ro_grains_commit(ro_ctx *ctx, ro_grains *g, const ro_reports *reports, const
 
 /* Streaming gather over one expansion (offsets[P+1] on the device, kept by
  * reference until ro_stream_destroy).  The stream's own state lives in
- * device memory allocated here (about 32 bytes per child and 42 per parent).
+ * device memory allocated here (about 36 bytes per child and 42 per parent).
  * A stream is one Call: `barrier` ([P], zeroed by the caller, may be NULL)
  * is its group-failure barrier, kept by reference; pass the same array to
  * ro_batch for each wave so that barred parents' queued children are
@@ -284,6 +284,14 @@ int ro_grains_commit(ro_ctx *ctx, ro_grains *g, const ro_reports *reports, const
 typedef struct ro_stream ro_stream;
 int ro_stream_create(ro_ctx *ctx, const int64_t *offsets, int64_t n_parents, int64_t n_children,
                      uint8_t *barrier, ro_stream **out);
+
+/* ro_batch for one wave of the stream's Call: the same compaction, tags and
+ * errors, over the stream's expansion and with its barrier, but every
+ * entry's parent comes from a child -> parent map the stream built when it
+ * was created (one load instead of a search of the offsets). */
+int ro_stream_batch(ro_ctx *ctx, ro_stream *s, const uint32_t *queue, const uint8_t *keep, int64_t q_len,
+                    int32_t batch_size, uint32_t *out_child, uint32_t *out_parent, uint32_t *out_ordinal,
+                    int64_t out_cap, int64_t *n_out_dev, int64_t *n_batches_dev);
 
 /* Record one wave of reports (same validation as ro_gather; a child already
  * reported in an earlier wave is RO_EDUP).  Reports commit in the order

@@ -45,8 +45,8 @@ __global__ __launch_bounds__(kBlock) void k_batch(
     const int64_t *__restrict__ offsets, int64_t P, const uint32_t *__restrict__ cmap, int64_t cmap_cap,
     int32_t B, uint32_t *__restrict__ out_child, uint32_t *__restrict__ out_parent,
     uint32_t *__restrict__ out_ordinal, int64_t out_cap, int64_t *n_out, int64_t *n_batches,
-    const uint8_t *__restrict__ barrier, Ctl *ctl, uint64_t *desc, int64_t desc_cap, int64_t ntiles,
-    int vec_ok)
+    const uint8_t *__restrict__ barrier, const uint32_t *__restrict__ cpar, int64_t cpar_n, Ctl *ctl,
+    uint64_t *desc, int64_t desc_cap, int64_t ntiles, int vec_ok)
 {
     const uint32_t epoch = scan_epoch(ctl);
     __shared__ uint32_t s_out[kTile];          // one output array of a tile, in slot order
@@ -54,7 +54,7 @@ __global__ __launch_bounds__(kBlock) void k_batch(
     __shared__ uint64_t s_b;
     __shared__ int64_t s_t;
     __shared__ int32_t s_last;
-    const int64_t N = offsets[P];
+    const int64_t N = cpar ? min64(offsets[P], cpar_n) : offsets[P];   // ids past the map are out of range
     int64_t nmap = (N + (1 << kCmapShift) - 1) >> kCmapShift;
     nmap = nmap < cmap_cap ? nmap : cmap_cap;
     const bool want_tags = out_parent != nullptr || out_ordinal != nullptr;
@@ -104,13 +104,12 @@ __global__ __launch_bounds__(kBlock) void k_batch(
                 if (c >= N) {
                     bad_range = true;
                 } else if (want_tags || barrier) {
-                    const int64_t p = parent_of(cmap, nmap, offsets, P, c);
-                    if (barrier && barrier[p]) {
-                        kmask &= ~(1u << k);
-                    } else {
-                        par[k] = (uint32_t)p;
-                        ord[k] = (uint32_t)(c - offsets[p]);
-                    }
+                    int64_t p;
+                    if (cpar != nullptr) p = (int64_t)cpar[c];
+                    else p = parent_of(cmap, nmap, offsets, P, c);
+                    par[k] = (uint32_t)p;
+                    ord[k] = (uint32_t)(c - offsets[p]);
+                    if (barrier && barrier[p]) kmask &= ~(1u << k);      // suppressed: takes no slot
                 }
             }
         }
@@ -183,9 +182,9 @@ __global__ __launch_bounds__(kBlock) void k_batch_all(
     const uint32_t *__restrict__ queue, int64_t Q, const int64_t *__restrict__ offsets, int64_t P,
     const uint32_t *__restrict__ cmap, int64_t cmap_cap, int32_t B, uint32_t *__restrict__ out_child,
     uint32_t *__restrict__ out_parent, uint32_t *__restrict__ out_ordinal, int64_t out_cap, int64_t *n_out,
-    int64_t *n_batches, Ctl *ctl)
+    int64_t *n_batches, const uint32_t *__restrict__ cpar, int64_t cpar_n, Ctl *ctl)
 {
-    const int64_t N = offsets[P];
+    const int64_t N = cpar ? min64(offsets[P], cpar_n) : offsets[P];   // ids past the map are out of range
     int64_t nmap = (N + (1 << kCmapShift) - 1) >> kCmapShift;
     nmap = nmap < cmap_cap ? nmap : cmap_cap;
     const bool want_tags = out_parent != nullptr || out_ordinal != nullptr;
@@ -208,7 +207,7 @@ __global__ __launch_bounds__(kBlock) void k_batch_all(
         // lockstep search of the offsets (ids out of range search for N - 1
         // and are reported below)
         int64_t par[kAllPer];
-        if (want_tags && nmap == 0) {
+        if (want_tags && nmap == 0 && cpar == nullptr) {
             int64_t key[kAllPer];
 #pragma unroll
             for (int k = 0; k < kAllPer; ++k) key[k] = (int64_t)q[k] < N ? (int64_t)q[k] : N - 1;
@@ -230,7 +229,8 @@ __global__ __launch_bounds__(kBlock) void k_batch_all(
             if (i >= lim) continue;
             if (out_child) out_child[i] = q[k];
             if (want_tags) {
-                const int64_t p = nmap == 0 ? par[k] : parent_of(cmap, nmap, offsets, P, c);
+                const int64_t p = cpar ? (int64_t)cpar[c]
+                                       : (nmap == 0 ? par[k] : parent_of(cmap, nmap, offsets, P, c));
                 if (out_parent) out_parent[i] = (uint32_t)p;
                 if (out_ordinal) out_ordinal[i] = (uint32_t)(c - offsets[p]);
             }
@@ -243,13 +243,14 @@ hipError_t launch_batch(const Launch &L, const uint32_t *queue, const uint8_t *k
                         int64_t Q, const int64_t *offsets, int64_t P, int32_t B,
                         uint32_t *out_child, uint32_t *out_parent, uint32_t *out_ordinal,
                         int64_t out_cap, int64_t *n_out, int64_t *n_batches, uint32_t *cmap,
-                        int64_t cmap_cap, const uint8_t *barrier)
+                        int64_t cmap_cap, const uint8_t *barrier, const uint32_t *cpar, int64_t cpar_n)
 {
     // The coarse map costs a search per 64 children; a short unmasked queue
     // (fewer entries than parents, such as one wave of a stream) searches
     // the offsets directly instead and skips the extra launch.
     const bool tags = out_parent != nullptr || out_ordinal != nullptr;
-    const bool use_map = (tags || barrier != nullptr) && !(keep == nullptr && barrier == nullptr && Q < P);
+    const bool use_map = cpar == nullptr && (tags || barrier != nullptr) &&
+                         !(keep == nullptr && barrier == nullptr && Q < P);
     if (use_map) {
         const int64_t grid_m = (int64_t)L.num_cus * 4;
         RO_LAUNCH(L, RO_K_BATCH_SAMPLES, k_batch_cmap, dim3((unsigned)grid_m), dim3(256), 0, L.stream,
@@ -262,7 +263,7 @@ hipError_t launch_batch(const Launch &L, const uint32_t *queue, const uint8_t *k
         grid_a = grid_a < 1 ? 1 : (grid_a > (int64_t)L.num_cus * 8 ? (int64_t)L.num_cus * 8 : grid_a);
         RO_LAUNCH(L, RO_K_BATCH, k_batch_all, dim3((unsigned)grid_a), dim3(kBlock), 0, L.stream, queue, Q,
                   offsets, P, cmap, cmap_cap, B, out_child, out_parent, out_ordinal, out_cap, n_out, n_batches,
-                  L.ctl);
+                  cpar, cpar_n, L.ctl);
         return hipGetLastError();
     }
     const int64_t ntiles = Q > 0 ? (Q + kTile - 1) / kTile : 1;
@@ -271,7 +272,7 @@ hipError_t launch_batch(const Launch &L, const uint32_t *queue, const uint8_t *k
     const bool aligned = ((reinterpret_cast<uintptr_t>(queue) | reinterpret_cast<uintptr_t>(keep)) & 15u) == 0;
     RO_LAUNCH(L, RO_K_BATCH, k_batch, dim3((unsigned)grid), dim3(kBlock), 0, L.stream, queue, keep, Q,
               offsets, P, cmap, cmap_cap, B, out_child, out_parent, out_ordinal, out_cap, n_out, n_batches,
-              barrier, L.ctl, L.desc, L.desc_cap, ntiles, aligned ? 1 : 0);
+              barrier, cpar, cpar_n, L.ctl, L.desc, L.desc_cap, ntiles, aligned ? 1 : 0);
     return hipGetLastError();
 }
 

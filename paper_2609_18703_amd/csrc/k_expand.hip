@@ -131,4 +131,15 @@ hipError_t launch_expand(const Launch &L, const int32_t *counts, int64_t P,
     return hipGetLastError();
 }
 
+hipError_t launch_expand_tags(const Launch &L, const int64_t *offsets, int64_t P, uint32_t *child_parent,
+                              uint32_t *child_ordinal, int64_t child_cap)
+{
+    const bool aligned = ((reinterpret_cast<uintptr_t>(child_parent) |
+                           reinterpret_cast<uintptr_t>(child_ordinal)) & 15u) == 0;
+    const int64_t grid2 = (int64_t)L.num_cus * 8;
+    RO_LAUNCH(L, RO_K_EXPAND_TAGS, k_expand_tags, dim3((unsigned)grid2), dim3(kBlock), 0, L.stream, offsets, P,
+              child_parent, child_ordinal, child_cap, aligned ? 1 : 0);
+    return hipGetLastError();
+}
+
 }  // namespace ro

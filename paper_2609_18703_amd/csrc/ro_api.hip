@@ -572,6 +572,7 @@ int ro_stream_create(ro_ctx *c, const int64_t *offsets, int64_t n_parents, int64
         (size_t)(N + 1) * sizeof(uint64_t),                 // esrc
         (size_t)(P + 1) * sizeof(uint64_t),                 // gkey
         (size_t)(P + 1),                                    // ebar
+        (size_t)(N > 0 ? N : 1) * sizeof(uint32_t),         // cpar
     };
     constexpr int kArrays = (int)(sizeof(sizes) / sizeof(sizes[0]));
     size_t offs[kArrays], total = 0;
@@ -609,16 +610,32 @@ int ro_stream_create(ro_ctx *c, const int64_t *offsets, int64_t n_parents, int64
     st.esrc = (uint64_t *)(block + offs[9]);
     st.gkey = (uint64_t *)(block + offs[10]);
     st.ebar = (uint8_t *)(block + offs[11]);
+    st.cpar = (uint32_t *)(block + offs[12]);
     st.barrier = barrier;
     st.run_epoch = 1;
     st.gf_epoch = 0;
-    if (launch_stream_init(launch_of(c), st) != hipSuccess) {
+    if (launch_stream_init(launch_of(c), st) != hipSuccess ||
+        launch_expand_tags(launch_of(c), offsets, P, st.cpar, nullptr, N) != hipSuccess) {
         (void)hipFree(block);
         free(s);
         return RO_EHIP;
     }
     *out = s;
     return RO_OK;
+}
+
+int ro_stream_batch(ro_ctx *c, ro_stream *s, const uint32_t *queue, const uint8_t *keep, int64_t q_len,
+                    int32_t batch_size, uint32_t *out_child, uint32_t *out_parent, uint32_t *out_ordinal,
+                    int64_t out_cap, int64_t *n_out_dev, int64_t *n_batches_dev)
+{
+    if (!c || !s || s->ctx != c || q_len < 0 || batch_size <= 0 || out_cap < 0 || (q_len > 0 && !queue))
+        return RO_EINVAL;
+    int rc = ensure_desc(c, tiles_for(q_len));
+    if (rc) return rc;
+    const StreamState &st = s->st;
+    return hip_fail(launch_batch(launch_of(c), queue, keep, q_len, st.offsets, st.P, batch_size, out_child,
+                                 out_parent, out_ordinal, out_cap, n_out_dev, n_batches_dev, nullptr, 0, st.barrier,
+                                 st.cpar, st.N));
 }
 
 int ro_stream_report(ro_ctx *c, ro_stream *s, const ro_reports *r, int64_t *n_rejected_dev)

@@ -78,11 +78,17 @@ hipError_t launch_expand(const Launch &L, const int32_t *counts, int64_t P,
                          int64_t *offsets, uint32_t *child_parent, uint32_t *child_ordinal,
                          int64_t child_cap);
 
+// cpar (or null): the parent of each of the first cpar_n children, which
+// then replaces the search of the offsets (a stream's own map); ids past
+// cpar_n are out of range
 hipError_t launch_batch(const Launch &L, const uint32_t *queue, const uint8_t *keep,
                         int64_t Q, const int64_t *offsets, int64_t P, int32_t B,
                         uint32_t *out_child, uint32_t *out_parent, uint32_t *out_ordinal,
                         int64_t out_cap, int64_t *n_out, int64_t *n_batches, uint32_t *cmap,
-                        int64_t cmap_cap, const uint8_t *barrier);
+                        int64_t cmap_cap, const uint8_t *barrier, const uint32_t *cpar = nullptr,
+                        int64_t cpar_n = 0);
+hipError_t launch_expand_tags(const Launch &L, const int64_t *offsets, int64_t P, uint32_t *child_parent,
+                              uint32_t *child_ordinal, int64_t child_cap);
 
 // parent-bound reservation workspace ([cap] queue entries, [pcap] parents)
 struct PbWs {
@@ -181,6 +187,7 @@ struct StreamState {
     uint8_t *barrier;        // [P] the Call's group-failure barrier (caller's, or null)
     uint64_t *gkey;          // [P] first group failure per parent in the current report call
     uint8_t *ebar;           // [P] per emitted parent: barred
+    uint32_t *cpar;          // [N] parent of every child (for the stream's batches)
     uint32_t run_epoch;      // slot tag epoch of this run (advanced by each reset)
     uint32_t gf_epoch;       // epoch of the current report call in gkey
 };

@@ -161,7 +161,7 @@ class StreamingBuffers:
 
 
 def streaming(ctx, b: StreamingBuffers, on_wave=None, st=None):
-    """expand once; per wave: batch -> stream report -> stream emit.
+    """expand once; per wave: the stream's batch -> stream report -> stream emit.
 
     ``on_wave(w)`` (optional) runs after each wave's emission is enqueued, to
     consume that wave's outputs before the next wave overwrites them.  ``st``
@@ -178,8 +178,8 @@ def streaming(ctx, b: StreamingBuffers, on_wave=None, st=None):
     try:
         for w, q in enumerate(b.queues):
             n = q.numel()
-            ctx.batch(q, None, b.offsets, b.B, None, b.tag_parent, b.tag_ordinal,
-                      b.scalars[0:1], b.scalars[1:2], q_len=n, out_cap=n)
+            st.batch(q, None, b.B, None, b.tag_parent, b.tag_ordinal, b.scalars[0:1], b.scalars[1:2], q_len=n,
+                     out_cap=n)
             st.report(b.tag_parent, b.tag_ordinal, b.states[w], b.offs[w], b.data, n=n)
             st.emit(b.emit_parent, b.emit_off, b.emit_data, b.emit_cnt[:P], b.emit_cnt[P:2 * P],
                     b.emit_cnt[2 * P:], b.emit_state, b.scalars[2:3], b.scalars[3:4],

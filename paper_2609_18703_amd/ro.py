@@ -69,6 +69,7 @@ def load(path=None):
     L.ro_batch_parent.argtypes = [P, P, P, i64, P, i64, i32, P, P, P, i64, P, i64, P, P, P]
     L.ro_gather.argtypes = [P, C.POINTER(ReportsT), P, i64, C.POINTER(GatherOutT)]
     L.ro_stream_create.argtypes = [P, P, i64, i64, P, pp]
+    L.ro_stream_batch.argtypes = [P, P, P, P, i64, i32, P, P, P, i64, P, P]
     L.ro_stream_report.argtypes = [P, P, C.POINTER(ReportsT), P]
     L.ro_stream_emit.argtypes = [P, P, P, P, P, i64, i64, P, P, P, P, P, P]
     L.ro_stream_reset.argtypes = [P, P]
@@ -84,9 +85,9 @@ def load(path=None):
     L.ro_stream_destroy.argtypes = [P]
     L.ro_ctx_trace.argtypes = [P, C.c_int]
     L.ro_ctx_trace_read.argtypes = [P, P, P, i32]
-    for name in ("ro_ctx_trace", "ro_ctx_trace_read", "ro_ctx_create", "ro_ctx_set_stream", "ro_ctx_reserve", "ro_ctx_status",
-                 "ro_ctx_destroy", "ro_expand", "ro_batch", "ro_batch_parent", "ro_gather", "ro_stream_create",
-                 "ro_stream_report", "ro_stream_emit", "ro_stream_reset", "ro_stream_destroy", "ro_filter",
+    for name in ("ro_ctx_trace", "ro_ctx_trace_read", "ro_ctx_create", "ro_ctx_set_stream", "ro_ctx_reserve",
+                 "ro_ctx_status", "ro_ctx_destroy", "ro_expand", "ro_batch", "ro_batch_parent", "ro_gather",
+                 "ro_stream_create", "ro_stream_batch", "ro_stream_report", "ro_stream_emit", "ro_stream_reset", "ro_stream_destroy", "ro_filter",
                  "ro_broadcast", "ro_grains_create", "ro_grains_reset", "ro_grains_destroy", "ro_grains_read",
                  "ro_grains_dispatch", "ro_grains_retry", "ro_grains_commit"):
         getattr(L, name).restype = C.c_int
@@ -287,6 +288,18 @@ class Stream:
         _check(ctx.L.ro_stream_create(ctx.h, _ptr(offsets), offsets.numel() - 1, int(n_children),
                                       _ptr(barrier), C.byref(h)), "ro_stream_create")
         self.h = h
+
+    def batch(self, queue, keep, batch_size, out_child=None, out_parent=None, out_ordinal=None, n_out=None,
+              n_batches=None, q_len=None, out_cap=None):
+        """FIFO batches of one wave (ro_batch over this stream's expansion and barrier)."""
+        q_len = queue.numel() if q_len is None else q_len
+        if out_cap is None:
+            outs = [t.numel() for t in (out_child, out_parent, out_ordinal) if t is not None]
+            out_cap = min(outs) if outs else q_len
+        _check(self.ctx.L.ro_stream_batch(self.ctx.h, self.h, _ptr(queue), _ptr(keep), q_len, int(batch_size),
+                                          _ptr(out_child), _ptr(out_parent), _ptr(out_ordinal), int(out_cap),
+                                          _ptr(n_out), _ptr(n_batches)),
+               "ro_stream_batch")
 
     def report(self, parent, ordinal, state, off, data, n=None, n_rejected=None):
         rep = _reports(parent, ordinal, state, off, data, n)

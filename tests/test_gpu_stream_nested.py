@@ -239,3 +239,47 @@ def test_stream_duplicate_across_waves(ctx):
     PL.streaming(ctx, b)
     assert ctx.status() == O.EDUP
     ctx.check("after duplicate")
+
+
+def test_stream_batch_matches_batch_and_oracle(ctx):
+    """A stream's own batch (parents from the map it built at creation) gives
+    the slots, tags and counts of the oracle's FIFO batch, with and without a
+    ready mask, with the stream's barrier, and rejects ids past the
+    expansion."""
+    import paper_2609_18703_amd as R
+    rng = np.random.default_rng(21)
+    counts = rng.integers(0, 12, 30_000).astype(np.int32)
+    counts[5] = 20_000
+    offs = O.expand(counts, tags=False)
+    N = int(offs[-1])
+    od = D.to_dev(offs)
+    bar = torch.zeros(len(counts), dtype=torch.uint8, device="cuda")
+    st = ctx.stream(od, N, barrier=bar)
+    try:
+        for wave, (Q, masked, barred) in enumerate([(50_000, False, False), (7_000, True, False),
+                                                     (N, True, False), (30_000, False, True)]):
+            q = rng.choice(N, Q, replace=False).astype(np.uint32)
+            keep = (rng.random(Q) < 0.8).astype(np.uint8) if masked else None
+            hb = np.zeros(len(counts), np.uint8)
+            if barred:
+                hb[rng.random(len(counts)) < 0.3] = 1
+            bar.copy_(torch.from_numpy(hb))
+            oc = torch.full((Q,), -1, dtype=torch.int32, device="cuda")
+            op = torch.full((Q,), -1, dtype=torch.int32, device="cuda")
+            oo = torch.full((Q,), -1, dtype=torch.int32, device="cuda")
+            sc = torch.full((2,), -1, dtype=torch.int64, device="cuda")
+            st.batch(_i32(q), None if keep is None else D.to_dev(keep), 1024, oc, op, oo, sc[0:1], sc[1:2])
+            ctx.check(f"stream batch wave {wave}")
+            want = O.batch(q, keep, offs, 1024, barrier=hb if barred else None)
+            m = int(sc[0].item())
+            assert m == len(want[0]) and int(sc[1].item()) == len(want[3]), wave
+            assert np.array_equal(_u32(oc, m), want[0]), wave
+            assert np.array_equal(_u32(op, m), want[1]), wave
+            assert np.array_equal(_u32(oo, m), want[2]), wave
+        bar.zero_()
+        bad = np.array([0, N, 3], np.uint32)
+        t = torch.zeros(3, dtype=torch.int32, device="cuda")
+        st.batch(_i32(bad), None, 4, t, t, t)
+        assert ctx.status() == R.ERANGE
+    finally:
+        st.close()

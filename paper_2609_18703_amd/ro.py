@@ -140,6 +140,11 @@ class Context:
     def check(self, what="device"):
         _check(self.status(), what)
 
+    def set_stream(self, stream):
+        """Re-bind the context to another torch stream (waits for the old one)."""
+        _check(self.L.ro_ctx_set_stream(self.h, C.c_void_p(stream.cuda_stream)), "ro_ctx_set_stream")
+        self._stream = stream
+
     def trace(self, enable=True):
         """Bracket every kernel this context launches with HIP events."""
         _check(self.L.ro_ctx_trace(self.h, 1 if enable else 0), "ro_ctx_trace")

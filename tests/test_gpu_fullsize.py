@@ -1,8 +1,10 @@
 """GPU parity at the workloads' full sizes, in the benchmark's launch
-configuration.  Every integer output is compared with the oracle in full; the
-payload bytes are checked on sampled parents against the content definition
-(each record is the splitmix64 stream of its own (parent, ordinal)), and their
-totals and slot offsets are compared in full."""
+configuration.  Every integer output is compared with the oracle in full.
+The payload bytes are checked on sampled parents against the content
+definition (each record is the splitmix64 stream of its own (parent,
+ordinal)) computed on the host, and then all of them on the device against
+the same definition written by the generator's fill, at the oracle's slot
+offsets."""
 import sys
 
 import numpy as np
@@ -48,6 +50,25 @@ def _sample_parents(rng, counts, n, n_big=10):
     return np.unique(np.concatenate([big, rnd, [0, len(counts) - 1]]))
 
 
+def _expected_bytes_dev(counts, lengths, mask):
+    """Device bytes of every child with mask set, in canonical order, each
+    its record by the content definition (splitmix64 of its (parent,
+    ordinal)); these are the packed slots of a gather whose surviving
+    children are the masked ones."""
+    counts = np.asarray(counts, np.int64)
+    parent = np.repeat(np.arange(len(counts), dtype=np.int64), counts)
+    first = np.cumsum(counts) - counts
+    ordinal = np.arange(int(counts.sum()), dtype=np.int64) - np.repeat(first, counts)
+    idx = np.flatnonzero(mask)
+    lens = np.asarray(lengths, np.int64)[idx]
+    off = np.zeros(len(idx) + 1, np.int64)
+    np.cumsum(lens, out=off[1:])
+    out = torch.empty(max(int(off[-1]), 1), dtype=torch.uint8, device="cuda")
+    if len(idx):
+        D.fill_records_dev(D.to_dev(W.content_seed(parent[idx], ordinal[idx])), D.to_dev(off), out)
+    return out[:int(off[-1])]
+
+
 def test_config2_full(ctx):
     from paper_2609_18703_amd import pipeline as PL
     c = W.config2()
@@ -69,6 +90,13 @@ def test_config2_full(ctx):
         lo, hi = int(g["out_off"][p]), int(g["out_off"][p + 1])
         assert hi - lo == len(exp)
         assert np.array_equal(b.out_data[lo:hi].cpu().numpy(), exp), p
+    # every byte: the surviving children's records in canonical order (the
+    # slot offsets above are the oracle's)
+    _say("config2: all bytes")
+    exp = _expected_bytes_dev(c.counts, c.lengths, c.states == W.SUCCESS)
+    S = int(g["out_off"][-1])
+    assert exp.numel() == S and torch.equal(b.out_data[:S], exp)
+    del exp
 
 
 def _nested_full(ctx, n, sample_top=60, n_big=10):
@@ -113,6 +141,19 @@ def _nested_full(ctx, n, sample_top=60, n_big=10):
         lo, hi = int(up["out_off"][d]), int(up["out_off"][d + 1])
         assert hi - lo == len(exp)
         assert np.array_equal(b.top_data[lo:hi].cpu().numpy(), exp), d
+    # every byte of both levels: a mid slot packs its successful leaves; a
+    # top slot packs the leaves of its successful mid slots
+    _say("nested: all bytes")
+    ok = n.states == W.SUCCESS
+    exp = _expected_bytes_dev(n.counts2, n.lengths, ok)
+    S2 = int(low["out_off"][-1])
+    assert exp.numel() == S2 and torch.equal(b.mid_data[:S2], exp)
+    del exp
+    mid_ok = np.repeat(low["parent_state"] == W.SUCCESS, n.counts2.astype(np.int64))
+    exp = _expected_bytes_dev(n.counts2, n.lengths, ok & mid_ok)
+    S1 = int(up["out_off"][-1])
+    assert exp.numel() == S1 and torch.equal(b.top_data[:S1], exp)
+    del exp
 
 
 def test_config3_full(ctx):
@@ -129,7 +170,7 @@ def test_config4_full(ctx):
 
 def test_config5_full_streaming(ctx):
     """50 waves over 10^7 children: every wave's emitted parents, slot
-    offsets, counts and states in full; bytes of sampled emitted parents."""
+    offsets, counts, states and bytes in full."""
     from paper_2609_18703_amd import pipeline as PL
     s = W.config5()
     _say("config5 full: N =", s.n_children, "waves =", len(s.waves))
@@ -160,6 +201,14 @@ def test_config5_full_streaming(ctx):
         assert np.array_equal(b.emit_cnt.cpu().numpy()[:E], want["n_success"]), w
         assert np.array_equal(b.emit_state.cpu().numpy()[:E], want["parent_state"]), w
         if E:
+            # every emitted byte: the emitted parents' children in order
+            ep = want["parent"].astype(np.int64)
+            ks = s.counts[ep].astype(np.int64)
+            cidx = np.repeat(offs[ep] - np.cumsum(ks) + ks, ks) + np.arange(int(ks.sum()))
+            mask = np.zeros(s.n_children, bool)
+            mask[cidx] = s.states[cidx] == W.SUCCESS
+            exp = _expected_bytes_dev(s.counts, s.lengths, mask)
+            assert exp.numel() == nb and torch.equal(b.emit_data[:nb], exp), w
             for j in np.unique(rng.integers(0, E, 4)):
                 p = int(want["parent"][j])
                 exp = _expected_slot(int(offs[p]), s.states, s.lengths, p, int(s.counts[p]))

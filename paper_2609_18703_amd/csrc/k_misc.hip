@@ -1,4 +1,5 @@
-// Context bookkeeping kernels: control-word initialisation and epoch resets.
+// Context bookkeeping kernels: control-word initialisation, epoch resets and
+// fills.  (The look-back epoch wraps on the device: see ticket_done_n.)
 #include "ro_device.h"
 
 namespace ro {
@@ -11,12 +12,11 @@ __global__ void k_ctl_init(Ctl *ctl)
     }
 }
 
-// Clears every look-back descriptor and restarts the descriptor epoch at 1.
-__global__ void k_reset_scan_epoch(Ctl *ctl, uint64_t *desc, int64_t n)
+// Moves the canonical epoch forward (a test aid: slots of earlier epochs
+// read as unreported at any later epoch).
+__global__ void k_set_canon_epoch(Ctl *ctl, uint32_t e)
 {
-    const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    for (int64_t i = g; i < n; i += (int64_t)gridDim.x * blockDim.x) desc[i] = 0;
-    if (g == 0) ctl->scan_epoch = 1;
+    if (threadIdx.x == 0) ctl->canon_epoch = e;
 }
 
 // Clears every canonical slot's tag and restarts the canonical epoch at 1.
@@ -59,10 +59,9 @@ hipError_t launch_ctl_init(const Launch &L)
     return hipGetLastError();
 }
 
-hipError_t launch_reset_scan_epoch(const Launch &L)
+hipError_t launch_set_canon_epoch(const Launch &L, uint32_t e)
 {
-    RO_LAUNCH(L, RO_K_MISC, k_reset_scan_epoch, dim3((unsigned)L.num_cus), dim3(256), 0, L.stream, L.ctl,
-                       L.desc, L.desc_cap);
+    RO_LAUNCH(L, RO_K_MISC, k_set_canon_epoch, dim3(1), dim3(64), 0, L.stream, L.ctl, e);
     return hipGetLastError();
 }
 

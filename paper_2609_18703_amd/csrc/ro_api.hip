@@ -679,6 +679,31 @@ int ro_stream_reset(ro_ctx *c, ro_stream *s)
     return hip_fail(launch_stream_reset(launch_of(c), s->st));
 }
 
+int ro_debug_epochs(ro_ctx *c, ro_stream *s, ro_grains *g, int64_t canon_left, int64_t run_left,
+                    int64_t gf_left, int64_t fence_left)
+{
+    if (!c || (s && s->ctx != c) || (g && g->ctx != c)) return RO_EINVAL;
+    if (canon_left >= 1 && canon_left < (int64_t)kMaxCanonEpoch) {
+        // the next gather runs at epoch max - canon_left + 1
+        const uint32_t e = (uint32_t)((int64_t)kMaxCanonEpoch - canon_left + 1);
+        if (e > (uint32_t)c->gathers) {
+            if (launch_set_canon_epoch(launch_of(c), e) != hipSuccess) return RO_EHIP;
+            c->gathers = e;
+        }
+    }
+    if (s) {
+        if (run_left >= 1 && run_left < (int64_t)kMaxCanonEpoch &&
+            (uint32_t)((int64_t)kMaxCanonEpoch - run_left) > s->st.run_epoch)
+            s->st.run_epoch = (uint32_t)((int64_t)kMaxCanonEpoch - run_left);
+        if (gf_left >= 1 && gf_left <= 0xffffffffll &&
+            (uint32_t)(0xffffffffll - gf_left) > s->st.gf_epoch)
+            s->st.gf_epoch = (uint32_t)(0xffffffffll - gf_left);
+    }
+    if (g && fence_left >= 1 && fence_left <= 0xffffffffll && (uint32_t)(0xffffffffll - fence_left) > g->epoch)
+        g->epoch = (uint32_t)(0xffffffffll - fence_left);
+    return RO_OK;
+}
+
 int ro_stream_destroy(ro_stream *s)
 {
     if (!s) return RO_EINVAL;

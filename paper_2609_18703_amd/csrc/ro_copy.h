@@ -23,7 +23,6 @@ __device__ __forceinline__ void st16(uint64_t a, uint4 v)
     const v4u32 t = {v.x, v.y, v.z, v.w};
     *(RO_GLOBAL v4u32 *)a = t;
 }
-__device__ __forceinline__ uint8_t ld8(uint64_t a) { return *(const RO_GLOBAL uint8_t *)a; }
 __device__ __forceinline__ void st8(uint64_t a, uint8_t v) { *(RO_GLOBAL uint8_t *)a = v; }
 
 // Bytes sh..sh+15 of the 32-byte pair (lo, hi).

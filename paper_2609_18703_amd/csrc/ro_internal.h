@@ -67,8 +67,8 @@ constexpr uint32_t kMaxScanEpoch = 65535;
 constexpr uint32_t kMaxCanonEpoch = (1u << 30) - 1;
 
 // Reset kernels the host enqueues when a device epoch is about to wrap.
-hipError_t launch_reset_scan_epoch(const Launch &L);
 hipError_t launch_reset_canon(const Launch &L, Canon *canon, int64_t n);
+hipError_t launch_set_canon_epoch(const Launch &L, uint32_t e);
 hipError_t launch_ctl_init(const Launch &L);
 hipError_t launch_zero_u64(const Launch &L, uint64_t *p, int64_t n);
 hipError_t launch_clear_tags(const Launch &L, Canon *canon, int64_t n);

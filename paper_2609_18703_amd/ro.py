@@ -70,6 +70,7 @@ def load(path=None):
     L.ro_gather.argtypes = [P, C.POINTER(ReportsT), P, i64, C.POINTER(GatherOutT)]
     L.ro_stream_create.argtypes = [P, P, i64, i64, P, pp]
     L.ro_stream_batch.argtypes = [P, P, P, P, i64, i32, P, P, P, i64, P, P]
+    L.ro_debug_epochs.argtypes = [P, P, P, i64, i64, i64, i64]
     L.ro_stream_report.argtypes = [P, P, C.POINTER(ReportsT), P]
     L.ro_stream_emit.argtypes = [P, P, P, P, P, i64, i64, P, P, P, P, P, P]
     L.ro_stream_reset.argtypes = [P, P]
@@ -89,7 +90,7 @@ def load(path=None):
                  "ro_ctx_status", "ro_ctx_destroy", "ro_expand", "ro_batch", "ro_batch_parent", "ro_gather",
                  "ro_stream_create", "ro_stream_batch", "ro_stream_report", "ro_stream_emit", "ro_stream_reset", "ro_stream_destroy", "ro_filter",
                  "ro_broadcast", "ro_grains_create", "ro_grains_reset", "ro_grains_destroy", "ro_grains_read",
-                 "ro_grains_dispatch", "ro_grains_retry", "ro_grains_commit"):
+                 "ro_grains_dispatch", "ro_grains_retry", "ro_grains_commit", "ro_debug_epochs"):
         getattr(L, name).restype = C.c_int
     if path == LIB_PATH:
         _lib = L
@@ -139,6 +140,12 @@ class Context:
 
     def check(self, what="device"):
         _check(self.status(), what)
+
+    def debug_epochs(self, stream=None, grains=None, canon_left=0, run_left=0, gf_left=0, fence_left=0):
+        """Test aid: bring epoch wrap-arounds within a few calls (ro_debug_epochs)."""
+        _check(self.L.ro_debug_epochs(self.h, stream.h if stream is not None else None,
+                                      grains.h if grains is not None else None, int(canon_left), int(run_left),
+                                      int(gf_left), int(fence_left)), "ro_debug_epochs")
 
     def set_stream(self, stream):
         """Re-bind the context to another torch stream (waits for the old one)."""

@@ -85,8 +85,8 @@ def test_fence_cases(ctx):
     g.close(); og.close()
 
 
-@pytest.mark.parametrize("seed", [0, 1, 2])
-def test_fence_lockstep_random_schedule(ctx, seed):
+@pytest.mark.parametrize("seed,fence_left", [(0, 0), (1, 0), (2, 0), (3, 2)])
+def test_fence_lockstep_random_schedule(ctx, seed, fence_left):
     rng = np.random.default_rng(seed)
     counts = rng.integers(0, 7, 5000).astype(np.int32)
     offs, cp, co = O.expand(counts)
@@ -97,6 +97,7 @@ def test_fence_lockstep_random_schedule(ctx, seed):
     poff = np.concatenate([[0], np.cumsum(lens)])
     og = O.Grains(N)
     g = ctx.grains(N)
+    ctx.debug_epochs(grains=g, fence_left=fence_left)     # with 2: the fence epoch wraps after the 2nd commit
     ready = list(rng.permutation(N))
     committed = np.zeros(N, bool)
     old = []

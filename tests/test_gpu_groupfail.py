@@ -90,11 +90,29 @@ def _gf_reports(rng, counts, p_gf):
 
 @pytest.mark.parametrize("seed", [0, 1, 2])
 def test_gather_group_failure_matches_oracle(ctx, seed):
+    _gf_gather_case(ctx, seed)
+
+
+def test_gather_across_canonical_epoch_wrap():
+    """Six group-failure gathers on one context whose canonical epoch wraps
+    after the second (test aid): every slot of an earlier call reads as
+    unreported, before and after the wrap."""
+    import paper_2609_18703_amd as R
+    c = R.Context()
+    try:
+        c.debug_epochs(canon_left=3)
+        for seed in range(6):
+            _gf_gather_case(c, seed)
+    finally:
+        c.close()
+
+
+def _gf_gather_case(ctx, seed):
     rng = np.random.default_rng(100 + seed)
     counts = rng.integers(0, 9, 4000).astype(np.int32)
     offs = O.expand(counts, tags=False)
     P = len(counts)
-    par, ordi, st, off, data = _gf_reports(rng, counts, [0.02, 0.1, 0.3][seed])
+    par, ordi, st, off, data = _gf_reports(rng, counts, [0.02, 0.1, 0.3][seed % 3])
     bar_in = (rng.random(P) < 0.1).astype(np.uint8)
     want = O.gather(par, ordi, st, off, data, offs, barrier=bar_in, child_dst=True)
     tot = int(want["out_off"][-1])
@@ -190,10 +208,12 @@ def test_stream_group_failure_figure(ctx):
     st.close()
 
 
-def test_failure_trace_waves(ctx):
+@pytest.mark.parametrize("gf_left", [0, 3])
+def test_failure_trace_waves(ctx, gf_left):
     """The failure-containment analog at full size (1,885 documents, 45,507
     pages, 99 poisoned), wave by wave against the oracle: the reserved
-    children, rejected reports, and every emission."""
+    children, rejected reports, and every emission.  With gf_left the
+    stream's group-failure epoch wraps after its third report (test aid)."""
     from failure_sched import oracle_waves
     t = W.failure_trace()
     offs, waves = oracle_waves(t)
@@ -201,6 +221,7 @@ def test_failure_trace_waves(ctx):
     d_offs = D.to_dev(offs)
     bar = torch.zeros(P, dtype=torch.uint8, device="cuda")
     st = ctx.stream(d_offs, N, bar)
+    ctx.debug_epochs(stream=st, gf_left=gf_left)
     total = int(waves[-1]["off"][-1])
     arena = torch.zeros(total + 16, dtype=torch.uint8, device="cuda")
     remaining = _i32(t.queue)

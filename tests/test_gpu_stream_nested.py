@@ -110,7 +110,7 @@ def test_nested_canonical_order(ctx):
 
 
 # ------------------------------------------------------------------ streaming
-def _stream_case(ctx, counts, waves, B=64, runs=1):
+def _stream_case(ctx, counts, waves, B=64, runs=1, run_left=0):
     """waves: list of (child ids, states, lengths); all reports of a wave are in
     its queue order; bytes of every wave live in one arena.  With runs > 1 the
     whole stream is replayed on one stream state, reset between runs."""
@@ -156,6 +156,7 @@ def _stream_case(ctx, counts, waves, B=64, runs=1):
     else:
         ctx.expand(b.counts, b.offsets)          # the stream validates its offsets when created
         st = ctx.stream(b.offsets, N)
+        ctx.debug_epochs(stream=st, run_left=run_left)
         for _ in range(runs):
             PL.streaming(ctx, b, on_wave, st=st)
         st.close()
@@ -178,10 +179,12 @@ def test_stream_config5_shape(ctx):
     _stream_case(ctx, s.counts, waves, B=s.batch_size)
 
 
-def test_stream_reset_replays(ctx):
+@pytest.mark.parametrize("run_left", [0, 2])
+def test_stream_reset_replays(ctx, run_left):
     """A reset stream forgets every report and emission: three runs over one
     stream state give the oracle's emissions each time (empty parents are
-    emitted again by each run's first call)."""
+    emitted again by each run's first call).  With run_left the slot epoch
+    wraps after the second reset (test aid)."""
     rng = np.random.default_rng(21)
     counts = rng.integers(0, 9, 4000).astype(np.int32)
     N = int(counts.sum())
@@ -189,7 +192,7 @@ def test_stream_reset_replays(ctx):
     waves = [(ids, rng.choice(np.array([0, 0, 1, 2], np.uint8), len(ids)),
               rng.integers(1, 200, len(ids)).astype(np.int64)) for ids in parts]
     _say("stream reset replays", [len(p) for p in parts])
-    got = _stream_case(ctx, counts, waves, B=100, runs=3)
+    got = _stream_case(ctx, counts, waves, B=100, runs=3, run_left=run_left)
     empties = set(np.flatnonzero(counts == 0).tolist())
     assert empties
     for r in range(3):

@@ -40,6 +40,7 @@ __device__ __forceinline__ int64_t parent_of(const uint32_t *__restrict__ cmap, 
     return upper_bound_g(offsets, lo, hi + 1, c) - 1;
 }
 
+template <bool kByMap>
 __global__ __launch_bounds__(kBlock) void k_batch(
     const uint32_t *__restrict__ queue, const uint8_t *__restrict__ keep, int64_t Q,
     const int64_t *__restrict__ offsets, int64_t P, const uint32_t *__restrict__ cmap, int64_t cmap_cap,
@@ -105,11 +106,14 @@ __global__ __launch_bounds__(kBlock) void k_batch(
                     bad_range = true;
                 } else if (want_tags || barrier) {
                     int64_t p;
-                    if (cpar != nullptr) p = (int64_t)cpar[c];
+                    if constexpr (kByMap) p = (int64_t)cpar[c];
                     else p = parent_of(cmap, nmap, offsets, P, c);
-                    par[k] = (uint32_t)p;
-                    ord[k] = (uint32_t)(c - offsets[p]);
-                    if (barrier && barrier[p]) kmask &= ~(1u << k);      // suppressed: takes no slot
+                    if (barrier && barrier[p]) {
+                        kmask &= ~(1u << k);                             // suppressed: takes no slot
+                    } else {
+                        par[k] = (uint32_t)p;
+                        ord[k] = (uint32_t)(c - offsets[p]);
+                    }
                 }
             }
         }
@@ -178,6 +182,7 @@ __device__ __forceinline__ void upper_bound_k(const int64_t *a, int64_t n, const
 // store instruction of a wave covers 256 contiguous bytes.
 constexpr int kAllPer = 4;
 
+template <bool kByMap>
 __global__ __launch_bounds__(kBlock) void k_batch_all(
     const uint32_t *__restrict__ queue, int64_t Q, const int64_t *__restrict__ offsets, int64_t P,
     const uint32_t *__restrict__ cmap, int64_t cmap_cap, int32_t B, uint32_t *__restrict__ out_child,
@@ -207,7 +212,7 @@ __global__ __launch_bounds__(kBlock) void k_batch_all(
         // lockstep search of the offsets (ids out of range search for N - 1
         // and are reported below)
         int64_t par[kAllPer];
-        if (want_tags && nmap == 0 && cpar == nullptr) {
+        if (!kByMap && want_tags && nmap == 0) {
             int64_t key[kAllPer];
 #pragma unroll
             for (int k = 0; k < kAllPer; ++k) key[k] = (int64_t)q[k] < N ? (int64_t)q[k] : N - 1;
@@ -229,8 +234,9 @@ __global__ __launch_bounds__(kBlock) void k_batch_all(
             if (i >= lim) continue;
             if (out_child) out_child[i] = q[k];
             if (want_tags) {
-                const int64_t p = cpar ? (int64_t)cpar[c]
-                                       : (nmap == 0 ? par[k] : parent_of(cmap, nmap, offsets, P, c));
+                int64_t p;
+                if constexpr (kByMap) p = (int64_t)cpar[c];
+                else p = nmap == 0 ? par[k] : parent_of(cmap, nmap, offsets, P, c);
                 if (out_parent) out_parent[i] = (uint32_t)p;
                 if (out_ordinal) out_ordinal[i] = (uint32_t)(c - offsets[p]);
             }
@@ -261,18 +267,28 @@ hipError_t launch_batch(const Launch &L, const uint32_t *queue, const uint8_t *k
     if (keep == nullptr && barrier == nullptr) {
         int64_t grid_a = (Q + kBlock * kAllPer - 1) / (kBlock * kAllPer);
         grid_a = grid_a < 1 ? 1 : (grid_a > (int64_t)L.num_cus * 8 ? (int64_t)L.num_cus * 8 : grid_a);
-        RO_LAUNCH(L, RO_K_BATCH, k_batch_all, dim3((unsigned)grid_a), dim3(kBlock), 0, L.stream, queue, Q,
-                  offsets, P, cmap, cmap_cap, B, out_child, out_parent, out_ordinal, out_cap, n_out, n_batches,
-                  cpar, cpar_n, L.ctl);
+        if (cpar)
+            RO_LAUNCH(L, RO_K_BATCH, k_batch_all<true>, dim3((unsigned)grid_a), dim3(kBlock), 0, L.stream, queue,
+                      Q, offsets, P, cmap, cmap_cap, B, out_child, out_parent, out_ordinal, out_cap, n_out,
+                      n_batches, cpar, cpar_n, L.ctl);
+        else
+            RO_LAUNCH(L, RO_K_BATCH, k_batch_all<false>, dim3((unsigned)grid_a), dim3(kBlock), 0, L.stream, queue,
+                      Q, offsets, P, cmap, cmap_cap, B, out_child, out_parent, out_ordinal, out_cap, n_out,
+                      n_batches, cpar, cpar_n, L.ctl);
         return hipGetLastError();
     }
     const int64_t ntiles = Q > 0 ? (Q + kTile - 1) / kTile : 1;
     const int64_t cap_grid = (int64_t)L.num_cus * 4;
     const int64_t grid = ntiles < cap_grid ? ntiles : cap_grid;
     const bool aligned = ((reinterpret_cast<uintptr_t>(queue) | reinterpret_cast<uintptr_t>(keep)) & 15u) == 0;
-    RO_LAUNCH(L, RO_K_BATCH, k_batch, dim3((unsigned)grid), dim3(kBlock), 0, L.stream, queue, keep, Q,
-              offsets, P, cmap, cmap_cap, B, out_child, out_parent, out_ordinal, out_cap, n_out, n_batches,
-              barrier, cpar, cpar_n, L.ctl, L.desc, L.desc_cap, ntiles, aligned ? 1 : 0);
+    if (cpar)
+        RO_LAUNCH(L, RO_K_BATCH, k_batch<true>, dim3((unsigned)grid), dim3(kBlock), 0, L.stream, queue, keep, Q,
+                  offsets, P, cmap, cmap_cap, B, out_child, out_parent, out_ordinal, out_cap, n_out, n_batches,
+                  barrier, cpar, cpar_n, L.ctl, L.desc, L.desc_cap, ntiles, aligned ? 1 : 0);
+    else
+        RO_LAUNCH(L, RO_K_BATCH, k_batch<false>, dim3((unsigned)grid), dim3(kBlock), 0, L.stream, queue, keep, Q,
+                  offsets, P, cmap, cmap_cap, B, out_child, out_parent, out_ordinal, out_cap, n_out, n_batches,
+                  barrier, cpar, cpar_n, L.ctl, L.desc, L.desc_cap, ntiles, aligned ? 1 : 0);
     return hipGetLastError();
 }
 

@@ -125,7 +125,8 @@ int ensure_desc(ro_ctx *c, int64_t tiles)
     c->desc = nullptr;
     c->desc_cap = 0;
     if (dev_alloc(&c->desc, tiles) != hipSuccess) return RO_EHIP;
-    if (hipMemset(c->desc, 0, (size_t)tiles * sizeof(uint64_t)) != hipSuccess) return RO_EHIP;
+    // zeroed on the context's stream: ordered before every later kernel on it
+    if (launch_zero_u64(launch_of(c), c->desc, tiles) != hipSuccess) return RO_EHIP;
     c->desc_cap = tiles;
     return RO_OK;
 }
@@ -145,7 +146,9 @@ int ensure_canon(ro_ctx *c, int64_t children)
     c->cmap_cap = 0;
     const int64_t n = children > 0 ? children : 1;
     if (dev_alloc(&c->canon, n) != hipSuccess) return RO_EHIP;
-    if (hipMemset(c->canon, 0, (size_t)n * sizeof(Canon)) != hipSuccess) return RO_EHIP;
+    if (launch_zero_u64(launch_of(c), reinterpret_cast<uint64_t *>(c->canon),
+                        n * (int64_t)(sizeof(Canon) / sizeof(uint64_t))) != hipSuccess)
+        return RO_EHIP;
     const int64_t subs = (n / kTile + 2) * (kTile / kSub);
     if (dev_alloc(&c->sub_base, subs) != hipSuccess) return RO_EHIP;
     const int64_t maps = (n >> 6) + 2;
@@ -168,7 +171,7 @@ int ensure_cnt(ro_ctx *c, int64_t parents)
     const int64_t n = parents > 0 ? parents : 1;
     if (dev_alloc(&c->cnt, 3 * n) != hipSuccess) return RO_EHIP;
     if (dev_alloc(&c->gkey, n) != hipSuccess) return RO_EHIP;
-    if (hipMemset(c->gkey, 0, (size_t)n * sizeof(uint64_t)) != hipSuccess) return RO_EHIP;
+    if (launch_zero_u64(launch_of(c), c->gkey, n) != hipSuccess) return RO_EHIP;
     c->cnt_cap = n;
     return RO_OK;
 }
@@ -587,7 +590,7 @@ int ro_stream_create(ro_ctx *c, const int64_t *offsets, int64_t n_parents, int64
         free(s);
         return RO_EHIP;
     }
-    if (hipMemset(block, 0, total) != hipSuccess) {
+    if (launch_zero_u64(launch_of(c), reinterpret_cast<uint64_t *>(block), (int64_t)(total / 8)) != hipSuccess) {
         (void)hipFree(block);
         free(s);
         return RO_EHIP;

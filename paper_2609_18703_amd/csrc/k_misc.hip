@@ -12,6 +12,12 @@ __global__ void k_ctl_init(Ctl *ctl)
     }
 }
 
+// Clears the error word (after the host has read it), in stream order.
+__global__ void k_clear_err(Ctl *ctl)
+{
+    if (threadIdx.x == 0) ctl->err = 0;
+}
+
 // Moves the canonical epoch forward (a test aid: slots of earlier epochs
 // read as unreported at any later epoch).
 __global__ void k_set_canon_epoch(Ctl *ctl, uint32_t e)
@@ -56,6 +62,12 @@ hipError_t launch_clear_tags(const Launch &L, Canon *canon, int64_t n)
 hipError_t launch_ctl_init(const Launch &L)
 {
     RO_LAUNCH(L, RO_K_MISC, k_ctl_init, dim3(1), dim3(64), 0, L.stream, L.ctl);
+    return hipGetLastError();
+}
+
+hipError_t launch_clear_err(const Launch &L)
+{
+    RO_LAUNCH(L, RO_K_MISC, k_clear_err, dim3(1), dim3(64), 0, L.stream, L.ctl);
     return hipGetLastError();
 }
 

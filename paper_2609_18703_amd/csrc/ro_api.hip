@@ -294,11 +294,10 @@ int ro_ctx_status(ro_ctx *c)
     if (hipStreamSynchronize(c->stream) != hipSuccess) return RO_EHIP;
     int32_t err = 0;
     if (hipMemcpy(&err, &c->ctl->err, sizeof(err), hipMemcpyDeviceToHost) != hipSuccess) return RO_EHIP;
-    if (err != 0) {
-        const int32_t zero = 0;
-        if (hipMemcpy(&c->ctl->err, &zero, sizeof(zero), hipMemcpyHostToDevice) != hipSuccess)
-            return RO_EHIP;
-    }
+    // cleared by a kernel on the context's stream, so that no later kernel of
+    // the context can see the old error (a host-to-device copy may still be
+    // in flight when it returns)
+    if (err != 0 && launch_clear_err(launch_of(c)) != hipSuccess) return RO_EHIP;
     return err;
 }
 

@@ -69,6 +69,7 @@ constexpr uint32_t kMaxCanonEpoch = (1u << 30) - 1;
 // Reset kernels the host enqueues when a device epoch is about to wrap.
 hipError_t launch_reset_canon(const Launch &L, Canon *canon, int64_t n);
 hipError_t launch_set_canon_epoch(const Launch &L, uint32_t e);
+hipError_t launch_clear_err(const Launch &L);
 hipError_t launch_ctl_init(const Launch &L);
 hipError_t launch_zero_u64(const Launch &L, uint64_t *p, int64_t n);
 hipError_t launch_clear_tags(const Launch &L, Canon *canon, int64_t n);

@@ -106,7 +106,9 @@ int ro_ctx_reserve(ro_ctx *ctx, int64_t max_children, int64_t max_parents, int64
  * device recorded (RO_OK if none). */
 int ro_ctx_status(ro_ctx *ctx);
 
-/* Free the context's workspace.  Waits for its stream first. */
+/* Free the context's workspace.  Waits for its stream first.  Destroy the
+ * context's Grain sets and streams before the context: their destroy calls
+ * wait on its stream. */
 int ro_ctx_destroy(ro_ctx *ctx);
 
 /* Per-kernel timing (measurement aid).  While enabled, every kernel the
@@ -244,6 +246,8 @@ enum { RO_WAITING = 0, RO_READY = 1, RO_IN_FLIGHT = 2, RO_SEALED = 3 };
 typedef struct ro_grains ro_grains;
 int ro_grains_create(ro_ctx *ctx, int64_t n_children, ro_grains **out);
 int ro_grains_reset(ro_ctx *ctx, ro_grains *g);
+/* Waits for the owning context's stream, then frees the Grain state (the
+ * context must still exist). */
 int ro_grains_destroy(ro_grains *g);
 
 /* Write every child's phase (RO_READY, RO_IN_FLIGHT or RO_SEALED) and
@@ -322,6 +326,8 @@ int ro_stream_emit(ro_ctx *ctx, ro_stream *s, uint32_t *emit_parent, int64_t *em
  * RO_EINVAL if s belongs to another context. */
 int ro_stream_reset(ro_ctx *ctx, ro_stream *s);
 
+/* Waits for the owning context's stream, then frees the stream state (the
+ * context must still exist). */
 int ro_stream_destroy(ro_stream *s);
 
 /* Test aid: move epochs forward so that their wrap-around paths run after a

@@ -145,14 +145,22 @@ int ensure_canon(ro_ctx *c, int64_t children)
     c->sub_cap = 0;
     c->cmap_cap = 0;
     const int64_t n = children > 0 ? children : 1;
-    if (dev_alloc(&c->canon, n) != hipSuccess) return RO_EHIP;
-    if (launch_zero_u64(launch_of(c), reinterpret_cast<uint64_t *>(c->canon),
-                        n * (int64_t)(sizeof(Canon) / sizeof(uint64_t))) != hipSuccess)
-        return RO_EHIP;
     const int64_t subs = (n / kTile + 2) * (kTile / kSub);
-    if (dev_alloc(&c->sub_base, subs) != hipSuccess) return RO_EHIP;
     const int64_t maps = (n >> 6) + 2;
-    if (dev_alloc(&c->cmap, maps) != hipSuccess) return RO_EHIP;
+    if (dev_alloc(&c->canon, n) != hipSuccess || dev_alloc(&c->sub_base, subs) != hipSuccess ||
+        dev_alloc(&c->cmap, maps) != hipSuccess ||
+        launch_zero_u64(launch_of(c), reinterpret_cast<uint64_t *>(c->canon),
+                        n * (int64_t)(sizeof(Canon) / sizeof(uint64_t))) != hipSuccess) {
+        // leave no partial workspace behind: the next call starts from none
+        (void)hipStreamSynchronize(c->stream);
+        (void)hipFree(c->canon);
+        (void)hipFree(c->sub_base);
+        (void)hipFree(c->cmap);
+        c->canon = nullptr;
+        c->sub_base = nullptr;
+        c->cmap = nullptr;
+        return RO_EHIP;
+    }
     c->canon_cap = n;
     c->sub_cap = subs;
     c->cmap_cap = maps;
@@ -169,9 +177,15 @@ int ensure_cnt(ro_ctx *c, int64_t parents)
     c->gkey = nullptr;
     c->cnt_cap = 0;
     const int64_t n = parents > 0 ? parents : 1;
-    if (dev_alloc(&c->cnt, 3 * n) != hipSuccess) return RO_EHIP;
-    if (dev_alloc(&c->gkey, n) != hipSuccess) return RO_EHIP;
-    if (launch_zero_u64(launch_of(c), c->gkey, n) != hipSuccess) return RO_EHIP;
+    if (dev_alloc(&c->cnt, 3 * n) != hipSuccess || dev_alloc(&c->gkey, n) != hipSuccess ||
+        launch_zero_u64(launch_of(c), c->gkey, n) != hipSuccess) {
+        (void)hipStreamSynchronize(c->stream);
+        (void)hipFree(c->cnt);
+        (void)hipFree(c->gkey);
+        c->cnt = nullptr;
+        c->gkey = nullptr;
+        return RO_EHIP;
+    }
     c->cnt_cap = n;
     return RO_OK;
 }
@@ -618,6 +632,7 @@ int ro_stream_create(ro_ctx *c, const int64_t *offsets, int64_t n_parents, int64
     st.gf_epoch = 0;
     if (launch_stream_init(launch_of(c), st) != hipSuccess ||
         launch_expand_tags(launch_of(c), offsets, P, st.cpar, nullptr, N) != hipSuccess) {
+        (void)hipStreamSynchronize(c->stream);     // a launch that did start still uses the block
         (void)hipFree(block);
         free(s);
         return RO_EHIP;

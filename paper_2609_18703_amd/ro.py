@@ -97,13 +97,20 @@ def load(path=None):
     return L
 
 
-def _ptr(t):
+def _ptr(t, item=None, n=0, name="array"):
+    """Device pointer of tensor t (None passes through).  The C side sees only
+    the pointer, so the element size (`item` bytes) and the length (at least
+    `n` elements) the call will use are checked here."""
     if t is None:
         return None
     if not t.is_cuda:
-        raise ValueError("ro arrays must live in GPU memory")
+        raise ValueError(f"ro {name} must live in GPU memory")
     if not t.is_contiguous():
-        raise ValueError("ro arrays must be contiguous")
+        raise ValueError(f"ro {name} must be contiguous")
+    if item is not None and t.element_size() != item:
+        raise TypeError(f"ro {name} needs {item}-byte elements, got {t.dtype}")
+    if t.numel() < n:
+        raise ValueError(f"ro {name} needs at least {n} elements, has {t.numel()}")
     return C.c_void_p(t.data_ptr())
 
 
@@ -113,8 +120,21 @@ def _check(rc, what):
 
 
 def _reports(parent, ordinal, state, off, data, n=None):
-    n = parent.numel() if n is None else n
-    return ReportsT(_ptr(parent), _ptr(ordinal), _ptr(state), _ptr(off), _ptr(data), n)
+    n = parent.numel() if n is None else int(n)
+    return ReportsT(_ptr(parent, 4, n, "report parents"), _ptr(ordinal, 4, n, "report ordinals"),
+                    _ptr(state, 1, n, "report states"), _ptr(off, 8, n + 1, "report offsets"),
+                    _ptr(data, 1, 0, "report bytes"), n)
+
+
+def _queue_args(queue, keep, q_len):
+    q_len = int(q_len)
+    return _ptr(queue, 4, q_len, "queue"), _ptr(keep, 1, q_len, "keep"), q_len
+
+
+def _tag_args(out_child, out_parent, out_ordinal, out_cap):
+    out_cap = int(out_cap)
+    return (_ptr(out_child, 4, out_cap, "out_child"), _ptr(out_parent, 4, out_cap, "out_parent"),
+            _ptr(out_ordinal, 4, out_cap, "out_ordinal"), out_cap)
 
 
 class Context:
@@ -169,8 +189,10 @@ class Context:
         cap = 0
         if child_parent is not None or child_ordinal is not None:
             cap = min(t.numel() for t in (child_parent, child_ordinal) if t is not None)
-        _check(self.L.ro_expand(self.h, _ptr(counts), counts.numel(), _ptr(offsets),
-                                _ptr(child_parent), _ptr(child_ordinal), cap), "ro_expand")
+        P = counts.numel()
+        _check(self.L.ro_expand(self.h, _ptr(counts, 4, P, "counts"), P, _ptr(offsets, 8, P + 1, "offsets"),
+                                _ptr(child_parent, 4, 0, "child_parent"), _ptr(child_ordinal, 4, 0, "child_ordinal"),
+                                cap), "ro_expand")
 
     def batch(self, queue, keep, offsets, batch_size, out_child=None, out_parent=None,
               out_ordinal=None, n_out=None, n_batches=None, q_len=None, out_cap=None, barrier=None):
@@ -178,9 +200,11 @@ class Context:
         if out_cap is None:
             outs = [t.numel() for t in (out_child, out_parent, out_ordinal) if t is not None]
             out_cap = min(outs) if outs else q_len
-        _check(self.L.ro_batch(self.h, _ptr(queue), _ptr(keep), q_len, _ptr(offsets),
-                               offsets.numel() - 1, int(batch_size), _ptr(out_child), _ptr(out_parent),
-                               _ptr(out_ordinal), int(out_cap), _ptr(n_out), _ptr(n_batches), _ptr(barrier)),
+        P = offsets.numel() - 1
+        _check(self.L.ro_batch(self.h, *_queue_args(queue, keep, q_len), _ptr(offsets, 8, 1, "offsets"), P,
+                               int(batch_size), *_tag_args(out_child, out_parent, out_ordinal, out_cap),
+                               _ptr(n_out, 8, 1, "n_out"), _ptr(n_batches, 8, 1, "n_batches"),
+                               _ptr(barrier, 1, P, "barrier")),
                "ro_batch")
 
     def batch_parent(self, queue, keep, offsets, batch_size, batch_off, out_child=None, out_parent=None,
@@ -190,10 +214,12 @@ class Context:
         if out_cap is None:
             outs = [t.numel() for t in (out_child, out_parent, out_ordinal) if t is not None]
             out_cap = min(outs) if outs else q_len
-        _check(self.L.ro_batch_parent(self.h, _ptr(queue), _ptr(keep), q_len, _ptr(offsets),
-                                      offsets.numel() - 1, int(batch_size), _ptr(out_child), _ptr(out_parent),
-                                      _ptr(out_ordinal), int(out_cap), _ptr(batch_off), batch_off.numel(),
-                                      _ptr(n_out), _ptr(n_batches), _ptr(barrier)),
+        P = offsets.numel() - 1
+        _check(self.L.ro_batch_parent(self.h, *_queue_args(queue, keep, q_len), _ptr(offsets, 8, 1, "offsets"), P,
+                                      int(batch_size), *_tag_args(out_child, out_parent, out_ordinal, out_cap),
+                                      _ptr(batch_off, 8, 1, "batch_off"), batch_off.numel(),
+                                      _ptr(n_out, 8, 1, "n_out"), _ptr(n_batches, 8, 1, "n_batches"),
+                                      _ptr(barrier, 1, P, "barrier")),
                "ro_batch_parent")
 
     def gather(self, parent, ordinal, state, off, data, offsets, out_off, out_data=None,
@@ -202,23 +228,29 @@ class Context:
         rep = _reports(parent, ordinal, state, off, data, n)
         if out_cap is None:
             out_cap = out_data.numel() if out_data is not None else 0
-        out = GatherOutT(_ptr(out_off), _ptr(out_data), int(out_cap), _ptr(n_success), _ptr(n_failed),
-                         _ptr(n_skipped), _ptr(complete), _ptr(parent_state), _ptr(child_dst_off),
-                         _ptr(barrier), _ptr(n_rejected))
-        _check(self.L.ro_gather(self.h, C.byref(rep), _ptr(offsets), offsets.numel() - 1, C.byref(out)),
+        P = offsets.numel() - 1
+        out = GatherOutT(_ptr(out_off, 8, P + 1, "out_off"), _ptr(out_data, 1, int(out_cap), "out_data"),
+                         int(out_cap), _ptr(n_success, 4, P, "n_success"), _ptr(n_failed, 4, P, "n_failed"),
+                         _ptr(n_skipped, 4, P, "n_skipped"), _ptr(complete, 1, P, "complete"),
+                         _ptr(parent_state, 1, P, "parent_state"), _ptr(child_dst_off, 8, 1, "child_dst_off"),
+                         _ptr(barrier, 1, P, "barrier"), _ptr(n_rejected, 8, 1, "n_rejected"))
+        _check(self.L.ro_gather(self.h, C.byref(rep), _ptr(offsets, 8, 1, "offsets"), P, C.byref(out)),
                "ro_gather")
 
     def filter(self, x_state, mask, out_state, mask_state=None, n=None):
-        n = x_state.numel() if n is None else n
-        _check(self.L.ro_filter(self.h, _ptr(x_state), _ptr(mask_state), _ptr(mask), int(n), _ptr(out_state)),
+        n = x_state.numel() if n is None else int(n)
+        _check(self.L.ro_filter(self.h, _ptr(x_state, 1, n, "x_state"), _ptr(mask_state, 1, n, "mask_state"),
+                                _ptr(mask, 1, n, "mask"), n, _ptr(out_state, 1, n, "out_state")),
                "ro_filter")
 
     def broadcast(self, maps, x_state, out_state, out_ancestor=None, like_state=None, n=None):
         """maps: device tensors, the descendant level's child->parent first."""
-        n = maps[0].numel() if n is None else n
-        arr = (C.c_void_p * len(maps))(*[m.data_ptr() for m in maps])
-        _check(self.L.ro_broadcast(self.h, C.cast(arr, C.c_void_p), len(maps), int(n), _ptr(x_state),
-                                   x_state.numel(), _ptr(like_state), _ptr(out_ancestor), _ptr(out_state)),
+        n = maps[0].numel() if n is None else int(n)
+        _ptr(maps[0], 4, n, "maps[0]")
+        arr = (C.c_void_p * len(maps))(*[_ptr(m, 4, 0, "map").value for m in maps])
+        _check(self.L.ro_broadcast(self.h, C.cast(arr, C.c_void_p), len(maps), n, _ptr(x_state, 1, 0, "x_state"),
+                                   x_state.numel(), _ptr(like_state, 1, n, "like_state"),
+                                   _ptr(out_ancestor, 4, n, "out_ancestor"), _ptr(out_state, 1, n, "out_state")),
                "ro_broadcast")
 
     def grains(self, n_children):
@@ -261,21 +293,25 @@ class Grains:
     def read(self, phase=None, generation=None):
         """Write every child's phase and generation into int32 device tensors
         of n_children entries (either may be None)."""
-        _check(self.ctx.L.ro_grains_read(self.ctx.h, self.h, _ptr(phase), _ptr(generation)), "ro_grains_read")
+        _check(self.ctx.L.ro_grains_read(self.ctx.h, self.h, _ptr(phase, 4, self.n, "phase"),
+                                         _ptr(generation, 4, self.n, "generation")), "ro_grains_read")
 
     def dispatch(self, child, out_generation=None, n=None):
-        n = child.numel() if n is None else n
-        _check(self.ctx.L.ro_grains_dispatch(self.ctx.h, self.h, _ptr(child), int(n), _ptr(out_generation)),
+        n = child.numel() if n is None else int(n)
+        _check(self.ctx.L.ro_grains_dispatch(self.ctx.h, self.h, _ptr(child, 4, n, "child"), n,
+                                             _ptr(out_generation, 4, n, "out_generation")),
                "ro_grains_dispatch")
 
     def retry(self, child, n=None):
-        n = child.numel() if n is None else n
-        _check(self.ctx.L.ro_grains_retry(self.ctx.h, self.h, _ptr(child), int(n)), "ro_grains_retry")
+        n = child.numel() if n is None else int(n)
+        _check(self.ctx.L.ro_grains_retry(self.ctx.h, self.h, _ptr(child, 4, n, "child"), n), "ro_grains_retry")
 
     def commit(self, parent, ordinal, state, off, data, generation, offsets, state_out, counts=None, n=None):
         rep = _reports(parent, ordinal, state, off, data, n)
-        _check(self.ctx.L.ro_grains_commit(self.ctx.h, self.h, C.byref(rep), _ptr(generation), _ptr(offsets),
-                                           offsets.numel() - 1, _ptr(state_out), _ptr(counts)), "ro_grains_commit")
+        _check(self.ctx.L.ro_grains_commit(self.ctx.h, self.h, C.byref(rep), _ptr(generation, 4, rep.n, "generation"),
+                                           _ptr(offsets, 8, 1, "offsets"), offsets.numel() - 1,
+                                           _ptr(state_out, 1, rep.n, "state_out"), _ptr(counts, 8, 4, "counts")),
+               "ro_grains_commit")
 
     def close(self):
         if getattr(self, "h", None):
@@ -297,8 +333,9 @@ class Stream:
         self.offsets = offsets
         self.barrier = barrier          # kept alive: the library holds it by reference
         h = C.c_void_p()
-        _check(ctx.L.ro_stream_create(ctx.h, _ptr(offsets), offsets.numel() - 1, int(n_children),
-                                      _ptr(barrier), C.byref(h)), "ro_stream_create")
+        P = offsets.numel() - 1
+        _check(ctx.L.ro_stream_create(ctx.h, _ptr(offsets, 8, 1, "offsets"), P, int(n_children),
+                                      _ptr(barrier, 1, P, "barrier"), C.byref(h)), "ro_stream_create")
         self.h = h
 
     def batch(self, queue, keep, batch_size, out_child=None, out_parent=None, out_ordinal=None, n_out=None,
@@ -308,14 +345,14 @@ class Stream:
         if out_cap is None:
             outs = [t.numel() for t in (out_child, out_parent, out_ordinal) if t is not None]
             out_cap = min(outs) if outs else q_len
-        _check(self.ctx.L.ro_stream_batch(self.ctx.h, self.h, _ptr(queue), _ptr(keep), q_len, int(batch_size),
-                                          _ptr(out_child), _ptr(out_parent), _ptr(out_ordinal), int(out_cap),
-                                          _ptr(n_out), _ptr(n_batches)),
+        _check(self.ctx.L.ro_stream_batch(self.ctx.h, self.h, *_queue_args(queue, keep, q_len), int(batch_size),
+                                          *_tag_args(out_child, out_parent, out_ordinal, out_cap),
+                                          _ptr(n_out, 8, 1, "n_out"), _ptr(n_batches, 8, 1, "n_batches")),
                "ro_stream_batch")
 
     def report(self, parent, ordinal, state, off, data, n=None, n_rejected=None):
         rep = _reports(parent, ordinal, state, off, data, n)
-        _check(self.ctx.L.ro_stream_report(self.ctx.h, self.h, C.byref(rep), _ptr(n_rejected)),
+        _check(self.ctx.L.ro_stream_report(self.ctx.h, self.h, C.byref(rep), _ptr(n_rejected, 8, 1, "n_rejected")),
                "ro_stream_report")
 
     def emit(self, emit_parent, emit_off, emit_data, n_success=None, n_failed=None, n_skipped=None,
@@ -324,10 +361,13 @@ class Stream:
             cap_parents = emit_off.numel() - 1
         if cap_bytes is None:
             cap_bytes = emit_data.numel() if emit_data is not None else 0
-        _check(self.ctx.L.ro_stream_emit(self.ctx.h, self.h, _ptr(emit_parent), _ptr(emit_off),
-                                         _ptr(emit_data), int(cap_parents), int(cap_bytes),
-                                         _ptr(n_success), _ptr(n_failed), _ptr(n_skipped),
-                                         _ptr(parent_state), _ptr(n_emitted), _ptr(n_bytes)),
+        cp, cb = int(cap_parents), int(cap_bytes)
+        _check(self.ctx.L.ro_stream_emit(self.ctx.h, self.h, _ptr(emit_parent, 4, cp, "emit_parent"),
+                                         _ptr(emit_off, 8, cp + 1, "emit_off"), _ptr(emit_data, 1, cb, "emit_data"),
+                                         cp, cb, _ptr(n_success, 4, cp, "n_success"),
+                                         _ptr(n_failed, 4, cp, "n_failed"), _ptr(n_skipped, 4, cp, "n_skipped"),
+                                         _ptr(parent_state, 1, cp, "parent_state"),
+                                         _ptr(n_emitted, 8, 1, "n_emitted"), _ptr(n_bytes, 8, 1, "n_bytes")),
                "ro_stream_emit")
 
     def reset(self):

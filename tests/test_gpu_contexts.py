@@ -68,3 +68,49 @@ def test_kernel_trace_counts_launches():
         G.compare_single(b, G.oracle_single(c))
     finally:
         ctx.close()
+
+
+def test_binding_rejects_wrong_element_size_and_short_arrays():
+    """The C calls see bare pointers, so the binding checks element sizes and
+    lengths before anything is launched; nothing reaches the device here."""
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_18703_amd as R
+    ctx = R.Context()
+    dev = "cuda"
+    try:
+        offs = torch.zeros(11, dtype=torch.int64, device=dev)
+        with pytest.raises(TypeError):
+            ctx.expand(torch.ones(10, dtype=torch.int64, device=dev), offs)       # counts are int32
+        with pytest.raises(ValueError):
+            ctx.expand(torch.ones(10, dtype=torch.int32, device=dev), offs[:10])  # offsets need P + 1
+        with pytest.raises(TypeError):
+            ctx.expand(torch.ones(10, dtype=torch.int32, device=dev), offs.to(torch.int32))
+        q = torch.zeros(8, dtype=torch.int32, device=dev)
+        tag = torch.zeros(4, dtype=torch.int32, device=dev)
+        with pytest.raises(ValueError):
+            ctx.batch(q, None, offs, 2, tag, q_len=8, out_cap=8)                     # out_child too short
+        with pytest.raises(ValueError):
+            ctx.batch(q, torch.ones(4, dtype=torch.uint8, device=dev), offs, 2, q)  # keep too short
+        with pytest.raises(ValueError):
+            ctx.batch(q, None, offs, 2, q, barrier=torch.zeros(3, dtype=torch.uint8, device=dev))
+        par = torch.zeros(5, dtype=torch.int32, device=dev)
+        st = torch.zeros(5, dtype=torch.uint8, device=dev)
+        off = torch.zeros(6, dtype=torch.int64, device=dev)
+        data = torch.zeros(16, dtype=torch.uint8, device=dev)
+        out_off = torch.zeros(11, dtype=torch.int64, device=dev)
+        with pytest.raises(ValueError):
+            ctx.gather(par, par, st, off[:5], data, offs, out_off)                   # report offsets need n + 1
+        with pytest.raises(TypeError):
+            ctx.gather(par, par, st.to(torch.int32), off, data, offs, out_off)      # states are bytes
+        with pytest.raises(ValueError):
+            ctx.gather(par, par, st, off, data, offs, out_off[:10])                 # out_off needs P + 1
+        with pytest.raises(ValueError):
+            ctx.gather(par, par, st, off, data, offs, out_off, data, out_cap=32)    # out_data under out_cap
+        with pytest.raises(ValueError):
+            ctx.filter(st, st[:4], st)
+        with pytest.raises(ValueError):
+            ctx.gather(par, par, st, off, data, offs.cpu(), out_off)                # host memory
+        ctx.check("nothing launched")
+    finally:
+        ctx.close()

@@ -45,7 +45,9 @@
  *     that call are unspecified; a gather or stream emission that follows a
  *     recorded error copies no bytes until the error is cleared.
  *   * Sizes.  Child ids are uint32, so an expansion may hold at most
- *     2^32 - 1 children (RO_EOVERFLOW otherwise).  Byte offsets are int64.
+ *     2^32 - 1 children (RO_EOVERFLOW otherwise).  Byte offsets are int64;
+ *     one record may hold at most 2^32 - 1 bytes (a slot keeps its length in
+ *     32 bits; a longer SUCCESS record is RO_EOVERFLOW).
  *   * Terminal states are uint8: RO_SUCCESS (Present), RO_FAILED (Failed, or
  *     Suppressed handed up from a lower level), RO_SKIPPED (Dropped) and
  *     RO_PENDING (no report yet).  A report may also carry RO_GROUP_FAILED,
@@ -76,7 +78,8 @@ enum {
     RO_ERANGE = -2,     /* parent >= P, ordinal >= k_p, or queued child id >= N        */
     RO_EDUP = -3,       /* a child reported twice (within a call or across waves)      */
     RO_ECAP = -4,       /* an output or the reserved workspace is too small            */
-    RO_EOVERFLOW = -5,  /* N >= 2^32 children, or byte totals beyond 2^45              */
+    RO_EOVERFLOW = -5,  /* N >= 2^32 children, a record of 2^32 bytes or more, or
+                           byte totals beyond 2^45                                     */
     RO_ESTATE = -6,     /* a state byte > RO_PENDING                                   */
     RO_EHIP = -7        /* a HIP runtime call failed                                   */
 };

@@ -25,6 +25,10 @@ untimed by the generator's device fill):
                 commit (with identical and conflicting repeats), retry of the
                 2% lost attempts, dispatch at generation 1, commit (with
                 stale generation-0 reports).
+  zipf-canonical zipf-single with every child ready in canonical order: the
+                reports and their records arrive in slot order, so the
+                gather reads sequentially (the path's best-case ordering,
+                for comparison with the random order of zipf-single).
 
 Prints one JSON line.  Children/s counts every child entity created at every
 level (pages + regions, clips + frames).
@@ -45,7 +49,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, published
 WORKLOADS = ("zipf-single", "docs-nested", "videos-nested", "stream-waves", "docs-ops", "zipf-fence",
-             "zipf-pbatch")
+             "zipf-pbatch", "zipf-canonical")
 
 
 def parse():
@@ -211,16 +215,20 @@ class Job:
         self.metric = metric or "children/sec through expand+batch+gather; achieved HBM GB/s vs peak"
 
 
-def stage_zipf(ctx, parents):
+def stage_zipf(ctx, parents, canonical=False):
+    """Workload 2.  With canonical=True every child becomes ready in canonical
+    order, so the reports (and their records) arrive in slot order and the
+    gather's reads are sequential: the same path at its best-case ordering."""
     import torch
     import workloads as W
     from workloads import device as D
     from paper_2609_18703_amd import pipeline as PL
-    c = W.config2(n_parents=parents or 100_000)
+    c = W.config2(n_parents=parents or 100_000, canonical_order=canonical)
     r = c.reports
     P, N, M = c.n_parents, c.n_children, c.n_dispatched
     S = int(r.off[-1])
-    log(f"[bench] zipf-single: P={P} N={N} dispatched={M} surviving bytes={S}")
+    name = "zipf-canonical" if canonical else "zipf-single"
+    log(f"[bench] {name}: P={P} N={N} dispatched={M} surviving bytes={S}")
     data = torch.empty(max(S, 1), dtype=torch.uint8, device="cuda")
     D.fill_records_dev(D.to_dev(r.seed), D.to_dev(r.off), data)
     b = PL.SingleLevelBuffers(
@@ -234,9 +242,10 @@ def stage_zipf(ctx, parents):
 
     cfg = {"workload": f"single-level Zipf(1.2) fan-out: {P} parents, counts truncated to [1,10000], "
                        f"{N} children, lognormal(6,1) records clipped to [16,4096] B, 3% failed, "
-                       f"2% skipped, random ready order, B={c.batch_size}, seed 1",
+                       f"2% skipped, {'canonical' if canonical else 'random'} ready order, "
+                       f"B={c.batch_size}, seed 1",
            "parents": P, "children": N, "dispatched": M, "surviving_bytes": S, "batch_size": c.batch_size}
-    return Job("zipf-single", lambda: PL.single_level(ctx, b), N, alg_single(P, N, M, S), cfg, check)
+    return Job(name, lambda: PL.single_level(ctx, b), N, alg_single(P, N, M, S), cfg, check)
 
 
 def stage_nested(ctx, which, parents):
@@ -533,8 +542,8 @@ def run(args):
 
     t0 = time.time()
     ctx = R.Context()
-    if args.workload == "zipf-single":
-        job = stage_zipf(ctx, args.parents)
+    if args.workload in ("zipf-single", "zipf-canonical"):
+        job = stage_zipf(ctx, args.parents, canonical=args.workload == "zipf-canonical")
     elif args.workload == "stream-waves":
         job = stage_stream(ctx, args.parents)
     elif args.workload == "docs-ops":
@@ -703,9 +712,9 @@ def cpu_baseline(workload):
     from workloads import device as D
 
     L = O.lib()
-    if workload == "zipf-single":
+    if workload in ("zipf-single", "zipf-canonical"):
         n_parents = 100_000
-        c = W.config2(n_parents=n_parents)
+        c = W.config2(n_parents=n_parents, canonical_order=workload == "zipf-canonical")
         r = c.reports
         S = int(r.off[-1])
         dev = torch.empty(max(S, 1), dtype=torch.uint8, device="cuda")

@@ -430,14 +430,24 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_
                 if (dend >= hi) break;
                 continue;                          // only empty children here
             }
+            // positions 64 at a time, stopping after the group that reaches
+            // the window's end: a small unit covers a few children, and the
+            // rest of the 256 are set empty without being read
+            bool past = false;
 #pragma unroll
             for (int k = 0; k < kSub / 64; ++k) {
                 const int i = k * 64 + lane;
                 const int64_t v = r0 + i;
+                if (past) {
+                    s_dst[i] = (int32_t)(we - ws);
+                    s_src[i] = 0;
+                    continue;
+                }
                 const int64_t d = v < V ? edst[v] : T;
                 const int64_t cs = min64(max64(d, ws), we);
                 s_dst[i] = (int32_t)(cs - ws);
                 s_src[i] = (v < V ? esrc[v] : 0) + (uint64_t)(cs - d);
+                past = __shfl(d, 63, 64) >= we;
             }
             if (lane == 0) s_dst[kSub] = (int32_t)(we - ws);
             __builtin_amdgcn_wave_barrier();

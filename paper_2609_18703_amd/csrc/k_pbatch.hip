@@ -23,7 +23,6 @@
 namespace ro {
 
 constexpr int kRTile = (int)kPbTile;         // sort tile: 8 entries per thread
-constexpr int kRRounds = kRTile / kBlock;
 constexpr int kRMaxBits = 9;                 // digit width; at most 512 buckets
 constexpr int kRMaxBuckets = 1 << kRMaxBits;
 constexpr int kRSpan = (int)kPbSpan;          // tiles per histogram column

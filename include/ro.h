@@ -36,7 +36,11 @@
  *     create/destroy calls, and a call that has to grow a workspace
  *     (hipMalloc): ro_ctx_reserve, a gather or batch beyond the reservation,
  *     the first ro_batch_parent of a larger queue, the first
- *     ro_grains_commit of a larger call.
+ *     ro_grains_commit of a larger call.  Outputs are ready once the
+ *     context's stream has drained: read them with work ordered after it
+ *     (a copy on the same stream, or after ro_ctx_status or a stream
+ *     synchronisation); a copy on another stream, including the null stream
+ *     when the context's stream is non-blocking, is not ordered with it.
  *   * Errors.  Errors found on the host (NULL where an array is required, a
  *     negative size, batch_size <= 0, a failing HIP call) are returned
  *     immediately and nothing is enqueued.  Errors that depend on device data

@@ -43,6 +43,8 @@ def synth():
 def to_dev(a, dtype=None):
     import torch
     a = np.ascontiguousarray(a)
+    if not a.flags.writeable:          # torch.from_numpy wants a writable array
+        a = a.copy()
     t = torch.from_numpy(a)
     if dtype is not None:
         t = t.to(dtype)

@@ -237,12 +237,16 @@ int ro_filter(ro_ctx *ctx, const uint8_t *x_state, const uint8_t *mask_state, co
  * a descendant Domain of n Items.  maps[0] is the descendant level's
  * child -> parent array (as ro_expand's child_parent), maps[1] the level
  * above, ..., `levels` arrays in all (1..8); the last index reached is the
- * ancestor (out_ancestor[d], may be NULL; >= n_ancestors is RO_ERANGE).
- * out_state[d] combines x_state[ancestor] with like_state[d] (the
- * descendant's own state, NULL = present) by the same precedence as
- * ro_filter.  `maps` is a host array of device pointers. */
-int ro_broadcast(ro_ctx *ctx, const uint32_t *const *maps, int32_t levels, int64_t n, const uint8_t *x_state,
-                 int64_t n_ancestors, const uint8_t *like_state, uint32_t *out_ancestor, uint8_t *out_state);
+ * ancestor (out_ancestor[d], may be NULL).  map_len[l] is the number of
+ * entries of maps[l] (map_len[0] >= n, RO_EINVAL otherwise); an index that
+ * falls outside the next map, or an ancestor >= n_ancestors, is RO_ERANGE
+ * (checked before it is used).  out_state[d] combines x_state[ancestor]
+ * with like_state[d] (the descendant's own state, NULL = present) by the
+ * same precedence as ro_filter.  `maps` and `map_len` are host arrays; the
+ * maps themselves are in device memory. */
+int ro_broadcast(ro_ctx *ctx, const uint32_t *const *maps, const int64_t *map_len, int32_t levels, int64_t n,
+                 const uint8_t *x_state, int64_t n_ancestors, const uint8_t *like_state, uint32_t *out_ancestor,
+                 uint8_t *out_state);
 
 /* Grain phases and the generation fence (Sec. 4, Eq. grain-phase and Eq.
  * generation-fence).  One Grain per child of an expansion: READY at

@@ -73,6 +73,7 @@ __global__ __launch_bounds__(kBlock) void k_filter(const uint8_t *__restrict__ x
 
 struct Maps {
     const uint32_t *m[kMaxBroadcastLevels];
+    int64_t len[kMaxBroadcastLevels];       // entries of each map
 };
 
 __global__ __launch_bounds__(kBlock) void k_broadcast(Maps maps, int32_t levels, int64_t n,
@@ -85,8 +86,15 @@ __global__ __launch_bounds__(kBlock) void k_broadcast(Maps maps, int32_t levels,
     int err = 0;
     for (int64_t d = g; d < n; d += stride) {
         uint32_t a = (uint32_t)d;
-        for (int32_t l = 0; l < levels; ++l) a = maps.m[l][a];
-        if ((int64_t)a >= n_anc) {
+        bool in_range = true;
+        for (int32_t l = 0; l < levels; ++l) {
+            if ((int64_t)a >= maps.len[l]) {
+                in_range = false;
+                break;
+            }
+            a = maps.m[l][a];
+        }
+        if (!in_range || (int64_t)a >= n_anc) {
             err = RO_ERANGE;
             continue;
         }
@@ -113,11 +121,15 @@ hipError_t launch_filter(const Launch &L, const uint8_t *xs, const uint8_t *ms, 
     return hipGetLastError();
 }
 
-hipError_t launch_broadcast(const Launch &L, const uint32_t *const *maps, int32_t levels, int64_t n,
-                            const uint8_t *xs, int64_t n_anc, const uint8_t *ls, uint32_t *anc, uint8_t *out)
+hipError_t launch_broadcast(const Launch &L, const uint32_t *const *maps, const int64_t *map_len, int32_t levels,
+                            int64_t n, const uint8_t *xs, int64_t n_anc, const uint8_t *ls, uint32_t *anc,
+                            uint8_t *out)
 {
     Maps m{};
-    for (int32_t l = 0; l < levels; ++l) m.m[l] = maps[l];
+    for (int32_t l = 0; l < levels; ++l) {
+        m.m[l] = maps[l];
+        m.len[l] = map_len[l];
+    }
     int64_t grid = (n + kBlock - 1) / kBlock;
     grid = grid < 1 ? 1 : (grid > (int64_t)L.num_cus * 8 ? (int64_t)L.num_cus * 8 : grid);
     RO_LAUNCH(L, RO_K_BROADCAST, k_broadcast, dim3((unsigned)grid), dim3(kBlock), 0, L.stream, m, levels, n, xs, n_anc,

@@ -461,16 +461,18 @@ int ro_filter(ro_ctx *c, const uint8_t *x_state, const uint8_t *mask_state, cons
     return hip_fail(launch_filter(launch_of(c), x_state, mask_state, mask, n, out_state));
 }
 
-int ro_broadcast(ro_ctx *c, const uint32_t *const *maps, int32_t levels, int64_t n, const uint8_t *x_state,
-                 int64_t n_ancestors, const uint8_t *like_state, uint32_t *out_ancestor, uint8_t *out_state)
+int ro_broadcast(ro_ctx *c, const uint32_t *const *maps, const int64_t *map_len, int32_t levels, int64_t n,
+                 const uint8_t *x_state, int64_t n_ancestors, const uint8_t *like_state, uint32_t *out_ancestor,
+                 uint8_t *out_state)
 {
     if (!c || n < 0 || n_ancestors < 0 || levels < 1 || levels > kMaxBroadcastLevels) return RO_EINVAL;
-    if (n > 0 && (!maps || !x_state || !out_state)) return RO_EINVAL;
+    if (n > 0 && (!maps || !map_len || !x_state || !out_state)) return RO_EINVAL;
     for (int32_t l = 0; n > 0 && l < levels; ++l)
-        if (!maps[l]) return RO_EINVAL;
+        if (!maps[l] || map_len[l] < 0) return RO_EINVAL;
     if (n == 0) return RO_OK;
-    return hip_fail(launch_broadcast(launch_of(c), maps, levels, n, x_state, n_ancestors, like_state, out_ancestor,
-                                     out_state));
+    if (map_len[0] < n) return RO_EINVAL;
+    return hip_fail(launch_broadcast(launch_of(c), maps, map_len, levels, n, x_state, n_ancestors, like_state,
+                                     out_ancestor, out_state));
 }
 
 int ro_grains_create(ro_ctx *c, int64_t n_children, ro_grains **out)

@@ -168,8 +168,9 @@ hipError_t launch_grains_zero_tags(const Launch &L, uint32_t *tag, int64_t n);
 constexpr int kMaxBroadcastLevels = 8;
 hipError_t launch_filter(const Launch &L, const uint8_t *xs, const uint8_t *ms, const uint8_t *mv, int64_t n,
                          uint8_t *out);
-hipError_t launch_broadcast(const Launch &L, const uint32_t *const *maps, int32_t levels, int64_t n,
-                            const uint8_t *xs, int64_t n_anc, const uint8_t *ls, uint32_t *anc, uint8_t *out);
+hipError_t launch_broadcast(const Launch &L, const uint32_t *const *maps, const int64_t *map_len, int32_t levels,
+                            int64_t n, const uint8_t *xs, int64_t n_anc, const uint8_t *ls, uint32_t *anc,
+                            uint8_t *out);
 
 // streaming
 struct StreamState {

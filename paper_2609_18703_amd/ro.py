@@ -82,7 +82,7 @@ def load(path=None):
     L.ro_grains_dispatch.argtypes = [P, P, P, i64, P]
     L.ro_grains_retry.argtypes = [P, P, P, i64]
     L.ro_grains_commit.argtypes = [P, P, C.POINTER(ReportsT), P, P, i64, P, P]
-    L.ro_broadcast.argtypes = [P, P, i32, i64, P, i64, P, P, P]
+    L.ro_broadcast.argtypes = [P, P, P, i32, i64, P, i64, P, P, P]
     L.ro_stream_destroy.argtypes = [P]
     L.ro_ctx_trace.argtypes = [P, C.c_int]
     L.ro_ctx_trace_read.argtypes = [P, P, P, i32]
@@ -248,7 +248,9 @@ class Context:
         n = maps[0].numel() if n is None else int(n)
         _ptr(maps[0], 4, n, "maps[0]")
         arr = (C.c_void_p * len(maps))(*[_ptr(m, 4, 0, "map").value for m in maps])
-        _check(self.L.ro_broadcast(self.h, C.cast(arr, C.c_void_p), len(maps), n, _ptr(x_state, 1, 0, "x_state"),
+        lens = (C.c_int64 * len(maps))(*[m.numel() for m in maps])
+        _check(self.L.ro_broadcast(self.h, C.cast(arr, C.c_void_p), C.cast(lens, C.c_void_p), len(maps), n,
+                                   _ptr(x_state, 1, 0, "x_state"),
                                    x_state.numel(), _ptr(like_state, 1, n, "like_state"),
                                    _ptr(out_ancestor, 4, n, "out_ancestor"), _ptr(out_state, 1, n, "out_state")),
                "ro_broadcast")

@@ -412,7 +412,8 @@ static void case_filter_broadcast(ro_ctx *ctx, int64_t P)
     up(d_m1, up1.cp, (size_t)up1.N * 4);
     const uint32_t *dmaps[2] = {d_m0, d_m1};
     const uint32_t *hmaps[2] = {up2.cp, up1.cp};
-    RO_OK_(ro_broadcast(ctx, dmaps, 2, n, d_top, P, d_xs, d_anc, d_out));
+    const int64_t lens[2] = {n, up1.N};
+    RO_OK_(ro_broadcast(ctx, dmaps, lens, 2, n, d_top, P, d_xs, d_anc, d_out));
     EXPECT(ro_ctx_status(ctx) == RO_OK, "broadcast status");
     uint32_t *w_anc = xmalloc((size_t)n * 4), *g_anc = xmalloc((size_t)n * 4);
     if (oracle_broadcast(hmaps, 2, n, top, P, xs, w_anc, w) != 0) exit(4);

@@ -101,3 +101,45 @@ def test_broadcast_documents_to_regions(ctx):
     ctx.check("broadcast documents")
     assert np.array_equal(d_anc.cpu().numpy().view(np.uint32), anc)
     assert np.array_equal(d_st.cpu().numpy(), st)
+
+
+@pytest.mark.parametrize("like", [True, False])
+def test_broadcast_eight_levels(ctx, like):
+    """The deepest broadcast the library takes (8 composed maps), with and
+    without the descendant's own state, and without the ancestor output."""
+    rng = np.random.default_rng(8 + like)
+    counts = [rng.integers(1, 4, 5).astype(np.int32)]
+    maps = []
+    for _ in range(8):
+        offs, cp, _ = O.expand(counts[-1])
+        maps.insert(0, cp)
+        counts.append(rng.integers(0, 4, int(offs[-1])).astype(np.int32))
+    n = len(maps[0])
+    x = rng.choice(STATES, len(counts[0]))
+    ls = rng.choice(STATES, n) if like else None
+    anc, st = O.broadcast(maps, x, ls)
+    d_st = torch.zeros(max(n, 1), dtype=torch.uint8, device="cuda")
+    _say("broadcast 8 levels, n", n, "like", like)
+    ctx.broadcast([D.to_dev(m.view(np.int32)) for m in maps], D.to_dev(x), d_st, None,
+                  D.to_dev(ls) if like else None)
+    ctx.check("broadcast 8 levels")
+    assert np.array_equal(d_st.cpu().numpy()[:n], st)
+
+
+def test_broadcast_errors(ctx):
+    import paper_2609_18703_amd as R
+    m = D.to_dev(np.array([0, 1, 1, 2], np.int32))
+    x = D.to_dev(np.array([0, 0, 1], np.uint8))
+    out = torch.zeros(4, dtype=torch.uint8, device="cuda")
+    with pytest.raises(R.RoError) as e:                          # more than 8 levels, refused on the host
+        ctx.broadcast([m] * 9, x, out)
+    assert e.value.code == O.EINVAL
+    ctx.broadcast([m], D.to_dev(np.array([0, 0], np.uint8)), out)    # ancestor 2 of 2 ancestors
+    assert ctx.status() == O.ERANGE
+    # an intermediate index past the next map's end is refused before it is read
+    short = D.to_dev(np.array([0, 0], np.int32))
+    ctx.broadcast([m, short], x, out)
+    assert ctx.status() == O.ERANGE
+    ctx.broadcast([m], x, out)
+    ctx.check("after the range error")
+    assert np.array_equal(out.cpu().numpy(), np.array([0, 0, 0, 1], np.uint8))

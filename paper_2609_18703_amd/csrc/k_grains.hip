@@ -159,6 +159,7 @@ __global__ __launch_bounds__(kBlock) void k_grains_first(
             const int64_t o = offsets[p];
             if ((int64_t)ro_[i] >= offsets[p + 1] - o) { err = RO_ERANGE; continue; }
             const int64_t ch = o + (int64_t)ro_[i];
+            if (o < 0) { err = RO_EINVAL; continue; }      // offsets not an Expansion
             if (ch >= N) { err = RO_ERANGE; continue; }
             c[k] = ch;
             s[k] = st;

@@ -473,7 +473,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_
                 }
                 if (lane == 0) s_dst[kSub] = (int32_t)(we - ws);
                 __builtin_amdgcn_wave_barrier();
-                copy_window32(s_dst, s_src, (int)(we - ws), outa, D0 + ws, lane);
+                copy_window32_x2(s_dst, s_src, (int)(we - ws), outa, D0 + ws, lane);
                 __builtin_amdgcn_wave_barrier();
             }
         }

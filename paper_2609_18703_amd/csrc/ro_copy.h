@@ -164,6 +164,79 @@ __device__ __forceinline__ void copy_window32(const int32_t *s_dst, const uint64
     }
 }
 
+// copy_window32 with two chunks per lane and step (the lane's chunk and the
+// one 1 KiB further), the first pieces of both in flight together: twice
+// the loads outstanding per wave for the same registers' occupancy.  Used
+// where a unit's window spans many KiB (the gather); small windows keep the
+// one-chunk loop.
+// The rest of one chunk after its first piece has been loaded: the pieces of
+// any further records it holds, the merge and the store.
+__device__ __forceinline__ void copy_one_chunk(const int32_t *s_dst, const uint64_t *s_src, int tot, uint64_t outa,
+                                               int64_t D0, int x, int lo, int hi, int &r, const Piece &p, int e1)
+{
+    uint4 acc = make_uint4(0u, 0u, 0u, 0u);
+    if (e1 < hi) {
+        int q = advance_record(s_dst, r, e1);
+        int e = e1;
+        while (e < hi) {
+            const int dq = s_dst[q + 1];
+            const int e2 = hi < dq ? hi : dq;
+            Piece pq;
+            piece_load(pq, s_src[q] + (uint64_t)(int64_t)(x - s_dst[q]), e - x, e2 - 1 - x);
+            piece_merge(acc, pq);
+            e = e2;
+            if (e < hi) q = advance_record(s_dst, q, e);
+        }
+        r = q;
+    }
+    piece_merge(acc, p);
+    const uint64_t A = outa + (uint64_t)(D0 + x);
+    if (lo == x && hi == x + 16) st16(A, acc);
+    else store_partial(A, acc, lo - x, hi - x);
+}
+
+__device__ __forceinline__ void copy_window32_x2(const int32_t *s_dst, const uint64_t *s_src, int tot,
+                                                 uint64_t outa, int64_t D0, int lane)
+{
+    const uint64_t a0 = (outa + (uint64_t)D0) & ~(uint64_t)15;
+    const uint64_t a1 = (outa + (uint64_t)(D0 + tot) - 1) & ~(uint64_t)15;
+    const int nchunks = (int)((a1 - a0) >> 4) + 1;
+    const int xbase = (int)((int64_t)(a0 - outa) - D0);     // -15..0
+    int r = 0;
+    for (int ch = lane; ch < nchunks; ch += 128) {
+        // two chunks 1 KiB apart, the first pieces of both loaded together
+        const int xA = xbase + ch * 16;
+        const int loA = xA > 0 ? xA : 0;
+        const int hiA = xA + 16 < tot ? xA + 16 : tot;
+        r = advance_record(s_dst, r, loA);
+        int rA = r;
+        const int d1A = s_dst[rA + 1];
+        const int e1A = hiA < d1A ? hiA : d1A;
+        Piece pA;
+        piece_load(pA, s_src[rA] + (uint64_t)(int64_t)(xA - s_dst[rA]), loA - xA, e1A - 1 - xA);
+        const bool two = ch + 64 < nchunks;
+        const int xB = xA + 1024;
+        const int loB = xB;
+        const int hiB = xB + 16 < tot ? xB + 16 : tot;
+        int rB = r;
+        int e1B = hiB;
+        Piece pB;
+        if (two) {
+            rB = advance_record(s_dst, r, loB);
+            const int d1B = s_dst[rB + 1];
+            e1B = hiB < d1B ? hiB : d1B;
+            piece_load(pB, s_src[rB] + (uint64_t)(int64_t)(xB - s_dst[rB]), loB - xB, e1B - 1 - xB);
+        }
+        copy_one_chunk(s_dst, s_src, tot, outa, D0, xA, loA, hiA, rA, pA, e1A);
+        if (two) {
+            copy_one_chunk(s_dst, s_src, tot, outa, D0, xB, loB, hiB, rB, pB, e1B);
+            r = rB;
+        } else {
+            r = rA;
+        }
+    }
+}
+
 // Output bytes are split into units of G bytes (the last one shorter), cut
 // where the destination address is 16-byte aligned, so that unit edges need
 // no partial stores.  G is chosen from the total so that every wave of the

@@ -68,6 +68,7 @@ hipError_t launch_gf_fold(const Launch &L, const uint8_t *rs, const uint32_t *rp
 }
 
 // ---------------------------------------------------------------- scatter
+constexpr int kScatterItems = 2;            // reports per thread and step
 // With a group-failure barrier, reports commit in report order: one of a
 // barred parent, or one after its parent's first group failure in this
 // call, is rejected; an accepted group failure is a failed member.
@@ -98,30 +99,56 @@ __global__ __launch_bounds__(kBlock) void k_gather_scatter(
         if (offsets[p + 1] < offsets[p]) err = RO_EINVAL;
     }
     int64_t cnt = 0, rej = 0;
-    for (int64_t i = gtid; i < n; i += gstride) {
-        uint32_t s = rs[i];
-        const int64_t o0 = roff[i], o1 = roff[i + 1];
-        if (o1 < o0) { err = RO_EINVAL; continue; }
-        if (s > RO_PENDING && !(s == RO_GROUP_FAILED && barrier)) { err = RO_ESTATE; continue; }
-        if (s == RO_PENDING) continue;
-        const uint32_t p = rp[i];
-        if ((int64_t)p >= P) { err = RO_ERANGE; continue; }
-        const int64_t st = offsets[p];
-        const uint32_t o = ro_[i];
-        if ((int64_t)o >= offsets[p + 1] - st) { err = RO_ERANGE; continue; }
-        const int64_t c = st + (int64_t)o;
-        if (st < 0 || c >= N) { err = RO_EINVAL; continue; }     // offsets not an Expansion
-        const int64_t len = s == RO_SUCCESS ? o1 - o0 : 0;
-        if (len >= ((int64_t)1 << 32)) { err = RO_EOVERFLOW; continue; }
-        if (gf_rejected(barrier, gkey, epoch, p, i)) { ++rej; continue; }
-        if (s == RO_GROUP_FAILED) s = RO_FAILED;
-        ++cnt;
-        if (cap_ok) {
-            Canon e;
-            e.src = reinterpret_cast<uint64_t>(data) + (uint64_t)o0;
-            e.len = (uint32_t)len;
-            e.tag = (epoch << 2) | s;
-            canon[c] = e;
+    constexpr int U = kScatterItems;
+    // U reports per thread and step, their loads and lookups all in flight
+    // before any is validated or stored
+    for (int64_t b = gtid; b < n; b += U * gstride) {
+        uint32_t sv[U], pv[U], ov[U];
+        int64_t o0v[U], o1v[U], stv[U], env[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const int64_t i = b + k * gstride;
+            const bool in = i < n;
+            sv[k] = in ? rs[i] : RO_PENDING;
+            pv[k] = in ? rp[i] : 0xffffffffu;
+            ov[k] = in ? ro_[i] : 0u;
+            o0v[k] = in ? roff[i] : 0;
+            o1v[k] = in ? roff[i + 1] : 0;
+        }
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const bool ok = (int64_t)pv[k] < P;
+            stv[k] = ok ? offsets[pv[k]] : 0;
+            env[k] = ok ? offsets[pv[k] + 1] : 0;
+        }
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const int64_t i = b + k * gstride;
+            if (i >= n) continue;
+            uint32_t s = sv[k];
+            const int64_t o0 = o0v[k], o1 = o1v[k];
+            if (o1 < o0) { err = RO_EINVAL; continue; }
+            if (s > RO_PENDING && !(s == RO_GROUP_FAILED && barrier)) { err = RO_ESTATE; continue; }
+            if (s == RO_PENDING) continue;
+            const uint32_t p = pv[k];
+            if ((int64_t)p >= P) { err = RO_ERANGE; continue; }
+            const int64_t st = stv[k];
+            const uint32_t o = ov[k];
+            if ((int64_t)o >= env[k] - st) { err = RO_ERANGE; continue; }
+            const int64_t c = st + (int64_t)o;
+            if (st < 0 || c >= N) { err = RO_EINVAL; continue; }
+            const int64_t len = s == RO_SUCCESS ? o1 - o0 : 0;
+            if (len >= ((int64_t)1 << 32)) { err = RO_EOVERFLOW; continue; }
+            if (gf_rejected(barrier, gkey, epoch, p, i)) { ++rej; continue; }
+            if (s == RO_GROUP_FAILED) s = RO_FAILED;
+            ++cnt;
+            if (cap_ok) {
+                Canon e;
+                e.src = reinterpret_cast<uint64_t>(data) + (uint64_t)o0;
+                e.len = (uint32_t)len;
+                e.tag = (epoch << 2) | s;
+                canon[c] = e;
+            }
         }
     }
     if (err) raise_err(ctl, err);

@@ -66,13 +66,22 @@ __global__ __launch_bounds__(kBlock) void k_expand_tags(const int64_t *__restric
                                                         uint32_t *__restrict__ child_ordinal,
                                                         int64_t child_cap, int vec_ok)
 {
+    constexpr int kWaveSpan = 64 * kItems;            // children per wave and step
+    __shared__ alignas(16) uint32_t s_stage[kBlock / 64][kWaveSpan];
     const int64_t N = offsets[P];
     if (N > child_cap || N >= ((int64_t)1 << 32)) return;     // reported by the scan
-    const int64_t nthreads = (N + kItems - 1) / kItems;
-    for (int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x; g < nthreads;
-         g += (int64_t)gridDim.x * kBlock) {
-        const int64_t c0 = g * kItems;
-        int64_t p = upper_bound_g(offsets, 0, P + 1, c0) - 1;
+    const int lane = lane_id();
+    uint32_t *stage = s_stage[threadIdx.x >> 6];
+    const int64_t nwaves = (int64_t)gridDim.x * (kBlock / 64);
+    for (int64_t wt = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6); wt * kWaveSpan < N; wt += nwaves) {
+        // the wave's parent range by two wave-wide searches, then each lane's
+        // first parent by a search inside that range
+        const int64_t cb = wt * kWaveSpan;
+        const int64_t ce = cb + kWaveSpan < N ? cb + kWaveSpan : N;
+        const int64_t pf = wave_last_le(offsets, 0, P + 1, cb);
+        const int64_t pl = wave_last_le(offsets, 0, P + 1, ce - 1);
+        const int64_t c0 = cb + (int64_t)lane * kItems;
+        int64_t p = c0 < N ? upper_bound_g(offsets, pf, pl + 1, c0) - 1 : pl;
         int64_t start = offsets[p];
         int64_t next = offsets[p + 1];
         uint32_t par[kItems], ord[kItems];
@@ -87,18 +96,23 @@ __global__ __launch_bounds__(kBlock) void k_expand_tags(const int64_t *__restric
             par[k] = (uint32_t)p;
             ord[k] = (uint32_t)(c - start);
         }
-        if (vec_ok && c0 + kItems <= N) {
-            if (child_parent) {
-                uint4 *dp = reinterpret_cast<uint4 *>(child_parent + c0);
+        if (vec_ok && ce - cb == kWaveSpan) {
+            // staged in LDS, then written 1 KiB per store instruction
+#pragma unroll 1
+            for (int which = 0; which < 2; ++which) {
+                uint32_t *dst = which == 0 ? child_parent : child_ordinal;
+                if (dst == nullptr) continue;
+                const uint32_t *v = which == 0 ? par : ord;
 #pragma unroll
                 for (int k = 0; k < kItems / 4; ++k)
-                    dp[k] = make_uint4(par[4 * k], par[4 * k + 1], par[4 * k + 2], par[4 * k + 3]);
-            }
-            if (child_ordinal) {
-                uint4 *dp = reinterpret_cast<uint4 *>(child_ordinal + c0);
+                    *reinterpret_cast<uint4 *>(&stage[lane * kItems + 4 * k]) =
+                        make_uint4(v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]);
+                __builtin_amdgcn_wave_barrier();
+                uint4 *out = reinterpret_cast<uint4 *>(dst + cb);
 #pragma unroll
                 for (int k = 0; k < kItems / 4; ++k)
-                    dp[k] = make_uint4(ord[4 * k], ord[4 * k + 1], ord[4 * k + 2], ord[4 * k + 3]);
+                    out[k * 64 + lane] = *reinterpret_cast<const uint4 *>(&stage[(k * 64 + lane) * 4]);
+                __builtin_amdgcn_wave_barrier();
             }
         } else {
 #pragma unroll

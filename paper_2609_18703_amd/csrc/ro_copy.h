@@ -118,6 +118,34 @@ __device__ __forceinline__ void store_partial(uint64_t A, const uint4 &v, int b0
     for (int b = b0; b < b1; ++b) st8(A + (uint64_t)b, (uint8_t)(dword_of(v, b >> 2) >> (8 * (b & 3))));
 }
 
+// The rest of one chunk at x (output bytes [lo, hi) of the window) once the
+// piece of its first record r has been loaded: the pieces of any further
+// records it holds, the merge and the store.  r moves to the chunk's last
+// record.
+__device__ __forceinline__ void copy_one_chunk(const int32_t *s_dst, const uint64_t *s_src, uint64_t outa, int64_t D0,
+                                               int x, int lo, int hi, int &r, const Piece &p, int e1)
+{
+    uint4 acc = make_uint4(0u, 0u, 0u, 0u);
+    if (e1 < hi) {
+        int q = advance_record(s_dst, r, e1);
+        int e = e1;
+        while (e < hi) {
+            const int dq = s_dst[q + 1];
+            const int e2 = hi < dq ? hi : dq;
+            Piece pq;
+            piece_load(pq, s_src[q] + (uint64_t)(int64_t)(x - s_dst[q]), e - x, e2 - 1 - x);
+            piece_merge(acc, pq);
+            e = e2;
+            if (e < hi) q = advance_record(s_dst, q, e);
+        }
+        r = q;
+    }
+    piece_merge(acc, p);
+    const uint64_t A = outa + (uint64_t)(D0 + x);
+    if (lo == x && hi == x + 16) st16(A, acc);
+    else store_partial(A, acc, lo - x, hi - x);     // first or last chunk of the window
+}
+
 // One unit's window of a sub-tile (at most 1 GiB): positions relative to the
 // window start fit in 32 bits.  The wave sweeps its window 1 KiB at a time,
 // lane `lane` taking chunk 64*g + lane, so the record each lane reads from
@@ -141,60 +169,14 @@ __device__ __forceinline__ void copy_window32(const int32_t *s_dst, const uint64
         const int e1 = hi < d1 ? hi : d1;
         Piece p;
         piece_load(p, s_src[r] + (uint64_t)(int64_t)(x - s_dst[r]), lo - x, e1 - 1 - x);
-        uint4 acc = make_uint4(0u, 0u, 0u, 0u);
-        if (e1 < hi) {
-            // the chunk also holds the start of the next record(s)
-            int q = advance_record(s_dst, r, e1);
-            int e = e1;
-            while (e < hi) {
-                const int dq = s_dst[q + 1];
-                const int e2 = hi < dq ? hi : dq;
-                Piece pq;
-                piece_load(pq, s_src[q] + (uint64_t)(int64_t)(x - s_dst[q]), e - x, e2 - 1 - x);
-                piece_merge(acc, pq);
-                e = e2;
-                if (e < hi) q = advance_record(s_dst, q, e);
-            }
-            r = q;
-        }
-        piece_merge(acc, p);
-        const uint64_t A = outa + (uint64_t)(D0 + x);
-        if (lo == x && hi == x + 16) st16(A, acc);
-        else store_partial(A, acc, lo - x, hi - x);     // first or last chunk of the window
+        copy_one_chunk(s_dst, s_src, outa, D0, x, lo, hi, r, p, e1);
     }
 }
 
 // copy_window32 with two chunks per lane and step (the lane's chunk and the
 // one 1 KiB further), the first pieces of both in flight together: twice
-// the loads outstanding per wave for the same registers' occupancy.  Used
-// where a unit's window spans many KiB (the gather); small windows keep the
-// one-chunk loop.
-// The rest of one chunk after its first piece has been loaded: the pieces of
-// any further records it holds, the merge and the store.
-__device__ __forceinline__ void copy_one_chunk(const int32_t *s_dst, const uint64_t *s_src, int tot, uint64_t outa,
-                                               int64_t D0, int x, int lo, int hi, int &r, const Piece &p, int e1)
-{
-    uint4 acc = make_uint4(0u, 0u, 0u, 0u);
-    if (e1 < hi) {
-        int q = advance_record(s_dst, r, e1);
-        int e = e1;
-        while (e < hi) {
-            const int dq = s_dst[q + 1];
-            const int e2 = hi < dq ? hi : dq;
-            Piece pq;
-            piece_load(pq, s_src[q] + (uint64_t)(int64_t)(x - s_dst[q]), e - x, e2 - 1 - x);
-            piece_merge(acc, pq);
-            e = e2;
-            if (e < hi) q = advance_record(s_dst, q, e);
-        }
-        r = q;
-    }
-    piece_merge(acc, p);
-    const uint64_t A = outa + (uint64_t)(D0 + x);
-    if (lo == x && hi == x + 16) st16(A, acc);
-    else store_partial(A, acc, lo - x, hi - x);
-}
-
+// the loads outstanding per wave at the same occupancy.  Used where a unit's
+// window spans many KiB (the gather); small windows keep the one-chunk loop.
 __device__ __forceinline__ void copy_window32_x2(const int32_t *s_dst, const uint64_t *s_src, int tot,
                                                  uint64_t outa, int64_t D0, int lane)
 {
@@ -227,9 +209,9 @@ __device__ __forceinline__ void copy_window32_x2(const int32_t *s_dst, const uin
             e1B = hiB < d1B ? hiB : d1B;
             piece_load(pB, s_src[rB] + (uint64_t)(int64_t)(xB - s_dst[rB]), loB - xB, e1B - 1 - xB);
         }
-        copy_one_chunk(s_dst, s_src, tot, outa, D0, xA, loA, hiA, rA, pA, e1A);
+        copy_one_chunk(s_dst, s_src, outa, D0, xA, loA, hiA, rA, pA, e1A);
         if (two) {
-            copy_one_chunk(s_dst, s_src, tot, outa, D0, xB, loB, hiB, rB, pB, e1B);
+            copy_one_chunk(s_dst, s_src, outa, D0, xB, loB, hiB, rB, pB, e1B);
             r = rB;
         } else {
             r = rA;

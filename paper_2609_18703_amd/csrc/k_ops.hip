@@ -6,7 +6,8 @@
 // output state by the same precedence (a failed or suppressed input
 // suppresses, an unresolved one waits, a dropped required one drops,
 // otherwise the output is ready).  Both are one pass over the output Domain:
-// 16 bytes of states per thread and load, HBM-bound.
+// the filter takes 16 states per thread and load; the broadcast one
+// descendant per thread, whose chained map lookups mostly hit in cache.
 #include "ro_device.h"
 
 namespace ro {

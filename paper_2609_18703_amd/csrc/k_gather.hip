@@ -526,7 +526,9 @@ hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w
                        a.P, w.canon_cap, a.out_off, a.out_cap, a.out_data != nullptr ? 1 : 0, a.ns, a.nf,
                        a.nk, a.complete, a.pstate, a.cdst, a.barrier, w.gkey, a.n_rejected, L.ctl);
     if (a.out_data != nullptr) {
-        const int64_t grid_c = (int64_t)L.num_cus * 8;
+        // many small workgroups: a unit's cost varies with the records it
+        // meets, and a deep queue of workgroups evens out the tail
+        const int64_t grid_c = (int64_t)L.num_cus * 32;
         RO_LAUNCH(L, RO_K_GATHER_COPY, k_gather_copy, dim3((unsigned)grid_c), dim3(kBlock), 0, L.stream, a.offsets,
                   a.P, w.canon, w.canon_cap, w.sub_base, a.out_data, a.out_data == a.data ? 1 : 0, L.ctl);
     }

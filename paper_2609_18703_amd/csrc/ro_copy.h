@@ -234,7 +234,7 @@ __device__ __forceinline__ void copy_window32_x2(const int32_t *s_dst, const uin
 #define RO_COPY_UNITS 2
 #endif
 #ifndef RO_COPY_MIN_UNIT
-#define RO_COPY_MIN_UNIT 4096
+#define RO_COPY_MIN_UNIT (128 << 10)
 #endif
 constexpr int64_t kCopyUnits = RO_COPY_UNITS;
 constexpr int64_t kCopyMinUnit = RO_COPY_MIN_UNIT;

@@ -216,7 +216,8 @@ class Job:
 
 
 def stage_zipf(ctx, parents, canonical=False):
-    """Workload 2.  With canonical=True every child becomes ready in canonical
+    """The single-level Zipf(1.2) fan-out (100,000 parents, 41.1M children,
+    25.2 GB of surviving records).  With canonical=True every child becomes ready in canonical
     order, so the reports (and their records) arrive in slot order and the
     gather's reads are sequential: the same path at its best-case ordering."""
     import torch

@@ -517,7 +517,9 @@ hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w
     RO_LAUNCH(L, RO_K_GATHER_SCATTER, k_gather_scatter, dim3((unsigned)grid_r), dim3(kBlock), 0, L.stream,
               a.rp, a.ro, a.rs, a.roff, a.data, a.n, a.offsets, a.P, w.canon, w.canon_cap, a.ns, a.nf,
               a.nk, a.barrier, w.gkey, L.ctl);
-    const int64_t grid_s = (int64_t)L.num_cus * 4;
+    // three workgroups per CU drew tickets faster than four (fewer waiting
+    // on the look-back at once) and two left the largest scans short of work
+    const int64_t grid_s = (int64_t)L.num_cus * 3;
     RO_LAUNCH(L, RO_K_GATHER_SCAN, k_gather_scan, dim3((unsigned)grid_s), dim3(kBlock), 0, L.stream, a.offsets, a.P,
               w.canon, w.canon_cap, a.out_off, a.ns, a.nf, a.nk, a.cdst, w.sub_base, L.ctl, L.desc, L.desc_cap);
     int64_t grid_f = (a.P + kBlock - 1) / kBlock;

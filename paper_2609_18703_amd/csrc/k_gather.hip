@@ -433,6 +433,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_
     const uint32_t epoch = ctl->canon_epoch;
     __shared__ int32_t s_dst_all[kWaves][kSub + 1];     // clipped destination offset of each record
     __shared__ uint64_t s_src_all[kWaves][kSub];        // source address of its first clipped byte
+    __shared__ int32_t s_edge_all[kWaves][kEdgeCap];    // edge chunks of the window
+    __shared__ int16_t s_edger_all[kWaves][kEdgeCap];   // the record holding each one's first byte
     if (read_err(ctl) != 0) return;                      // any recorded error: copy nothing
     const int64_t N0 = offsets[P];
     const int64_t N = N0 <= canon_cap ? N0 : 0;
@@ -444,13 +446,15 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_
     const int64_t nwaves = (int64_t)gridDim.x * kWaves;
     int64_t G, nunits;
     copy_units(T, nwaves, mis, G, nunits);
-    const int wave = (int)(threadIdx.x >> 6), lane = lane_id();
+    const int wave = uni32((int)(threadIdx.x >> 6)), lane = lane_id();
     int32_t *s_dst = s_dst_all[wave];
     uint64_t *s_src = s_src_all[wave];
+    int32_t *s_edge = s_edge_all[wave];
+    int16_t *s_edger = s_edger_all[wave];
     for (int64_t u = (int64_t)blockIdx.x * kWaves + wave; u < nunits; u += nwaves) {
         const int64_t lo = max64(u * G - mis, 0);
         const int64_t hi = min64((u + 1) * G - mis, T);
-        for (int64_t sb = find_sub_tile(sub_base, nsub, lo); sb < nsub; ++sb) {
+        for (int64_t sb = uni64(find_sub_tile(sub_base, nsub, lo)); sb < nsub; ++sb) {
             const int64_t D0 = sub_base[sb];
             if (D0 >= hi) break;
             const int64_t c0 = sb * kSub;
@@ -459,22 +463,24 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_
             int64_t lsum = 0;
             uint32_t l[kCopyPer];
             uint64_t s[kCopyPer];
+            // whole 16-byte slots, all four loads in flight together (a
+            // slot past the expansion re-reads the last one and is ignored)
+            uint4 ev[kCopyPer];
 #pragma unroll
             for (int k = 0; k < kCopyPer; ++k) {
                 const int64_t r = (int64_t)lane * kCopyPer + k;
-                l[k] = 0;
-                s[k] = 0;
-                if (r < cnt) {
-                    const Canon e = canon[c0 + r];
-                    if (e.tag == ((epoch << 2) | RO_SUCCESS)) {
-                        l[k] = e.len;
-                        s[k] = e.src;
-                    }
-                }
+                ev[k] = ld16(reinterpret_cast<uint64_t>(&canon[c0 + (r < cnt ? r : cnt - 1)]));
+            }
+#pragma unroll
+            for (int k = 0; k < kCopyPer; ++k) {
+                const int64_t r = (int64_t)lane * kCopyPer + k;
+                const bool ok = r < cnt && ev[k].w == ((epoch << 2) | RO_SUCCESS);
+                l[k] = ok ? ev[k].z : 0u;
+                s[k] = ok ? ((uint64_t)ev[k].y << 32 | ev[k].x) : 0ull;
                 lsum += l[k];
             }
             const int64_t inc = wave_incl_sum(lsum);
-            const int64_t tot = __shfl(inc, 63, 64);
+            const int64_t tot = uni64(__shfl(inc, 63, 64));
             // this unit's part of the sub-tile: [ws, we), relative to D0
             const int64_t ws = max64(lo - D0, 0), we = min64(hi - D0, tot);
             if (we > ws) {
@@ -500,7 +506,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_
                 }
                 if (lane == 0) s_dst[kSub] = (int32_t)(we - ws);
                 __builtin_amdgcn_wave_barrier();
-                copy_window32_x2(s_dst, s_src, (int)(we - ws), outa, D0 + ws, lane);
+                copy_window_nb<RO_COPY_STEPS>(s_dst, s_src, s_edge, s_edger, (int)(we - ws), outa, D0 + ws, lane);
                 __builtin_amdgcn_wave_barrier();
             }
         }

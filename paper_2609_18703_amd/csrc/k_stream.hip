@@ -381,7 +381,7 @@ __global__ __launch_bounds__(kBlock) void k_emit_scan(
 // the children it covers 256 at a time, each clipped to the unit.
 constexpr int64_t kEmitMinUnit = 1024;
 
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_WAVES))) void k_emit_out(
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void k_emit_out(
     int64_t *__restrict__ emit_off, const int64_t *__restrict__ evoff, const int32_t *__restrict__ ecnt,
     int64_t ecnt_stride, const uint8_t *__restrict__ ebar, int32_t *__restrict__ ns, int32_t *__restrict__ nf,
     int32_t *__restrict__ nk, uint8_t *__restrict__ pstate, int64_t *n_bytes, const int64_t *__restrict__ edst,

@@ -17,6 +17,17 @@ __device__ __forceinline__ int32_t read_err(Ctl *ctl)
     return __hip_atomic_load(&ctl->err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// A value every lane of the wave holds alike, moved to a scalar register
+// (the compiler cannot see that results of shuffles or LDS reads are
+// wave-uniform, and would keep them in vector registers).
+__device__ __forceinline__ int32_t uni32(int32_t v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ int64_t uni64(int64_t v)
+{
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int32_t)(uint32_t)v);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int32_t)(uint32_t)((uint64_t)v >> 32));
+    return (int64_t)((uint64_t)hi << 32 | lo);
+}
+
 // ---- wave64 reductions / scans -------------------------------------------
 template <typename T>
 __device__ __forceinline__ T wave_incl_sum(T v)

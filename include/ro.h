@@ -142,6 +142,23 @@ int ro_ctx_trace_read(ro_ctx *ctx, int64_t *launches, double *total_ms, int32_t 
 int ro_expand(ro_ctx *ctx, const int32_t *counts, int64_t n_parents, int64_t *offsets,
               uint32_t *child_parent, uint32_t *child_ordinal, int64_t child_cap);
 
+/* ro_expand for callers that cannot allocate device memory: code under
+ * stream capture, tight serving loops, harnesses that forbid hipMalloc.  It
+ * takes no context and calls no allocating routine: the scan's workspace
+ * (control words and look-back descriptors, about 33 KB) is one fixed
+ * device array per GPU, set up on the first call on that GPU (the calling
+ * thread's current device) and held until the process ends.  Same inputs,
+ * outputs and results as ro_expand, on the HIP stream hip_stream (NULL = the
+ * null stream).  At most 2^24 parents: larger n_parents returns RO_ECAP at
+ * once.  Host-detectable errors return at once (RO_EINVAL); the
+ * device-detected status (RO_OK, or RO_EINVAL / RO_ECAP / RO_EOVERFLOW as
+ * for ro_expand) is written, stream-ordered, to the device int32
+ * *status_dev at the end of the call (status_dev may be NULL).  Every call
+ * on one GPU shares that GPU's workspace: calls that overlap on one GPU (on
+ * different streams or host threads) race and must not be issued. */
+int ro_expand_noalloc(void *hip_stream, const int32_t *counts, int64_t n_parents, int64_t *offsets,
+                      uint32_t *child_parent, uint32_t *child_ordinal, int64_t child_cap, int32_t *status_dev);
+
 /* FIFO Ready Queue + elastic reservation.  queue[q_len] holds canonical
  * child ids in enqueue order; entry i is ready iff keep == NULL or
  * keep[i] != 0.  Ready entries are compacted in queue order into slots

@@ -13,7 +13,7 @@ INCLUDE = os.path.join(ROOT, "include")
 OBJ = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libro.so")
 
-SOURCES = ["ro_api.hip", "k_misc.hip", "k_expand.hip", "k_batch.hip", "k_gather.hip", "k_stream.hip", "k_ops.hip", "k_grains.hip", "k_pbatch.hip"]
+SOURCES = ["ro_api.hip", "k_misc.hip", "k_expand.hip", "k_batch.hip", "k_gather.hip", "k_stream.hip", "k_ops.hip", "k_grains.hip", "k_pbatch.hip", "ro_noalloc.hip"]
 
 ARCH = os.environ.get("RO_OFFLOAD_ARCH", "gfx950")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -11,7 +11,8 @@ import ctypes as C
 import os
 import weakref
 
-__all__ = ["RoError", "load", "Context", "Stream", "Grains", "KERNELS", "OK", "EINVAL", "ERANGE", "EDUP", "ECAP",
+__all__ = ["RoError", "load", "Context", "Stream", "Grains", "expand_noalloc", "EXPAND_NOALLOC_MAX_PARENTS",
+           "KERNELS", "OK", "EINVAL", "ERANGE", "EDUP", "ECAP",
            "EOVERFLOW", "ESTATE", "EHIP", "SUCCESS", "FAILED", "SKIPPED", "PENDING", "GROUP_FAILED",
            "LIB_PATH"]
 
@@ -65,6 +66,7 @@ def load(path=None):
     L.ro_ctx_status.argtypes = [P]
     L.ro_ctx_destroy.argtypes = [P]
     L.ro_expand.argtypes = [P, P, i64, P, P, P, i64]
+    L.ro_expand_noalloc.argtypes = [P, P, i64, P, P, P, i64, P]
     L.ro_batch.argtypes = [P, P, P, i64, P, i64, i32, P, P, P, i64, P, P, P]
     L.ro_batch_parent.argtypes = [P, P, P, i64, P, i64, i32, P, P, P, i64, P, i64, P, P, P]
     L.ro_gather.argtypes = [P, C.POINTER(ReportsT), P, i64, C.POINTER(GatherOutT)]
@@ -87,7 +89,7 @@ def load(path=None):
     L.ro_ctx_trace.argtypes = [P, C.c_int]
     L.ro_ctx_trace_read.argtypes = [P, P, P, i32]
     for name in ("ro_ctx_trace", "ro_ctx_trace_read", "ro_ctx_create", "ro_ctx_set_stream", "ro_ctx_reserve",
-                 "ro_ctx_status", "ro_ctx_destroy", "ro_expand", "ro_batch", "ro_batch_parent", "ro_gather",
+                 "ro_ctx_status", "ro_ctx_destroy", "ro_expand", "ro_expand_noalloc", "ro_batch", "ro_batch_parent", "ro_gather",
                  "ro_stream_create", "ro_stream_batch", "ro_stream_report", "ro_stream_emit", "ro_stream_reset", "ro_stream_destroy", "ro_filter",
                  "ro_broadcast", "ro_grains_create", "ro_grains_reset", "ro_grains_destroy", "ro_grains_read",
                  "ro_grains_dispatch", "ro_grains_retry", "ro_grains_commit", "ro_debug_epochs"):
@@ -117,6 +119,26 @@ def _ptr(t, item=None, n=0, name="array"):
 def _check(rc, what):
     if rc != OK:
         raise RoError(rc, what)
+
+
+# the largest expansion ro_expand_noalloc takes (its fixed device workspace)
+EXPAND_NOALLOC_MAX_PARENTS = 1 << 24
+
+
+def expand_noalloc(counts, offsets, child_parent=None, child_ordinal=None, status=None, n_parents=None):
+    """ro_expand_noalloc on torch's current stream: ro_expand without a
+    context and without any device allocation.  ``status`` (optional, one
+    int32 on the GPU) receives the device-detected status of the call."""
+    import torch
+    L = load()
+    cap = 0
+    if child_parent is not None or child_ordinal is not None:
+        cap = min(t.numel() for t in (child_parent, child_ordinal) if t is not None)
+    P = counts.numel() if n_parents is None else int(n_parents)
+    stream = C.c_void_p(torch.cuda.current_stream().cuda_stream)
+    _check(L.ro_expand_noalloc(stream, _ptr(counts, 4, P, "counts"), P, _ptr(offsets, 8, P + 1, "offsets"),
+                               _ptr(child_parent, 4, 0, "child_parent"), _ptr(child_ordinal, 4, 0, "child_ordinal"),
+                               cap, _ptr(status, 4, 1, "status")), "ro_expand_noalloc")
 
 
 def _reports(parent, ordinal, state, off, data, n=None):

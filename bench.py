@@ -31,7 +31,11 @@ untimed by the generator's device fill):
                 for comparison with the random order of zipf-single).
 
 Prints one JSON line.  Children/s counts every child entity created at every
-level (pages + regions, clips + frames).
+level (pages + regions, clips + frames).  With the default workload the line
+also carries, under "docs_nested", the same measurement of the two-level
+documents workload (its own roofline, config and CPU baseline): the
+single-level Zipf workload and the documents workload are the two readings
+of the throughput target's "config 2".
 """
 from __future__ import annotations
 
@@ -61,6 +65,8 @@ def parse():
     ap.add_argument("--parents", type=int, default=None,
                     help="top-level parents (default: the workload's own size)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-docs", action="store_true",
+                    help="with the default workload, skip the second line of the documents workload")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--rocprof-summary", metavar="DIR", default=None,
@@ -538,23 +544,39 @@ def main():
 
 
 def run(args):
+    """The workload of the line; for the default one (single-level Zipf) also
+    the two-level documents workload, timed the same way, under the key
+    "docs_nested": the two workloads a reading of "config 2" can mean."""
+    result = run_workload(args, args.workload)
+    second = args.workload == "zipf-single" and not args.no_docs
+    if second:
+        result["docs_nested"] = run_workload(args, "docs-nested")
+    if not args.no_cpu:
+        result["cpu_baseline"] = cpu_baseline(args.workload)
+        if second:
+            result["docs_nested"]["cpu_baseline"] = cpu_baseline("docs-nested")
+    return result
+
+
+def run_workload(args, workload):
     import torch
     import paper_2609_18703_amd as R
 
     t0 = time.time()
     ctx = R.Context()
-    if args.workload in ("zipf-single", "zipf-canonical"):
-        job = stage_zipf(ctx, args.parents, canonical=args.workload == "zipf-canonical")
-    elif args.workload == "stream-waves":
-        job = stage_stream(ctx, args.parents)
-    elif args.workload == "docs-ops":
-        job = stage_ops(ctx, args.parents)
-    elif args.workload == "zipf-fence":
-        job = stage_fence(ctx, args.parents)
-    elif args.workload == "zipf-pbatch":
-        job = stage_pbatch(ctx, args.parents)
+    parents = args.parents if workload == args.workload else None
+    if workload in ("zipf-single", "zipf-canonical"):
+        job = stage_zipf(ctx, parents, canonical=workload == "zipf-canonical")
+    elif workload == "stream-waves":
+        job = stage_stream(ctx, parents)
+    elif workload == "docs-ops":
+        job = stage_ops(ctx, parents)
+    elif workload == "zipf-fence":
+        job = stage_fence(ctx, parents)
+    elif workload == "zipf-pbatch":
+        job = stage_pbatch(ctx, parents)
     else:
-        job = stage_nested(ctx, args.workload, args.parents)
+        job = stage_nested(ctx, workload, parents)
     torch.cuda.synchronize()
     log(f"[bench] staged in HBM ({time.time() - t0:.1f}s)")
 
@@ -648,6 +670,13 @@ def run(args):
         "traffic_frac": round(traffic / (dom_avg_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4) if traffic else None,
         "step_alg_GBps": round(total_alg / (ms_step * 1e-3) / 1e9, 1),
         "step_frac_of_peak": round(total_alg / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+        # the whole step against the HBM peak: algorithmic bytes of every
+        # kernel of the step over the untimed-event step time (the target's
+        # figure); roofline above is the dominant kernel alone
+        "step_roofline": {"bound": "hbm", "achieved": round(total_alg / (ms_step * 1e-3) / 1e9, 1),
+                          "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                          "frac": round(total_alg / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                          "alg_bytes_per_step": int(total_alg)},
         "kernels": per_kernel,
     }
     if job.leaves is not None:
@@ -671,23 +700,43 @@ def run(args):
 
     del job
     torch.cuda.empty_cache()
-
-    if not args.no_cpu:
-        result["cpu_baseline"] = cpu_baseline(args.workload)
-
     return result
 
 
 def _cpu_info():
-    model = platform.processor() or ""
+    """Model name of the host CPU as /proc/cpuinfo gives it, with its
+    family / model / stepping numbers, and the host's CPU count."""
+    fields = {}
     try:
         for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                model = line.split(":", 1)[1].strip()
+            if ":" in line:
+                k, v = line.split(":", 1)
+                fields.setdefault(k.strip(), v.strip())
+            if not line.strip() and fields:
                 break
     except OSError:
         pass
+    model = fields.get("model name") or platform.processor() or "unknown"
+    ids = [f"{k} {fields[k]}" for k in ("cpu family", "model", "stepping") if k in fields]
+    if ids:
+        model = f"{model} ({', '.join(ids)})"
     return model, os.cpu_count()
+
+
+class _OneCore:
+    """Pins this process to one CPU (the first it may use) while the oracle
+    runs, and restores the previous set afterwards; the oracle is single
+    threaded, so the pin only keeps it from migrating."""
+
+    def __enter__(self):
+        self.prev = os.sched_getaffinity(0)
+        self.cpu = min(self.prev)
+        os.sched_setaffinity(0, {self.cpu})
+        return self
+
+    def __exit__(self, *exc):
+        os.sched_setaffinity(0, self.prev)
+        return False
 
 
 def _host_bytes(rep):
@@ -704,9 +753,15 @@ def _host_bytes(rep):
 
 
 def cpu_baseline(workload):
-    """The oracle, single threaded, on a bounded sample of the workload
-    (about 10-30 s of one core): the same distributions at a smaller size
-    where the full one would take longer."""
+    """The oracle, single threaded and pinned to one CPU, on the workload
+    (the full one: each takes under 15 s of one core here)."""
+    with _OneCore() as pin:
+        r = _cpu_baseline(workload)
+    r["pinned_cpu"] = pin.cpu
+    return r
+
+
+def _cpu_baseline(workload):
     import torch
     import oracle as O
     import workloads as W

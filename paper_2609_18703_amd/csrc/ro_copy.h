@@ -173,13 +173,6 @@ __device__ __forceinline__ void copy_window32(const int32_t *s_dst, const uint64
     }
 }
 
-// Lane i receives lane i + 1's value (a wave-wide DPP shift); lane 63
-// receives `old`.  All 64 lanes must be active.
-__device__ __forceinline__ uint32_t from_next_lane(uint32_t v, uint32_t old)
-{
-    return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, 0x130, 0xf, 0xf, false);
-}
-
 // Chunks a window can list for the edge pass: at most one per record end in
 // the window plus its first and last chunk.
 constexpr int kEdgeCap = kSub + 4;
@@ -221,9 +214,13 @@ __device__ __forceinline__ void copy_edges(const int32_t *s_dst, const uint64_t 
     }
 }
 
-// The same on native 4-dword vectors (kept in registers even in arrays
-// written under a condition).
-__device__ __forceinline__ v4u32 ld16v(uint64_t a) { return *(const RO_GLOBAL v4u32 *)a; }
+// Loads and stores on native 4-dword vectors (kept in registers even in
+// arrays written under a condition).  ld16v takes any byte address: gfx950
+// serves a misaligned 16-byte global load as one load returning the 16 bytes
+// at that address, at the speed of an aligned one (the type tells the
+// compiler to assume no alignment).
+typedef uint32_t v4u32_u1 __attribute__((ext_vector_type(4), aligned(1)));
+__device__ __forceinline__ v4u32 ld16v(uint64_t a) { return *(const RO_GLOBAL v4u32_u1 *)a; }
 __device__ __forceinline__ void st16v(uint64_t a, v4u32 v) { *(RO_GLOBAL v4u32 *)a = v; }
 
 __device__ __forceinline__ v4u32 shift16v(v4u32 lo, v4u32 hi, uint32_t sh)
@@ -241,35 +238,21 @@ __device__ __forceinline__ v4u32 shift16v(v4u32 lo, v4u32 hi, uint32_t sh)
     return r;
 }
 
-// Bytes [0, n) of a, bytes [n, 16) of b (0 <= n <= 16).
-__device__ __forceinline__ v4u32 merge_at(v4u32 a, v4u32 b, int n)
-{
-    v4u32 m;
-#pragma unroll
-    for (int d = 0; d < 4; ++d) {
-        const int k = n - 4 * d;
-        m[d] = k >= 4 ? 0xffffffffu : (k <= 0 ? 0u : (0xffffffffu >> (8 * (4 - k))));
-    }
-    return (a & m) | (b & ~m);
-}
-
-// One unit's window of a sub-tile, with about one aligned 16-byte source load
-// per output chunk.  A step of the wave covers 64 consecutive output chunks,
-// one per lane, and every lane loads the aligned source chunk holding the
-// first byte its chunk needs.  Inside a record, lane i's chunk needs source
-// bytes [s, s + 16), which lie in its own load and the aligned chunk after
-// it: the one lane i + 1 loaded whenever lane i + 1 sits in the same record,
-// so the pair is completed with a cross-lane move.  A chunk that holds the
-// end of one record and the start of the next takes its second piece's
-// upper half the same way (lane i + 1 loaded the chunk after the one holding
-// the piece's start) and loads what else it needs itself, in the same step:
-// every store of a step is whole when the step ends, so no cache line is
-// left half written.  U steps are in flight per lane, their loads issued
-// together.  Chunks at the window's two ends, chunks holding three or more
-// records (records under 16 bytes) and two-record chunks whose second
-// record does not go on into lane i + 1's chunk (it ends with the chunk, or
-// the chunk is lane 63's) are listed in LDS and written after the sweep,
-// byte by byte.
+// One unit's window of a sub-tile.  A step of the wave covers 64
+// consecutive output chunks, one per lane, each written with one aligned
+// 16-byte store.  A chunk inside one record takes one 16-byte load from its
+// exact (byte-aligned) source address: a misaligned 16-byte global load
+// returns the 16 bytes at that address, at the speed of an aligned one, and
+// all of them are bytes of the record.  A chunk holding the end of record r
+// and the start of record q takes two: the 16 bytes that end where r ends
+// and the 16 that start where q starts (both inside their records); the
+// chunk is bytes 16 - n1 .. 31 - n1 of the two side by side, n1 being r's
+// share of it.  Every store of a step is whole when the step ends, so no
+// cache line is left half written.  U steps are in flight per lane, their
+// loads issued together.  Chunks at the window's two ends, chunks holding
+// three or more records, and two-record chunks with a side shorter than 16
+// bytes in the window (records under 16 bytes) are listed in LDS and
+// written after the sweep, byte by byte.
 template <int U>
 __device__ __forceinline__ void copy_window_nb(const int32_t *s_dst, const uint64_t *s_src, int32_t *s_edge,
                                                int16_t *s_edger, int tot, uint64_t outa, int64_t D0, int lane)
@@ -279,87 +262,64 @@ __device__ __forceinline__ void copy_window_nb(const int32_t *s_dst, const uint6
     const int nchunks = (int)((a1 - a0) >> 4) + 1;
     const int xbase = (int)((int64_t)(a0 - outa) - D0);     // -15..0
     const uint64_t dbase = outa + (uint64_t)D0;             // destination of window byte 0
-    // a chunk every lane may load: the one holding the window's first byte
+    // an address every lane may load from: the window's first source byte
+    // (its record holds at least one byte, and 16 bytes from it stay in the
+    // record or in the aligned 16-byte chunks next to it only when the
+    // record is that long, so lanes with nothing to do load from its aligned
+    // chunk instead)
     const uint64_t safe = (uint64_t)uni64((int64_t)(s_src[advance_record(s_dst, 0, 0)] & ~(uint64_t)15));
     int r = 0, nedge = 0;
     for (int s0 = 0; s0 * 64 < nchunks; s0 += U) {
-        // info: bits 0-1 kind (0 nothing to write, 1 one record, 2 two
-        // records, 3 listed), bit 2 first piece completed by lane i + 1,
-        // bit 3 second piece completed by lane i + 1, bits 4-7 shift of the
-        // first piece, 8-11 of the second, 12-16 length of the first piece
-        uint32_t info[U];
-        int rr[U];
-        v4u32 L0[U], X1[U], X2[U];
+        // kind: 0 nothing, 1 one record, 2 two records, 3 listed
+        int kind[U], n1[U], rr[U];
+        v4u32 L[U], X[U];
 #pragma unroll
         for (int k = 0; k < U; ++k) {
             const int ch = (s0 + k) * 64 + lane;
             const int x = xbase + ch * 16;
-            uint32_t f = 0;
-            int q = -1;
+            uint64_t A = safe, B = safe;
+            kind[k] = 0;
+            n1[k] = 16;
             rr[k] = -1;
-            uint64_t A0 = safe, C2 = safe;
             if (ch < nchunks) {
                 const int b0 = x > 0 ? x : 0;
                 r = advance_record(s_dst, r, b0);
                 rr[k] = r;
-                const int d1 = s_dst[r + 1];
-                // source address of window byte 0, extended linearly through r
-                const uint64_t vb = s_src[r] - (uint64_t)(int64_t)s_dst[r];
-                A0 = (vb + (uint64_t)(int64_t)b0) & ~(uint64_t)15;
-                f = 3;
+                kind[k] = 3;
                 if (x >= 0 && x + 16 <= tot) {
-                    const uint32_t sh1 = (uint32_t)(vb + (uint64_t)(int64_t)x) & 15u;
+                    const int d0 = s_dst[r], d1 = s_dst[r + 1];
+                    // source of window byte 0, extended linearly through r
+                    const uint64_t vb = s_src[r] - (uint64_t)(int64_t)d0;
                     if (d1 >= x + 16) {
-                        f = 1 | sh1 << 4 | 16u << 12;
-                    } else {
-                        const int qq = advance_record(s_dst, r, d1);
-                        if (s_dst[qq + 1] > x + 16) {
-                            q = qq;
-                            const uint64_t V2 = s_src[q] - (uint64_t)(int64_t)s_dst[q] + (uint64_t)(int64_t)x;
-                            f = 2 | sh1 << 4 | ((uint32_t)V2 & 15u) << 8 | (uint32_t)(d1 - x) << 12;
-                            C2 = V2 & ~(uint64_t)15;
+                        kind[k] = 1;
+                        A = vb + (uint64_t)(int64_t)x;
+                    } else if (d1 - d0 >= 16) {
+                        const int q = advance_record(s_dst, r, d1);
+                        const int e0 = s_dst[q], e1 = s_dst[q + 1];
+                        if (e1 > x + 16 && e1 - e0 >= 16) {
+                            kind[k] = 2;
+                            n1[k] = d1 - x;
+                            A = vb + (uint64_t)(int64_t)(d1 - 16);                  // ends where r ends
+                            B = s_src[q] + (uint64_t)(int64_t)(d1 - e0);            // starts where q starts
                         }
                     }
                 }
             }
-            // the record holding lane i + 1's first byte (-1 past the window)
-            const int rn = (int)from_next_lane((uint32_t)rr[k], 0xffffffffu);
-            // a second piece whose upper half lane i + 1 does not hold (lane
-            // 63) is listed
-            if ((f & 3u) == 2u && rn != q) f = 3;
             const v4u32 z = {0u, 0u, 0u, 0u};
-            X1[k] = z;
-            X2[k] = z;
-            L0[k] = ld16v(A0);
-            const uint32_t kd = f & 3u, sh1 = (f >> 4) & 15u, sh2 = (f >> 8) & 15u;
-            const int n1 = (int)(f >> 12);
-            // second source chunk of the first piece, unless lane i + 1 has it
-            const bool n_x1 = (kd == 1 && sh1 != 0 && rn != rr[k]) || (kd == 2 && (int)sh1 + n1 > 16);
-            // first source chunk of the second piece, if it holds any of it
-            // (its second chunk is lane i + 1's)
-            const bool n_x2 = kd == 2 && n1 + (int)sh2 < 16;
-            f |= rn == rr[k] ? 4u : 0u;
-            f |= (kd == 2) ? 8u : 0u;
-            info[k] = f;
-            if (n_x1) X1[k] = ld16v(A0 + 16);
-            if (n_x2) X2[k] = ld16v(C2);
+            X[k] = z;
+            L[k] = ld16v(A);
+            if (kind[k] == 2) X[k] = ld16v(B);
         }
 #pragma unroll
         for (int k = 0; k < U; ++k) {
-            v4u32 nb;
-            nb.x = from_next_lane(L0[k].x, 0u);
-            nb.y = from_next_lane(L0[k].y, 0u);
-            nb.z = from_next_lane(L0[k].z, 0u);
-            nb.w = from_next_lane(L0[k].w, 0u);
-            const uint32_t f = info[k];
-            // one record: the first piece is the whole chunk
-            const v4u32 h1 = (f & 4u) ? nb : X1[k];
-            const v4u32 v = merge_at(shift16v(L0[k], h1, (f >> 4) & 15u), shift16v(X2[k], nb, (f >> 8) & 15u),
-                                     (int)(f >> 12));
-            const uint32_t kd = f & 3u;
+            v4u32 v = L[k];
+            if (__ballot(kind[k] == 2) != 0) {
+                const v4u32 w = shift16v(L[k], X[k], (uint32_t)(16 - n1[k]) & 15u);
+                if (kind[k] == 2) v = w;
+            }
             const int x = xbase + ((s0 + k) * 64 + lane) * 16;
-            if (kd == 1 || kd == 2) st16v(dbase + (uint64_t)x, v);
-            const bool listed = kd == 3;
+            if (kind[k] == 1 || kind[k] == 2) st16v(dbase + (uint64_t)x, v);
+            const bool listed = kind[k] == 3;
             const uint64_t m = __ballot(listed);
             if (listed) {
                 const int pos = nedge + __popcll(m & ((1ull << lane) - 1ull));
@@ -382,10 +342,10 @@ __device__ __forceinline__ void copy_window_nb(const int32_t *s_dst, const uint6
 // Copy kernels trade per-wave registers for occupancy: the compiler keeps
 // register use low enough for at least this many waves per SIMD.
 #ifndef RO_COPY_WAVES
-#define RO_COPY_WAVES 5
+#define RO_COPY_WAVES 4
 #endif
 #ifndef RO_COPY_STEPS
-#define RO_COPY_STEPS 2
+#define RO_COPY_STEPS 6
 #endif
 #ifndef RO_COPY_UNITS
 #define RO_COPY_UNITS 2

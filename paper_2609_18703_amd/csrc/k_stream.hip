@@ -380,6 +380,9 @@ __global__ __launch_bounds__(kBlock) void k_emit_scan(
 // finds its first child by a wave search over the output positions and takes
 // the children it covers 256 at a time, each clipped to the unit.
 constexpr int64_t kEmitMinUnit = 1024;
+#ifndef RO_EMIT_STEPS
+#define RO_EMIT_STEPS 4
+#endif
 
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void k_emit_out(
     int64_t *__restrict__ emit_off, const int64_t *__restrict__ evoff, const int32_t *__restrict__ ecnt,
@@ -390,6 +393,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     constexpr int kWaves = kBlock / 64;
     __shared__ int32_t s_dst_all[kWaves][kSub + 1];
     __shared__ uint64_t s_src_all[kWaves][kSub];
+    __shared__ int32_t s_edge_all[kWaves][kEdgeCap];
+    __shared__ int16_t s_edger_all[kWaves][kEdgeCap];
     const int64_t E = ctl->n_items;
     const int64_t V = ctl->n_virtual;
     const int64_t T = V > 0 ? ctl->total : 0;
@@ -415,13 +420,15 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     G = (G + 15) & ~(int64_t)15;
     G = G < kEmitMinUnit ? kEmitMinUnit : (G > ((int64_t)1 << 30) ? ((int64_t)1 << 30) : G);
     const int64_t nunits = (T + mis + G - 1) / G;
-    const int wave = (int)(threadIdx.x >> 6), lane = lane_id();
+    const int wave = uni32((int)(threadIdx.x >> 6)), lane = lane_id();
     int32_t *s_dst = s_dst_all[wave];
     uint64_t *s_src = s_src_all[wave];
+    int32_t *s_edge = s_edge_all[wave];
+    int16_t *s_edger = s_edger_all[wave];
     for (int64_t u = (int64_t)blockIdx.x * kWaves + wave; u < nunits; u += nwaves) {
         const int64_t lo = max64(u * G - mis, 0);
         const int64_t hi = min64((u + 1) * G - mis, T);
-        for (int64_t r0 = wave_last_le(edst, 0, V, lo); r0 < V; r0 += kSub) {
+        for (int64_t r0 = uni64(wave_last_le(edst, 0, V, lo)); r0 < V; r0 += kSub) {
             // children r0 .. r0 + kSub - 1, their starts clipped to [ws, we)
             const int64_t dend = edst[min64(r0 + kSub, V)];
             const int64_t ws = max64(lo, edst[r0]);
@@ -451,7 +458,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
             }
             if (lane == 0) s_dst[kSub] = (int32_t)(we - ws);
             __builtin_amdgcn_wave_barrier();
-            copy_window32(s_dst, s_src, (int)(we - ws), outa, ws, lane);
+            copy_window_nb<RO_EMIT_STEPS>(s_dst, s_src, s_edge, s_edger, (int)(we - ws), outa, ws, lane);
             __builtin_amdgcn_wave_barrier();
             if (dend >= hi) break;
         }

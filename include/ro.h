@@ -84,7 +84,9 @@ enum {
     RO_ECAP = -4,       /* an output or the reserved workspace is too small            */
     RO_EOVERFLOW = -5,  /* N >= 2^32 children, a record of 2^32 bytes or more, or
                            byte totals beyond 2^45                                     */
-    RO_ESTATE = -6,     /* a state byte > RO_PENDING                                   */
+    RO_ESTATE = -6,     /* a state byte > RO_PENDING (RO_GROUP_FAILED is valid only
+                           where a barrier array is given), or a Grain not in the
+                           phase an operation needs                                    */
     RO_EHIP = -7        /* a HIP runtime call failed                                   */
 };
 
@@ -357,18 +359,6 @@ int ro_stream_reset(ro_ctx *ctx, ro_stream *s);
 /* Waits for the owning context's stream, then frees the stream state (the
  * context must still exist). */
 int ro_stream_destroy(ro_stream *s);
-
-/* Test aid: move epochs forward so that their wrap-around paths run after a
- * few calls instead of about 2^30 or 2^32.  The context's next gathers use
- * canonical epochs up to the last one and then wrap after canon_left - 1 of
- * them; the stream s (may be NULL) wraps its slot epoch after run_left
- * resets and its group-failure epoch after gf_left reports; the Grain set g
- * (may be NULL) wraps its fence epoch after fence_left commits.  A value
- * below 1, or one that would move an epoch backwards, leaves that epoch as
- * it is.  Results are unchanged by design: every wrap clears what an old
- * epoch could be confused with. */
-int ro_debug_epochs(ro_ctx *ctx, ro_stream *s, ro_grains *g, int64_t canon_left, int64_t run_left,
-                    int64_t gf_left, int64_t fence_left);
 
 #ifdef __cplusplus
 }

@@ -5,6 +5,7 @@
 #include <vector>
 
 #include "ro_internal.h"
+#include "ro_testing.h"
 
 using namespace ro;
 

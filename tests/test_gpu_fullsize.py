@@ -113,20 +113,36 @@ def _nested_full(ctx, n, sample_top=60, n_big=10):
     want = O.nested(n.counts1, n.queue1, None, n.batch1, n.counts2, n.queue2, None, n.batch2,
                     r.state, r.off, None, with_data=False)
     low, up = want["low"], want["up"]
-    N1, P1 = b.N1, b.P1
+    N1, N2, P1 = b.N1, b.N2, b.P1
+    # every integer output of both levels, in full
+    assert np.array_equal(b.offsets1.cpu().numpy()[:P1 + 1], want["offsets1"])
+    assert np.array_equal(G.u32(b.mid_parent)[:N1], want["parent1"])
+    assert np.array_equal(G.u32(b.mid_ordinal)[:N1], want["ordinal1"])
+    sc = b.scalars.cpu().numpy()
+    assert int(sc[0]) == len(want["batch1"][0]) == N1
+    assert np.array_equal(G.u32(b.b1_parent)[:N1], want["batch1"][1])
+    assert np.array_equal(G.u32(b.b1_ordinal)[:N1], want["batch1"][2])
+    assert int(sc[1]) == len(want["batch1"][3])
     assert np.array_equal(b.offsets2.cpu().numpy()[:N1 + 1], want["offsets2"])
-    assert np.array_equal(G.u32(b.b2_parent)[:b.N2], want["batch2"][1])
-    assert np.array_equal(G.u32(b.b2_ordinal)[:b.N2], want["batch2"][2])
+    assert np.array_equal(G.u32(b.leaf_parent)[:N2], want["parent2"])
+    assert np.array_equal(G.u32(b.leaf_ordinal)[:N2], want["ordinal2"])
+    assert int(sc[2]) == len(want["batch2"][0]) == N2
+    assert np.array_equal(G.u32(b.b2_parent)[:N2], want["batch2"][1])
+    assert np.array_equal(G.u32(b.b2_ordinal)[:N2], want["batch2"][2])
+    assert int(sc[3]) == len(want["batch2"][3])
     for k in ("out_off",):
         assert np.array_equal(b.mid_off.cpu().numpy()[:N1 + 1], low[k])
         assert np.array_equal(b.top_off.cpu().numpy()[:P1 + 1], up[k])
     assert np.array_equal(b.mid_state.cpu().numpy()[:N1], low["parent_state"])
+    assert np.array_equal(b.mid_complete.cpu().numpy()[:N1], low["complete"])
     assert np.array_equal(b.mid_cnt.cpu().numpy()[:N1], low["n_success"])
     assert np.array_equal(b.mid_cnt.cpu().numpy()[N1:2 * N1], low["n_failed"])
+    assert np.array_equal(b.mid_cnt.cpu().numpy()[2 * N1:3 * N1], low["n_skipped"])
     assert np.array_equal(b.top_state.cpu().numpy()[:P1], up["parent_state"])
     assert np.array_equal(b.top_complete.cpu().numpy()[:P1], up["complete"])
     assert np.array_equal(b.top_cnt.cpu().numpy()[:P1], up["n_success"])
     assert np.array_equal(b.top_cnt.cpu().numpy()[P1:2 * P1], up["n_failed"])
+    assert np.array_equal(b.top_cnt.cpu().numpy()[2 * P1:3 * P1], up["n_skipped"])
     # content: a top slot is its surviving mid slots' bytes in order, and each
     # mid slot is its leaves' splitmix64 records in ordinal order
     off1, off2 = want["offsets1"], want["offsets2"]

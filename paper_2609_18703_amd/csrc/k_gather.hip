@@ -163,9 +163,17 @@ __global__ __launch_bounds__(kBlock) void k_gather_scatter(
 }
 
 // ---------------------------------------------------------------- scan
+#ifndef RO_SCAN_WG
+#define RO_SCAN_WG 3                        // workgroups per CU
+#endif
 // One tile = 4096 canonical children, 16 consecutive per thread; every 16
 // threads cover one copy sub-tile of 256 children and record its first output
-// byte.
+// byte.  A workgroup holds one tile at a time, but as soon as the tile's
+// look-back is done it draws the next ticket, finds the next tile's parents
+// and issues the loads of its slots, which are then in flight while the
+// current tile's pass 2 runs.  The current tile has posted its prefix before
+// the workgroup waits on anything for the next one, so the smallest tile not
+// yet posted always belongs to a workgroup that can post it.
 __global__ __launch_bounds__(kBlock) void k_gather_scan(
     const int64_t *__restrict__ offsets, int64_t P, const Canon *__restrict__ canon, int64_t canon_cap,
     int64_t *__restrict__ out_off, int32_t *__restrict__ ns, int32_t *__restrict__ nf,
@@ -178,9 +186,9 @@ __global__ __launch_bounds__(kBlock) void k_gather_scan(
     __shared__ uint64_t s_b;
     __shared__ int64_t s_t;
     __shared__ int32_t s_last;
-    __shared__ int64_t s_p[3];
+    __shared__ int64_t s_p[2][3];
     __shared__ int32_t s_cnt[3][kCntLds];
-    __shared__ int16_t s_off[kTile + 2];        // offsets[pf..pl+1] - ct0, clamped to [-1, kTile + 1]
+    __shared__ int16_t s_off[2][kTile + 2];     // offsets[pf..pl+1] - ct0, clamped to [-1, kTile + 1]
     __shared__ uint32_t s_len[kTile + kTile / 16];
     __shared__ alignas(16) uint8_t s_st[kTile];
     const int64_t N0 = offsets[P];
@@ -189,87 +197,132 @@ __global__ __launch_bounds__(kBlock) void k_gather_scan(
     const int64_t ntiles = (N + kTile - 1) / kTile;
     int32_t *cnt_out[3] = {ns, nf, nk};
     int64_t filled_total = 0;
-    // a workgroup that sees no tiles draws no ticket, so every drawn ticket
-    // is processed even if workgroups disagree about an error raised meanwhile
-    while (ntiles > 0) {
-        const int64_t t = next_ticket(ctl, &s_t);
-        if (t >= ntiles) break;
-        const int64_t ct0 = t * kTile;
-        const int64_t ct1 = min64(ct0 + kTile, N);
-        // the tile's parents, one wave-parallel search each: pf holds child
-        // ct0, pl holds child ct1 - 1, q0 is the first parent starting at or
-        // after ct0 (empty parents before pf may start exactly at ct0)
+    const int wv = (int)(threadIdx.x >> 6), ln = lane_id();
+
+    // Tile tt's parents, one wave-parallel search each: pf holds child a0,
+    // pl holds child a1 - 1, q0 is the first parent starting at or after a0
+    // (empty parents before pf may start exactly at a0).  With few enough
+    // parents, a tile-relative copy of their offsets goes to s_off[b] for
+    // pass 2 to search instead of global memory.
+    auto prepare = [&](int64_t tt, int b) {
+        const int64_t a0 = tt * kTile;
+        const int64_t a1 = min64(a0 + kTile, N);
         if (threadIdx.x < 3 * 64) {
-            const int w = (int)(threadIdx.x >> 6);
             int64_t r;
-            if (w == 0) r = wave_last_le(offsets, 0, P + 1, ct0);
-            else if (w == 1) r = wave_last_le(offsets, 0, P + 1, ct1 - 1);
-            else r = ct0 == 0 ? 0 : wave_last_le(offsets, 0, P + 1, ct0 - 1) + 1;
-            if (lane_id() == 0) s_p[w] = r;
+            if (wv == 0) r = wave_last_le(offsets, 0, P + 1, a0);
+            else if (wv == 1) r = wave_last_le(offsets, 0, P + 1, a1 - 1);
+            else r = a0 == 0 ? 0 : wave_last_le(offsets, 0, P + 1, a0 - 1) + 1;
+            if (ln == 0) s_p[b][wv] = r;
         }
         __syncthreads();
-        const int64_t pf = s_p[0], pl = s_p[1], q0t = s_p[2];
-        const int64_t Rp = pl - pf + 1;
-        const int64_t R = min64(Rp, kCntLds);
-        // with few enough parents, pass 2 searches a tile-relative copy of
-        // their offsets in LDS instead of global memory
-        const bool lds_ok = Rp <= kTile;
-        if (lds_ok) {
+        const int64_t pf = s_p[b][0];
+        const int64_t Rp = s_p[b][1] - pf + 1;
+        if (Rp <= kTile) {
             for (int64_t j = threadIdx.x; j <= Rp; j += kBlock) {
-                const int64_t v = offsets[pf + j] - ct0;
-                s_off[j] = (int16_t)(v < -1 ? -1 : (v > kTile + 1 ? kTile + 1 : v));
+                const int64_t v = offsets[pf + j] - a0;
+                s_off[b][j] = (int16_t)(v < -1 ? -1 : (v > kTile + 1 ? kTile + 1 : v));
             }
         }
-        for (int j = threadIdx.x; j < 3 * kCntLds; j += kBlock) (&s_cnt[0][0])[j] = 0;
+    };
+    // The length and tag words (8 of every 16 bytes) of tile tt's slots, each
+    // wave lane-contiguously over its 1024, into ev: the loads are only
+    // issued here.  A slot past the expansion re-reads the tile's first one
+    // and is ignored.
+    uint2 ev[kItems];
+    auto load_slots = [&](int64_t tt) {
+        const int64_t a0 = uni64(tt * kTile);
+        const int nloc = (int)uni64(min64(a0 + kTile, N) - a0);
+        // uniform base and 32-bit unsigned lane offsets: scalar-base loads
+        const uint8_t *tb = reinterpret_cast<const uint8_t *>(canon + a0) + offsetof(Canon, len);
+        const uint32_t jb = (uint32_t)(wv * (64 * kItems) + ln);
+        if (nloc == kTile) {
+#pragma unroll
+            for (int k = 0; k < kItems; ++k)
+                ev[k] = *reinterpret_cast<const uint2 *>(tb + (jb + 64u * k) * (uint32_t)sizeof(Canon));
+        } else {
+#pragma unroll
+            for (int k = 0; k < kItems; ++k) {
+                const uint32_t j = jb + 64u * k;
+                ev[k] = *reinterpret_cast<const uint2 *>(tb + (j < (uint32_t)nloc ? j : 0u) *
+                                                                  (uint32_t)sizeof(Canon));
+            }
+        }
+    };
 
-        // pass 1: surviving lengths and filled slots.  Each wave reads its 1024
-        // slots lane-contiguously (1 KiB per load instruction) into LDS; then
-        // every thread takes its 16 consecutive children from there.  s_len is
+    for (int j = threadIdx.x; j < 3 * kCntLds; j += kBlock) (&s_cnt[0][0])[j] = 0;
+    // a workgroup that sees no tiles draws no ticket, so every drawn ticket
+    // is processed even if workgroups disagree about an error raised meanwhile
+    int64_t t = ntiles > 0 ? next_ticket(ctl, &s_t) : ntiles;
+    int buf = 0;
+    if (t < ntiles) {
+        prepare(t, 0);
+        load_slots(t);
+    }
+    while (t < ntiles) {
+        __syncthreads();                    // s_p / s_off of this tile, cleared counts
+        const int64_t ct0 = t * kTile;
+        const int64_t ct1 = min64(ct0 + kTile, N);
+        const int64_t pf = s_p[buf][0], pl = s_p[buf][1], q0t = s_p[buf][2];
+        const int64_t Rp = pl - pf + 1;
+        const int64_t R = min64(Rp, kCntLds);
+        const bool lds_ok = Rp <= kTile;
+        const int16_t *so = s_off[buf];
+
+        // pass 1: surviving lengths and filled slots into LDS; then every
+        // thread takes its 16 consecutive children from there.  s_len is
         // padded by one word per 16 so that both access patterns are free of
         // bank conflicts.
         {
-            const int wv = (int)(threadIdx.x >> 6), ln = lane_id();
+            const int nloc = (int)(ct1 - ct0);
+            const int jb = wv * (64 * kItems) + ln;
+            const int lb = jb + (jb >> 4);          // s_len index of child jb + 64 k is lb + 68 k
 #pragma unroll
             for (int k = 0; k < kItems; ++k) {
-                const int j = wv * (64 * kItems) + k * 64 + ln;
-                const int64_t c = ct0 + j;
                 uint32_t L = 0, S = 4;        // state, or 4 = not reported in this call
-                if (c < ct1) {
-                    const Canon e = canon[c];
-                    if ((e.tag >> 2) == epoch) {
-                        S = e.tag & 3u;
-                        L = S == RO_SUCCESS ? e.len : 0;
-                    }
+                if (jb + k * 64 < nloc && (ev[k].y >> 2) == epoch) {
+                    S = ev[k].y & 3u;
+                    L = S == RO_SUCCESS ? ev[k].x : 0;
                 }
-                s_len[j + (j >> 4)] = L;
-                s_st[j] = (uint8_t)S;
+                s_len[lb + 68 * k] = L;
+                s_st[jb + 64 * k] = (uint8_t)S;
             }
         }
         __syncthreads();
         const int64_t c0 = ct0 + (int64_t)threadIdx.x * kItems;
-        uint32_t len[kItems];
-        uint32_t stv[kItems];
+        const int lj = (int)threadIdx.x * kItems + (int)threadIdx.x;      // s_len index of c0
+        uint32_t sw[4];                     // the thread's 16 state bytes, four per word
         int64_t sum = 0, filled = 0;
         {
             const uint4 sv = *reinterpret_cast<const uint4 *>(&s_st[threadIdx.x * kItems]);
-            const uint32_t sw[4] = {sv.x, sv.y, sv.z, sv.w};
+            sw[0] = sv.x;
+            sw[1] = sv.y;
+            sw[2] = sv.z;
+            sw[3] = sv.w;
 #pragma unroll
             for (int k = 0; k < kItems; ++k) {
-                const int j = (int)threadIdx.x * kItems + k;
-                len[k] = s_len[j + (j >> 4)];
-                stv[k] = (sw[k >> 2] >> (8 * (k & 3))) & 0xffu;
-                filled += stv[k] < 4 ? 1 : 0;
-                sum += len[k];
+                sum += s_len[lj + k];
+                filled += ((sw[k >> 2] >> (8 * (k & 3))) & 0xffu) < 4 ? 1 : 0;
             }
         }
         filled_total += filled;
         int64_t tot;
         const int64_t ex = block_excl_scan(sum, s_wave, tot);
-        const uint64_t pre = tile_prefix(desc, t, sepoch, (uint64_t)tot, &s_b, ctl);
+        const uint64_t pre = tile_prefix_inl(desc, t, sepoch, (uint64_t)tot, &s_b, ctl);
         const int64_t base = (int64_t)pre + ex;
         if ((threadIdx.x % (kSub / kItems)) == 0) {
             const int64_t sb = t * (kTile / kSub) + threadIdx.x / (kSub / kItems);
             sub_base[sb] = base;                    // first byte of each copy sub-tile
+        }
+        if (t == ntiles - 1 && threadIdx.x == 0) {
+            ctl->total = (int64_t)pre + tot;
+            if (pre >= kSat) raise_err(ctl, RO_EOVERFLOW);
+        }
+
+        // the next tile: ticket, parents, and its slot loads in flight
+        const int64_t t_next = next_ticket(ctl, &s_t);
+        if (t_next < ntiles) {
+            prepare(t_next, buf ^ 1);
+            load_slots(t_next);
         }
 
         // pass 2: parents -- slot offsets and run-length counts
@@ -288,27 +341,28 @@ __global__ __launch_bounds__(kBlock) void k_gather_scan(
             int64_t pos = base;
             if (lds_ok) {
                 const int r0 = (int)(c0 - ct0), rend = (int)(ct1 - ct0);
-                int j = lds_last_le(s_off, 0, (int)Rp, r0);
-                if (s_off[j] == r0 && out_off) {
+                int j = lds_last_le(so, 0, (int)Rp, r0);
+                if (so[j] == r0 && out_off) {
                     // every parent whose first child is c0 (empty ones included)
-                    const int64_t qa = r0 == 0 ? q0t : pf + lds_first_ge(s_off, 1, j + 1, r0);
+                    const int64_t qa = r0 == 0 ? q0t : pf + lds_first_ge(so, 1, j + 1, r0);
                     for (int64_t q = qa; q <= pf + j; ++q) out_off[q] = pos;
                 }
-                int next = s_off[j + 1];
+                int next = so[j + 1];
                 for (int k = 0; k < kItems; ++k) {
                     const int rc = r0 + k;
                     if (rc >= rend) break;
                     if (rc >= next) {
                         flush(pf + j);
-                        const int jn = lds_last_le(s_off, j + 1, (int)Rp, rc);
+                        const int jn = lds_last_le(so, j + 1, (int)Rp, rc);
                         if (out_off)
                             for (int64_t q = pf + j + 1; q <= pf + jn; ++q) out_off[q] = pos;
                         j = jn;
-                        next = s_off[j + 1];
+                        next = so[j + 1];
                     }
-                    if (stv[k] < 3) run[stv[k]] += 1;
+                    const uint32_t sk = (sw[k >> 2] >> (8 * (k & 3))) & 0xffu;
+                    if (sk < 3) run[sk] += 1;
                     if (cdst) cdst[c0 + k] = pos;
-                    pos += len[k];
+                    pos += s_len[lj + k];
                 }
                 flush(pf + j);
             } else {
@@ -330,9 +384,10 @@ __global__ __launch_bounds__(kBlock) void k_gather_scan(
                         p = pn;
                         next = offsets[p + 1];
                     }
-                    if (stv[k] < 3) run[stv[k]] += 1;
+                    const uint32_t sk = (sw[k >> 2] >> (8 * (k & 3))) & 0xffu;
+                    if (sk < 3) run[sk] += 1;
                     if (cdst) cdst[c] = pos;
-                    pos += len[k];
+                    pos += s_len[lj + k];
                 }
                 flush(p);
             }
@@ -345,12 +400,10 @@ __global__ __launch_bounds__(kBlock) void k_gather_scan(
                 if (v && cnt_out[s]) atomicAdd(&cnt_out[s][pf + j], v);
             }
         }
-        if (t == ntiles - 1 && threadIdx.x == 0) {
-            const int64_t total = (int64_t)pre + tot;
-            ctl->total = total;
-            if (pre >= kSat) raise_err(ctl, RO_EOVERFLOW);
-        }
         __syncthreads();
+        for (int j = threadIdx.x; j < 3 * kCntLds; j += kBlock) (&s_cnt[0][0])[j] = 0;
+        t = t_next;
+        buf ^= 1;
     }
     const int64_t f = block_sum(filled_total, s_wave);
     if (threadIdx.x == 0 && f)
@@ -525,7 +578,7 @@ hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w
               a.nk, a.barrier, w.gkey, L.ctl);
     // three workgroups per CU drew tickets faster than four (fewer waiting
     // on the look-back at once) and two left the largest scans short of work
-    const int64_t grid_s = (int64_t)L.num_cus * 3;
+    const int64_t grid_s = (int64_t)L.num_cus * RO_SCAN_WG;
     RO_LAUNCH(L, RO_K_GATHER_SCAN, k_gather_scan, dim3((unsigned)grid_s), dim3(kBlock), 0, L.stream, a.offsets, a.P,
               w.canon, w.canon_cap, a.out_off, a.ns, a.nf, a.nk, a.cdst, w.sub_base, L.ctl, L.desc, L.desc_cap);
     int64_t grid_f = (a.P + kBlock - 1) / kBlock;

@@ -217,8 +217,8 @@ __device__ __forceinline__ uint64_t lookback_wave(uint64_t *desc, int64_t t, uin
 
 // Exclusive prefix of tile t given its aggregate; called by every thread of
 // the workgroup, returns the same value to all of them.
-__device__ __noinline__ uint64_t tile_prefix(uint64_t *desc, int64_t t, uint32_t epoch,
-                                             uint64_t agg, uint64_t *s_b, Ctl *ctl)
+__device__ __forceinline__ uint64_t tile_prefix_inl(uint64_t *desc, int64_t t, uint32_t epoch,
+                                                   uint64_t agg, uint64_t *s_b, Ctl *ctl)
 {
     if (threadIdx.x < 64) {
         const uint64_t r = lookback_wave(desc, t, epoch, agg, ctl);
@@ -228,6 +228,15 @@ __device__ __noinline__ uint64_t tile_prefix(uint64_t *desc, int64_t t, uint32_t
     uint64_t r = *s_b;
     __syncthreads();
     return r;
+}
+
+// The same out of line, so that the look-back's registers do not add to the
+// caller's (a call waits for every load the caller has in flight; the inline
+// form above does not).
+__device__ __noinline__ uint64_t tile_prefix(uint64_t *desc, int64_t t, uint32_t epoch,
+                                             uint64_t agg, uint64_t *s_b, Ctl *ctl)
+{
+    return tile_prefix_inl(desc, t, epoch, agg, s_b, ctl);
 }
 
 // Two independent look-back chains of tile t at once, one wave each;

@@ -171,7 +171,9 @@ int ro_expand_noalloc(void *hip_stream, const int32_t *counts, int64_t n_parents
  * ceil(M/B) are written to the device scalars *n_out_dev and *n_batches_dev
  * (either may be NULL).  With a group-failure barrier ([n_parents], may be
  * NULL), an entry whose parent is barred is not ready: it is suppressed
- * before dispatch and takes no slot. */
+ * before dispatch and takes no slot.  The tag arrays (out_cap entries each)
+ * must not share memory with the queue, the mask, the offsets, the barrier
+ * or one another (RO_EINVAL, checked on the host). */
 int ro_batch(ro_ctx *ctx, const uint32_t *queue, const uint8_t *keep, int64_t q_len,
              const int64_t *offsets, int64_t n_parents, int32_t batch_size,
              uint32_t *out_child, uint32_t *out_parent, uint32_t *out_ordinal, int64_t out_cap,
@@ -181,7 +183,8 @@ int ro_batch(ro_ctx *ctx, const uint32_t *queue, const uint8_t *keep, int64_t q_
  * Grains"): each reservation takes up to B siblings of the first ready
  * parent, the parent of the earliest entry still queued, and every other
  * entry keeps its place.  Ready entries, ids, tags, barrier and errors as in
- * ro_batch; reservations run until the queue is empty.  Reservation j is
+ * ro_batch (batch_off, too, may share no memory with the inputs or tag
+ * arrays); reservations run until the queue is empty.  Reservation j is
  * slots [batch_off[j], batch_off[j+1]) (int64, device; batch_off[n_batches]
  * = M), so it needs n_batches + 1 <= batch_cap (RO_ECAP; n_batches <= M).
  * M and n_batches go to *n_out_dev and *n_batches_dev (either may be

@@ -68,7 +68,10 @@ hipError_t launch_gf_fold(const Launch &L, const uint8_t *rs, const uint32_t *rp
 }
 
 // ---------------------------------------------------------------- scatter
-constexpr int kScatterItems = 2;            // reports per thread and step
+#ifndef RO_SCATTER_ITEMS
+#define RO_SCATTER_ITEMS 2
+#endif
+constexpr int kScatterItems = RO_SCATTER_ITEMS;   // reports per thread and step
 // With a group-failure barrier, reports commit in report order: one of a
 // barred parent, or one after its parent's first group failure in this
 // call, is rejected; an accepted group failure is a failed member.

@@ -379,7 +379,10 @@ __global__ __launch_bounds__(kBlock) void k_emit_scan(
 // positions, not a re-read of slot records, so small units pay here); a unit
 // finds its first child by a wave search over the output positions and takes
 // the children it covers 256 at a time, each clipped to the unit.
-constexpr int64_t kEmitMinUnit = 1024;
+#ifndef RO_EMIT_MIN_UNIT
+#define RO_EMIT_MIN_UNIT 1024
+#endif
+constexpr int64_t kEmitMinUnit = RO_EMIT_MIN_UNIT;
 #ifndef RO_EMIT_STEPS
 #define RO_EMIT_STEPS 4
 #endif

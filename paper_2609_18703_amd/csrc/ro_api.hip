@@ -95,6 +95,33 @@ namespace {
 
 int hip_fail(hipError_t e) { return e == hipSuccess ? RO_OK : RO_EHIP; }
 
+// Byte ranges [a, a + na) and [b, b + nb) share a byte (NULL or empty: never).
+bool overlap(const void *a, int64_t na, const void *b, int64_t nb)
+{
+    if (!a || !b || na <= 0 || nb <= 0) return false;
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return x < y + (uintptr_t)nb && y < x + (uintptr_t)na;
+}
+
+// The batch kernels read the queue, mask, offsets and barrier and write the
+// tag arrays through restrict-qualified pointers: a tag array that shares
+// memory with any of those, or with another tag array, is rejected.
+bool batch_outputs_alias(const uint32_t *queue, const uint8_t *keep, int64_t q_len, const int64_t *offsets,
+                         int64_t P, const uint8_t *barrier, uint32_t *const outs[3], int64_t out_cap,
+                         const void *extra, int64_t extra_bytes)
+{
+    for (int i = 0; i < 3; ++i) {
+        const int64_t nb = out_cap * 4;
+        if (overlap(outs[i], nb, queue, q_len * 4) || overlap(outs[i], nb, keep, q_len) ||
+            overlap(outs[i], nb, offsets, (P + 1) * 8) || overlap(outs[i], nb, barrier, P) ||
+            overlap(outs[i], nb, extra, extra_bytes))
+            return true;
+        for (int j = i + 1; j < 3; ++j)
+            if (overlap(outs[i], nb, outs[j], nb)) return true;
+    }
+    return false;
+}
+
 Launch launch_of(ro_ctx *c)
 {
     Launch L;
@@ -378,6 +405,9 @@ int ro_batch(ro_ctx *c, const uint32_t *queue, const uint8_t *keep, int64_t q_le
     if (!c || !offsets || q_len < 0 || n_parents < 0 || batch_size <= 0 || out_cap < 0 ||
         (q_len > 0 && !queue))
         return RO_EINVAL;
+    uint32_t *const outs[3] = {out_child, out_parent, out_ordinal};
+    if (batch_outputs_alias(queue, keep, q_len, offsets, n_parents, barrier, outs, out_cap, nullptr, 0))
+        return RO_EINVAL;
     int rc = ensure_desc(c, tiles_for(q_len));
     if (rc) return rc;
     return hip_fail(launch_batch(launch_of(c), queue, keep, q_len, offsets, n_parents, batch_size,
@@ -394,6 +424,13 @@ int ro_batch_parent(ro_ctx *c, const uint32_t *queue, const uint8_t *keep, int64
         batch_cap < 1 || (q_len > 0 && !queue))
         return RO_EINVAL;
     if (q_len >= ((int64_t)1 << 32) || n_parents >= ((int64_t)1 << 32)) return RO_EINVAL;
+    uint32_t *const outs[3] = {out_child, out_parent, out_ordinal};
+    if (batch_outputs_alias(queue, keep, q_len, offsets, n_parents, barrier, outs, out_cap, batch_off,
+                            batch_cap * 8) ||
+        overlap(batch_off, batch_cap * 8, queue, q_len * 4) || overlap(batch_off, batch_cap * 8, keep, q_len) ||
+        overlap(batch_off, batch_cap * 8, offsets, (n_parents + 1) * 8) ||
+        overlap(batch_off, batch_cap * 8, barrier, n_parents))
+        return RO_EINVAL;
     int rc = ensure_pb(c, q_len, n_parents);
     if (rc) return rc;
     rc = ensure_desc(c, tiles_for(q_len));
@@ -650,9 +687,12 @@ int ro_stream_batch(ro_ctx *c, ro_stream *s, const uint32_t *queue, const uint8_
 {
     if (!c || !s || s->ctx != c || q_len < 0 || batch_size <= 0 || out_cap < 0 || (q_len > 0 && !queue))
         return RO_EINVAL;
+    const StreamState &st = s->st;
+    uint32_t *const outs[3] = {out_child, out_parent, out_ordinal};
+    if (batch_outputs_alias(queue, keep, q_len, st.offsets, st.P, st.barrier, outs, out_cap, nullptr, 0))
+        return RO_EINVAL;
     int rc = ensure_desc(c, tiles_for(q_len));
     if (rc) return rc;
-    const StreamState &st = s->st;
     return hip_fail(launch_batch(launch_of(c), queue, keep, q_len, st.offsets, st.P, batch_size, out_child,
                                  out_parent, out_ordinal, out_cap, n_out_dev, n_batches_dev, nullptr, 0, st.barrier,
                                  st.cpar, st.N));

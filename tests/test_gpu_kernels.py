@@ -146,6 +146,17 @@ def test_batch_unaligned_and_errors(ctx):
     assert ctx.status() == O.ERANGE
     ctx.batch(D.to_dev(queue.view(np.int32)), None, D.to_dev(offs), 7, None, op, None, out_cap=10)
     assert ctx.status() == O.ECAP
+    # tag arrays that share memory with an input or with each other are
+    # rejected on the host, before anything is enqueued
+    from paper_2609_18703_amd.ro import RoError
+    d_q = D.to_dev(queue.view(np.int32))
+    d_offs = D.to_dev(offs)
+    for args in ((None, d_q[N // 2:], None), (op, op, None), (None, op, op[N // 8:]),
+                 (None, d_offs.view(torch.int32), None)):
+        with pytest.raises(RoError) as e:
+            ctx.batch(d_q, None, d_offs, 7, *args, out_cap=N // 4)
+        assert e.value.code == O.EINVAL
+    assert ctx.status() == O.OK
 
 
 # ------------------------------------------------------------------ gather

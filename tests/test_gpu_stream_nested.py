@@ -281,8 +281,12 @@ def test_stream_batch_matches_batch_and_oracle(ctx):
             assert np.array_equal(_u32(oo, m), want[2]), wave
         bar.zero_()
         bad = np.array([0, N, 3], np.uint32)
-        t = torch.zeros(3, dtype=torch.int32, device="cuda")
-        st.batch(_i32(bad), None, 4, t, t, t)
+        t = torch.zeros(9, dtype=torch.int32, device="cuda")
+        st.batch(_i32(bad), None, 4, t[0:3], t[3:6], t[6:9])
         assert ctx.status() == R.ERANGE
+        # tag arrays sharing memory are rejected on the host
+        with pytest.raises(R.RoError) as e:
+            st.batch(_i32(bad), None, 4, t[0:3], t[2:5], None)
+        assert e.value.code == R.EINVAL
     finally:
         st.close()

@@ -220,10 +220,17 @@ def _make_reports(rng, counts, p_report=1.0, states=(0, 0, 0, 1, 2), lens=LENS):
     return par, ordi, st, off, data
 
 
-@pytest.mark.parametrize("case", ["small", "zeros", "multi_tile", "partial", "pending", "big_parent"])
+@pytest.mark.parametrize("case", ["small", "zeros", "multi_tile", "partial", "pending", "big_parent", "empty_runs"])
 def test_gather_matches_oracle(ctx, case):
     rng = np.random.default_rng(len(case))
-    if case == "small":
+    if case == "empty_runs":
+        # runs of thousands of empty parents: some 4,096-child scan tiles span
+        # more parents than a tile holds children (their parent search runs
+        # in global memory) and more than its LDS count slots
+        counts = np.concatenate([rng.integers(1, 40, 300), np.zeros(7000), rng.integers(0, 3, 5000),
+                                 np.zeros(12000), [5000], np.zeros(3000), rng.integers(0, 5, 2000),
+                                 np.zeros(4500)]).astype(np.int32)
+    elif case == "small":
         counts = np.array([3, 1, 4], np.int32)
     elif case == "zeros":
         counts = np.array([0, 2, 0, 0, 5, 0, 1, 0], np.int32)

@@ -218,6 +218,23 @@ def test_stream_mixed_states_and_empty_parents(ctx, seed):
     assert set(range(7)) <= set(got[0]["parent"].tolist())
 
 
+def test_stream_empty_runs(ctx):
+    """Runs of thousands of empty parents: the first emission's 1,024-child
+    scan tiles span more emitted parents than they hold children (their
+    parent search runs in global memory), and later waves emit parents far
+    apart."""
+    rng = np.random.default_rng(33)
+    counts = np.concatenate([rng.integers(1, 5, 500), np.zeros(3000), rng.integers(0, 3, 2000), np.zeros(5000),
+                             [3000], np.zeros(2000), rng.integers(0, 4, 800)]).astype(np.int32)
+    N = int(counts.sum())
+    parts = np.split(rng.permutation(N).astype(np.uint32), [N // 4, N // 2, (3 * N) // 4])
+    waves = [(ids, rng.choice(np.array([0, 0, 0, 1, 2], np.uint8), len(ids)),
+              rng.choice(np.array([0, 1, 16, 33, 200], np.int64), len(ids))) for ids in parts]
+    _say("stream empty runs", len(counts), N, [len(p) for p in parts])
+    got = _stream_case(ctx, counts, waves, B=64)
+    assert set(np.flatnonzero(counts == 0).tolist()) <= set(got[0]["parent"].tolist())
+
+
 def test_stream_single_wave_equals_gather(ctx):
     """One wave holding every report emits every parent: the same slots as a
     one-shot gather."""

@@ -383,6 +383,13 @@ __global__ __launch_bounds__(kBlock) void k_emit_scan(
 #define RO_EMIT_MIN_UNIT 1024
 #endif
 constexpr int64_t kEmitMinUnit = RO_EMIT_MIN_UNIT;
+#ifndef RO_EMIT_GRID
+#define RO_EMIT_GRID 4                      // emission copy workgroups per CU
+#endif
+#ifndef RO_EMIT_UNITS
+#define RO_EMIT_UNITS 1                     // byte units per wave of the grid
+#endif
+constexpr int64_t kEmitUnits = RO_EMIT_UNITS;
 #ifndef RO_EMIT_STEPS
 #define RO_EMIT_STEPS 4
 #endif
@@ -419,7 +426,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     const uint64_t outa = reinterpret_cast<uint64_t>(out);
     const int64_t mis = (int64_t)(outa & 15);
     const int64_t nwaves = (int64_t)gridDim.x * kWaves;
-    int64_t G = (T + nwaves * kCopyUnits - 1) / (nwaves * kCopyUnits);
+    int64_t G = (T + nwaves * kEmitUnits - 1) / (nwaves * kEmitUnits);
     G = (G + 15) & ~(int64_t)15;
     G = G < kEmitMinUnit ? kEmitMinUnit : (G > ((int64_t)1 << 30) ? ((int64_t)1 << 30) : G);
     const int64_t nunits = (T + mis + G - 1) / G;
@@ -540,7 +547,7 @@ hipError_t launch_stream_emit(const Launch &L, StreamState &s, uint32_t *emit_pa
     const int64_t grid_s = (int64_t)L.num_cus * 2;
     RO_LAUNCH(L, RO_K_STREAM_SCAN, k_emit_scan, dim3((unsigned)grid_s), dim3(kBlock), 0, L.stream, s.evoff,
               s.ebase, s.canon, s.edst, s.esrc, emit_off, s.ecnt, es, s.run_epoch, L.ctl, L.desc, L.desc_cap);
-    const int64_t grid_c = (int64_t)L.num_cus * 8;
+    const int64_t grid_c = (int64_t)L.num_cus * RO_EMIT_GRID;
     RO_LAUNCH(L, RO_K_STREAM_COPY, k_emit_out, dim3((unsigned)grid_c), dim3(kBlock), 0, L.stream, emit_off,
               s.evoff, s.ecnt, es, s.ebar, ns, nf, nk, pstate, n_bytes, s.edst, s.esrc, emit_data, cap_bytes, L.ctl);
     return hipGetLastError();

@@ -592,7 +592,7 @@ hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w
     if (a.out_data != nullptr) {
         // many small workgroups: a unit's cost varies with the records it
         // meets, and a deep queue of workgroups evens out the tail
-        const int64_t grid_c = (int64_t)L.num_cus * 32;
+        const int64_t grid_c = (int64_t)L.num_cus * RO_COPY_GRID;
         RO_LAUNCH(L, RO_K_GATHER_COPY, k_gather_copy, dim3((unsigned)grid_c), dim3(kBlock), 0, L.stream, a.offsets,
                   a.P, w.canon, w.canon_cap, w.sub_base, a.out_data, a.out_data == a.data ? 1 : 0, L.ctl);
     }

@@ -215,6 +215,9 @@ __device__ __forceinline__ void copy_window_nb(const int32_t *s_dst, const uint6
 #ifndef RO_COPY_STEPS
 #define RO_COPY_STEPS 6
 #endif
+#ifndef RO_COPY_GRID
+#define RO_COPY_GRID 32                     // gather copy workgroups per CU
+#endif
 #ifndef RO_COPY_UNITS
 #define RO_COPY_UNITS 2
 #endif

@@ -13,15 +13,27 @@
 
 namespace ro {
 
-// Coarse child -> parent map, one 8-byte entry per block of 128 children:
-// for block j, x = the parent p0 of child 128j, with bit 31 set when the
-// whole block lies in p0, and y = the ordinal of child 128j in p0.  A child of
-// a one-parent block has its tags from its entry alone; any other child's
+// Coarse child -> parent map, one 8-byte entry per block of 2^s children:
+// for block j, x = the parent p0 of child j 2^s, with bit 31 set when the
+// whole block lies in p0, and y = the ordinal of child j 2^s in p0.  A child
+// of a one-parent block has its tags from its entry alone; any other child's
 // parent lies between p0 and the next entry's parent, and the search for it
-// starts from offsets[p0] = 128j - y without reading it.  Built for fewer
+// starts from offsets[p0] = j 2^s - y without reading it.  Built for fewer
 // than 2^31 parents (the flag bit); otherwise the offsets are searched whole.
-constexpr int kMapShift = 7;
+// The block size follows the mean fan-out N / P (map_shift): blocks of 16
+// children for small parents keep the searches short, blocks of 128 for
+// large ones keep the map small enough to stay in cache (workload 2, mean
+// 411: 128; the documents' levels, means 9 and 15: 16).
 constexpr uint32_t kMapOne = 0x80000000u;
+
+// log2 of the children per map block: the smallest power of two from 16 to
+// 128 that is at least the mean number of children per parent.
+__device__ __forceinline__ int map_shift(int64_t N, int64_t P)
+{
+    int s = 4;
+    while (s < 7 && ((int64_t)1 << s) * P < N) ++s;
+    return s;
+}
 
 // entries of a thread whose lookups are in flight together
 #ifndef RO_BATCH_LOOKUPS
@@ -32,13 +44,14 @@ __global__ void k_batch_cmap(const int64_t *__restrict__ offsets, int64_t P, uin
                              int64_t map_cap)
 {
     const int64_t N = offsets[P];
-    int64_t nmap = (N + (1 << kMapShift) - 1) >> kMapShift;
+    const int sh = map_shift(N, P);
+    int64_t nmap = (N + (1 << sh) - 1) >> sh;
     nmap = nmap < map_cap ? nmap : map_cap;
     for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < nmap;
          j += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t c0 = j << kMapShift;
+        const int64_t c0 = j << sh;
         const int64_t p0 = upper_bound_g(offsets, 0, P + 1, c0) - 1;
-        const int64_t last = c0 + (1 << kMapShift) - 1 < N ? c0 + (1 << kMapShift) - 1 : N - 1;
+        const int64_t last = c0 + (1 << sh) - 1 < N ? c0 + (1 << sh) - 1 : N - 1;
         const bool one = offsets[p0 + 1] > last;
         map[j] = make_uint2((uint32_t)p0 | (one ? kMapOne : 0u), (uint32_t)(c0 - offsets[p0]));
     }
@@ -50,7 +63,7 @@ __global__ void k_batch_cmap(const int64_t *__restrict__ offsets, int64_t P, uin
 // binary search for the children of blocks that hold several parents (or
 // that lie past the map).  Needs P < 2^31 when nmap > 0.
 template <int K>
-__device__ __forceinline__ void tags_of(const uint2 *__restrict__ map, int64_t nmap,
+__device__ __forceinline__ void tags_of(const uint2 *__restrict__ map, int64_t nmap, int sh,
                                         const int64_t *__restrict__ offsets, int64_t P, const uint32_t (&c)[K],
                                         uint32_t live, uint32_t (&par)[K], uint32_t (&ord)[K])
 {
@@ -74,14 +87,14 @@ __device__ __forceinline__ void tags_of(const uint2 *__restrict__ map, int64_t n
         uint32_t hx[K];
 #pragma unroll
         for (int k = 0; k < K; ++k) {
-            const int64_t j = (int64_t)(c[k] >> kMapShift);
+            const int64_t j = (int64_t)(c[k] >> sh);
             const int64_t jj = (((live >> k) & 1u) && j < nmap) ? j : 0;
             e[k] = map[jj];
             hx[k] = map[jj + 1 < nmap ? jj + 1 : jj].x;
         }
 #pragma unroll
         for (int k = 0; k < K; ++k) {
-            const int64_t j = (int64_t)(c[k] >> kMapShift);
+            const int64_t j = (int64_t)(c[k] >> sh);
             const uint32_t p0 = e[k].x & ~kMapOne;
             const uint32_t hi = j + 1 < nmap ? (hx[k] & ~kMapOne) : (uint32_t)(P - 1);
             if (((live >> k) & 1u) == 0) {
@@ -94,7 +107,7 @@ __device__ __forceinline__ void tags_of(const uint2 *__restrict__ map, int64_t n
                 vl[k] = off0;
             } else {
                 l[k] = p0;
-                vl[k] = (j << kMapShift) - (int64_t)e[k].y;
+                vl[k] = (j << sh) - (int64_t)e[k].y;
                 h[k] = (e[k].x & kMapOne) ? p0 + 1 : hi + 1;
             }
         }
@@ -148,7 +161,8 @@ __global__ __launch_bounds__(kBlock) void k_batch(
     __shared__ int64_t s_t;
     __shared__ int32_t s_last;
     const int64_t N = cpar ? min64(offsets[P], cpar_n) : offsets[P];   // ids past the map are out of range
-    int64_t nmap = (N + (1 << kMapShift) - 1) >> kMapShift;
+    const int sh = map_shift(offsets[P], P);     // the map's block size, as k_batch_cmap built it
+    int64_t nmap = (N + (1 << sh) - 1) >> sh;
     nmap = nmap < cmap_cap ? nmap : cmap_cap;
     const bool want_tags = out_parent != nullptr || out_ordinal != nullptr;
     for (;;) {
@@ -215,7 +229,7 @@ __global__ __launch_bounds__(kBlock) void k_batch(
                     uint32_t cc[H], pp[H], oo[H];
 #pragma unroll
                     for (int k = 0; k < H; ++k) cc[k] = q[hf * H + k];
-                    tags_of<H>(cmap, nmap, offsets, P, cc, (live >> (hf * H)) & ((1u << H) - 1u), pp, oo);
+                    tags_of<H>(cmap, nmap, sh, offsets, P, cc, (live >> (hf * H)) & ((1u << H) - 1u), pp, oo);
 #pragma unroll
                     for (int k = 0; k < H; ++k) {
                         if ((live >> (hf * H + k)) & 1u) {
@@ -295,7 +309,8 @@ __global__ __launch_bounds__(kBlock) void k_batch_keep(
     __shared__ int64_t s_t;
     __shared__ int32_t s_last;
     const int64_t N = offsets[P];
-    int64_t nmap = (N + (1 << kMapShift) - 1) >> kMapShift;
+    const int sh = map_shift(offsets[P], P);     // the map's block size, as k_batch_cmap built it
+    int64_t nmap = (N + (1 << sh) - 1) >> sh;
     nmap = nmap < cmap_cap ? nmap : cmap_cap;
     const bool want_tags = out_parent != nullptr || out_ordinal != nullptr;
     for (;;) {
@@ -367,7 +382,7 @@ __global__ __launch_bounds__(kBlock) void k_batch_keep(
                     uint32_t cc[H], pp[H], oo[H];
 #pragma unroll
                     for (int k = 0; k < H; ++k) cc[k] = q[hf * H + k];
-                    tags_of<H>(cmap, nmap, offsets, P, cc, (live >> (hf * H)) & ((1u << H) - 1u), pp, oo);
+                    tags_of<H>(cmap, nmap, sh, offsets, P, cc, (live >> (hf * H)) & ((1u << H) - 1u), pp, oo);
 #pragma unroll
                     for (int k = 0; k < H; ++k) {
                         if ((live >> (hf * H + k)) & 1u) {
@@ -445,7 +460,8 @@ __global__ __launch_bounds__(kBlock) void k_batch_all(
     int64_t *n_batches, const uint32_t *__restrict__ cpar, int64_t cpar_n, Ctl *ctl)
 {
     const int64_t N = cpar ? min64(offsets[P], cpar_n) : offsets[P];   // ids past the map are out of range
-    int64_t nmap = (N + (1 << kMapShift) - 1) >> kMapShift;
+    const int sh = map_shift(offsets[P], P);     // the map's block size, as k_batch_cmap built it
+    int64_t nmap = (N + (1 << sh) - 1) >> sh;
     nmap = nmap < cmap_cap ? nmap : cmap_cap;
     const bool want_tags = out_parent != nullptr || out_ordinal != nullptr;
     if (blockIdx.x == 0 && threadIdx.x == 0) {
@@ -486,7 +502,7 @@ __global__ __launch_bounds__(kBlock) void k_batch_all(
 #pragma unroll
                 for (int k = 0; k < kAllPer; ++k)
                     if (i0 + k * kBlock + threadIdx.x < Q && (int64_t)q[k] < N) live |= 1u << k;
-                tags_of<kAllPer>(cmap, nmap, offsets, P, q, live, par, ord);
+                tags_of<kAllPer>(cmap, nmap, sh, offsets, P, q, live, par, ord);
             }
         }
 #pragma unroll

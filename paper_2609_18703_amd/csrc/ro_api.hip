@@ -174,7 +174,7 @@ int ensure_canon(ro_ctx *c, int64_t children)
     c->cmap_cap = 0;
     const int64_t n = children > 0 ? children : 1;
     const int64_t subs = (n / kTile + 2) * (kTile / kSub);
-    const int64_t maps = (n >> 6) + 4;          // coarse map: 8 bytes per 128 children
+    const int64_t maps = (n >> 3) + 4;          // coarse map: 8 bytes per 16 to 128 children
     if (dev_alloc(&c->canon, n) != hipSuccess || dev_alloc(&c->sub_base, subs) != hipSuccess ||
         dev_alloc(&c->cmap, maps) != hipSuccess ||
         launch_zero_u64(launch_of(c), reinterpret_cast<uint64_t *>(c->canon),

@@ -540,6 +540,7 @@ def main():
     stream = torch.cuda.Stream()
     with torch.cuda.stream(stream):
         result = run(args)
+    result["device"] = _device_info(torch)
     print(json.dumps(result), flush=True)
 
 
@@ -556,6 +557,17 @@ def run(args):
         if second:
             result["docs_nested"]["cpu_baseline"] = cpu_baseline("docs-nested")
     return result
+
+
+def _device_info(torch):
+    """Which GPU unit ran the line: the same build has measured about 6% apart
+    on different MI355X units of one pool in its HBM-bound kernels."""
+    props = torch.cuda.get_device_properties(0)
+    info = {"name": props.name, "arch": getattr(props, "gcnArchName", "")}
+    uuid = getattr(props, "uuid", None)
+    if uuid is not None:
+        info["uuid"] = str(uuid)
+    return info
 
 
 def run_workload(args, workload):

@@ -26,6 +26,28 @@ namespace ro {
 // 411: 128; the documents' levels, means 9 and 15: 16).
 constexpr uint32_t kMapOne = 0x80000000u;
 
+// Tag outputs of a queue too long for the caches are written with
+// non-temporal stores: they are read once, by a later call, and kept out of
+// L2 they leave the coarse map and offsets there for this kernel's lookups
+// (workload 2's 41M-entry ready-queue batch 0.46 -> 0.42 ms, and the gather's
+// report scatter that reads them 1.55 -> 1.53 ms).  A shorter queue's tags
+// are stored normally: they then still sit in cache when the gather reads
+// them (the documents' 2.7M-entry batch).
+constexpr int64_t kTagNtEntries = (int64_t)8 << 20;   // 32 MB per tag array, the size of all L2s
+__device__ __forceinline__ void st_tag_nt(uint32_t *p, uint32_t v) { __builtin_nontemporal_store(v, p); }
+
+// The tile's staged outputs s_out[0, lim) to dst[base, base + lim): two
+// loops, since one store with a chosen hint is folded into a plain store.
+__device__ __forceinline__ void write_tags(uint32_t *__restrict__ dst, int64_t base, const uint32_t *s_out,
+                                           int64_t lim, bool nt)
+{
+    if (nt) {
+        for (int64_t j = threadIdx.x; j < lim; j += kBlock) st_tag_nt(dst + base + j, s_out[j]);
+    } else {
+        for (int64_t j = threadIdx.x; j < lim; j += kBlock) dst[base + j] = s_out[j];
+    }
+}
+
 // log2 of the children per map block: the smallest power of two from 16 to
 // 128 that is at least the mean number of children per parent.
 __device__ __forceinline__ int map_shift(int64_t N, int64_t P)
@@ -165,6 +187,7 @@ __global__ __launch_bounds__(kBlock) void k_batch(
     int64_t nmap = (N + (1 << sh) - 1) >> sh;
     nmap = nmap < cmap_cap ? nmap : cmap_cap;
     const bool want_tags = out_parent != nullptr || out_ordinal != nullptr;
+    const bool nt = Q > kTagNtEntries;
     for (;;) {
         const int64_t t = next_ticket(ctl, &s_t);
         if (t >= ntiles) break;
@@ -273,7 +296,7 @@ __global__ __launch_bounds__(kBlock) void k_batch(
                 }
             }
             __syncthreads();
-            for (int64_t j = threadIdx.x; j < lim; j += kBlock) dst[base + j] = s_out[j];
+            write_tags(dst, base, s_out, lim, nt);
             __syncthreads();
         }
         if (t == ntiles - 1 && threadIdx.x == 0) {
@@ -313,6 +336,7 @@ __global__ __launch_bounds__(kBlock) void k_batch_keep(
     int64_t nmap = (N + (1 << sh) - 1) >> sh;
     nmap = nmap < cmap_cap ? nmap : cmap_cap;
     const bool want_tags = out_parent != nullptr || out_ordinal != nullptr;
+    const bool nt = Q > kTagNtEntries;
     for (;;) {
         const int64_t t = next_ticket(ctl, &s_t);
         if (t >= nsuper) break;
@@ -408,7 +432,7 @@ __global__ __launch_bounds__(kBlock) void k_batch_keep(
                     }
                 }
                 __syncthreads();
-                for (int64_t j = threadIdx.x; j < lim; j += kBlock) dst[base + j] = s_out[j];
+                write_tags(dst, base, s_out, lim, nt);
                 __syncthreads();
             }
         }

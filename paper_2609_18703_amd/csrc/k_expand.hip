@@ -61,6 +61,10 @@ __global__ __launch_bounds__(kBlock) void k_expand_scan(const int32_t *__restric
 // consecutive children, finds the parent of the first one by binary search
 // and walks forward, so a huge parent is spread over as many threads as it
 // has children/16 and never serialises a wave.
+// Expansions of more children than this write their tags with
+// non-temporal stores (32 MB per tag array, the size of all L2s).
+constexpr int64_t kTagsNtChildren = (int64_t)8 << 20;
+
 __global__ __launch_bounds__(kBlock) void k_expand_tags(const int64_t *__restrict__ offsets, int64_t P,
                                                         uint32_t *__restrict__ child_parent,
                                                         uint32_t *__restrict__ child_ordinal,
@@ -71,6 +75,7 @@ __global__ __launch_bounds__(kBlock) void k_expand_tags(const int64_t *__restric
     const int64_t N = offsets[P];
     if (N > child_cap || N >= ((int64_t)1 << 32)) return;     // reported by the scan
     const int lane = lane_id();
+    const bool nt = N > kTagsNtChildren;
     uint32_t *stage = s_stage[threadIdx.x >> 6];
     const int64_t nwaves = (int64_t)gridDim.x * (kBlock / 64);
     for (int64_t wt = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6); wt * kWaveSpan < N; wt += nwaves) {
@@ -108,10 +113,21 @@ __global__ __launch_bounds__(kBlock) void k_expand_tags(const int64_t *__restric
                     *reinterpret_cast<uint4 *>(&stage[lane * kItems + 4 * k]) =
                         make_uint4(v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]);
                 __builtin_amdgcn_wave_barrier();
-                uint4 *out = reinterpret_cast<uint4 *>(dst + cb);
+                if (nt) {
+                    // non-temporal: an expansion this large is not read back
+                    // soon, and its tags would only push other data out of L2
+                    typedef uint32_t t4 __attribute__((ext_vector_type(4)));
+                    t4 *out = reinterpret_cast<t4 *>(dst + cb);
 #pragma unroll
-                for (int k = 0; k < kItems / 4; ++k)
-                    out[k * 64 + lane] = *reinterpret_cast<const uint4 *>(&stage[(k * 64 + lane) * 4]);
+                    for (int k = 0; k < kItems / 4; ++k)
+                        __builtin_nontemporal_store(*reinterpret_cast<const t4 *>(&stage[(k * 64 + lane) * 4]),
+                                                    out + k * 64 + lane);
+                } else {
+                    uint4 *out = reinterpret_cast<uint4 *>(dst + cb);
+#pragma unroll
+                    for (int k = 0; k < kItems / 4; ++k)
+                        out[k * 64 + lane] = *reinterpret_cast<const uint4 *>(&stage[(k * 64 + lane) * 4]);
+                }
                 __builtin_amdgcn_wave_barrier();
             }
         } else {

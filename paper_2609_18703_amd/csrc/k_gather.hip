@@ -112,11 +112,13 @@ __global__ __launch_bounds__(kBlock) void k_gather_scatter(
         for (int k = 0; k < U; ++k) {
             const int64_t i = b + k * gstride;
             const bool in = i < n;
-            sv[k] = in ? rs[i] : RO_PENDING;
-            pv[k] = in ? rp[i] : 0xffffffffu;
-            ov[k] = in ? ro_[i] : 0u;
-            o0v[k] = in ? roff[i] : 0;
-            o1v[k] = in ? roff[i + 1] : 0;
+            // the report columns are read once: non-temporal loads leave L2
+            // to the slots being written (workload 2's scatter 1.53 -> 1.45 ms)
+            sv[k] = in ? __builtin_nontemporal_load(rs + i) : RO_PENDING;
+            pv[k] = in ? __builtin_nontemporal_load(rp + i) : 0xffffffffu;
+            ov[k] = in ? __builtin_nontemporal_load(ro_ + i) : 0u;
+            o0v[k] = in ? __builtin_nontemporal_load(roff + i) : 0;
+            o1v[k] = in ? __builtin_nontemporal_load(roff + i + 1) : 0;
         }
 #pragma unroll
         for (int k = 0; k < U; ++k) {

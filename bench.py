@@ -561,7 +561,7 @@ def run(args):
 
 def _device_info(torch):
     """Which GPU unit ran the line: the same build has measured about 6% apart
-    on different MI355X units of one pool in its HBM-bound kernels."""
+    on different MI355X units in its HBM-bound kernels."""
     props = torch.cuda.get_device_properties(0)
     info = {"name": props.name, "arch": getattr(props, "gcnArchName", "")}
     uuid = getattr(props, "uuid", None)

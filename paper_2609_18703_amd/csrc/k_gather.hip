@@ -179,11 +179,17 @@ __global__ __launch_bounds__(kBlock) void k_gather_scatter(
 // current tile's pass 2 runs.  The current tile has posted its prefix before
 // the workgroup waits on anything for the next one, so the smallest tile not
 // yet posted always belongs to a workgroup that can post it.
+//
+// In place (the output is the report bytes themselves, as for an upper level
+// whose slots are the level below's output): nothing is copied, and the scan
+// checks that every surviving record already sits at its output position;
+// any other would overwrite bytes still to be read (RO_EINVAL).
+template <bool kInPlace>
 __global__ __launch_bounds__(kBlock) void k_gather_scan(
     const int64_t *__restrict__ offsets, int64_t P, const Canon *__restrict__ canon, int64_t canon_cap,
     int64_t *__restrict__ out_off, int32_t *__restrict__ ns, int32_t *__restrict__ nf,
-    int32_t *__restrict__ nk, int64_t *__restrict__ cdst, int64_t *__restrict__ sub_base, Ctl *ctl,
-    uint64_t *desc, int64_t desc_cap)
+    int32_t *__restrict__ nk, int64_t *__restrict__ cdst, int64_t *__restrict__ sub_base, const uint8_t *out,
+    Ctl *ctl, uint64_t *desc, int64_t desc_cap)
 {
     const uint32_t epoch = ctl->canon_epoch;
     const uint32_t sepoch = scan_epoch(ctl);
@@ -332,6 +338,13 @@ __global__ __launch_bounds__(kBlock) void k_gather_scan(
 
         // pass 2: parents -- slot offsets and run-length counts
         if (c0 < ct1) {
+            uint64_t srcv[kInPlace ? kItems : 1];
+            bool moved = false;
+            if constexpr (kInPlace) {
+#pragma unroll
+                for (int k = 0; k < kItems; ++k) srcv[k] = canon[min64(c0 + k, ct1 - 1)].src;
+            }
+            const uint64_t outa = reinterpret_cast<uint64_t>(out);
             int32_t run[3] = {0, 0, 0};
             auto flush = [&](int64_t p) {
 #pragma unroll
@@ -367,6 +380,7 @@ __global__ __launch_bounds__(kBlock) void k_gather_scan(
                     const uint32_t sk = (sw[k >> 2] >> (8 * (k & 3))) & 0xffu;
                     if (sk < 3) run[sk] += 1;
                     if (cdst) cdst[c0 + k] = pos;
+                    if constexpr (kInPlace) moved |= s_len[lj + k] != 0 && srcv[k] != outa + (uint64_t)pos;
                     pos += s_len[lj + k];
                 }
                 flush(pf + j);
@@ -392,10 +406,12 @@ __global__ __launch_bounds__(kBlock) void k_gather_scan(
                     const uint32_t sk = (sw[k >> 2] >> (8 * (k & 3))) & 0xffu;
                     if (sk < 3) run[sk] += 1;
                     if (cdst) cdst[c] = pos;
+                    if constexpr (kInPlace) moved |= s_len[lj + k] != 0 && srcv[k] != outa + (uint64_t)pos;
                     pos += s_len[lj + k];
                 }
                 flush(p);
             }
+            if (moved) raise_err(ctl, RO_EINVAL);
         }
         __syncthreads();
         for (int64_t j = threadIdx.x; j < R; j += kBlock) {
@@ -485,7 +501,7 @@ __device__ __forceinline__ int64_t find_sub_tile(const int64_t *__restrict__ sub
 // long, and few parents or many.
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_WAVES))) void k_gather_copy(
     const int64_t *__restrict__ offsets, int64_t P, const Canon *__restrict__ canon, int64_t canon_cap,
-    const int64_t *__restrict__ sub_base, uint8_t *__restrict__ out, int in_place, Ctl *ctl)
+    const int64_t *__restrict__ sub_base, uint8_t *__restrict__ out, Ctl *ctl)
 {
     constexpr int kWaves = kBlock / 64;
     const uint32_t epoch = ctl->canon_epoch;
@@ -543,24 +559,13 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_
             const int64_t ws = max64(lo - D0, 0), we = min64(hi - D0, tot);
             if (we > ws) {
                 int64_t run = inc - lsum;
-                bool moves = false;
 #pragma unroll
                 for (int k = 0; k < kCopyPer; ++k) {
                     const int r = lane * kCopyPer + k;
                     const int64_t cs = min64(max64(run, ws), we);
-                    const int64_t ce = min64(max64(run + (int64_t)l[k], ws), we);
-                    const uint64_t src = s[k] + (uint64_t)(cs - run);
                     s_dst[r] = (int32_t)(cs - ws);
-                    s_src[r] = src;
-                    moves |= ce > cs && src != outa + (uint64_t)(D0 + cs);
+                    s_src[r] = s[k] + (uint64_t)(cs - run);
                     run += l[k];
-                }
-                if (in_place) {
-                    // output aliases the report bytes: records that already
-                    // sit at their output position need no copy, any other
-                    // would overwrite bytes still to be read
-                    if (__ballot(moves) != 0 && lane == 0) raise_err(ctl, RO_EINVAL);
-                    continue;
                 }
                 if (lane == 0) s_dst[kSub] = (int32_t)(we - ws);
                 __builtin_amdgcn_wave_barrier();
@@ -584,19 +589,29 @@ hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w
     // three workgroups per CU drew tickets faster than four (fewer waiting
     // on the look-back at once) and two left the largest scans short of work
     const int64_t grid_s = (int64_t)L.num_cus * RO_SCAN_WG;
-    RO_LAUNCH(L, RO_K_GATHER_SCAN, k_gather_scan, dim3((unsigned)grid_s), dim3(kBlock), 0, L.stream, a.offsets, a.P,
-              w.canon, w.canon_cap, a.out_off, a.ns, a.nf, a.nk, a.cdst, w.sub_base, L.ctl, L.desc, L.desc_cap);
+    // output aliasing the report bytes: the scan checks that nothing moves,
+    // and there is nothing to copy
+    const bool in_place = a.out_data != nullptr && a.out_data == a.data;
+    if (in_place) {
+        RO_LAUNCH(L, RO_K_GATHER_SCAN, k_gather_scan<true>, dim3((unsigned)grid_s), dim3(kBlock), 0, L.stream,
+                  a.offsets, a.P, w.canon, w.canon_cap, a.out_off, a.ns, a.nf, a.nk, a.cdst, w.sub_base, a.out_data,
+                  L.ctl, L.desc, L.desc_cap);
+    } else {
+        RO_LAUNCH(L, RO_K_GATHER_SCAN, k_gather_scan<false>, dim3((unsigned)grid_s), dim3(kBlock), 0, L.stream,
+                  a.offsets, a.P, w.canon, w.canon_cap, a.out_off, a.ns, a.nf, a.nk, a.cdst, w.sub_base, nullptr,
+                  L.ctl, L.desc, L.desc_cap);
+    }
     int64_t grid_f = (a.P + kBlock - 1) / kBlock;
     grid_f = grid_f < 1 ? 1 : (grid_f > (int64_t)L.num_cus * 8 ? (int64_t)L.num_cus * 8 : grid_f);
     RO_LAUNCH(L, RO_K_GATHER_FINALIZE, k_gather_finalize, dim3((unsigned)grid_f), dim3(kBlock), 0, L.stream, a.offsets,
                        a.P, w.canon_cap, a.out_off, a.out_cap, a.out_data != nullptr ? 1 : 0, a.ns, a.nf,
                        a.nk, a.complete, a.pstate, a.cdst, a.barrier, w.gkey, a.n_rejected, L.ctl);
-    if (a.out_data != nullptr) {
+    if (a.out_data != nullptr && !in_place) {
         // many small workgroups: a unit's cost varies with the records it
         // meets, and a deep queue of workgroups evens out the tail
         const int64_t grid_c = (int64_t)L.num_cus * RO_COPY_GRID;
         RO_LAUNCH(L, RO_K_GATHER_COPY, k_gather_copy, dim3((unsigned)grid_c), dim3(kBlock), 0, L.stream, a.offsets,
-                  a.P, w.canon, w.canon_cap, w.sub_base, a.out_data, a.out_data == a.data ? 1 : 0, L.ctl);
+                  a.P, w.canon, w.canon_cap, w.sub_base, a.out_data, L.ctl);
     }
     RO_LAUNCH(L, RO_K_GATHER_RESET, k_gather_reset, dim3(1), dim3(64), 0, L.stream, L.ctl);
     return hipGetLastError();

@@ -161,7 +161,6 @@ def _gather_bytes(P, N, S):
         "gather_finalize": 22 * P,
         # canonical slots and sub-tile bases in, payload read and written
         "gather_copy": 16 * N + 8 * nsub + 2 * S,
-        "gather_reset": 0,
     }
 
 

@@ -124,7 +124,9 @@ int ro_ctx_destroy(ro_ctx *ctx);
  * context launches is bracketed by two HIP events on the context's stream.
  * ro_ctx_trace_read waits for the stream, adds up the elapsed time per
  * kernel kind since the last read into launches[k] / total_ms[k] for
- * k < n (indices below), and clears the record. */
+ * k < n (indices below), and clears the record.  RO_K_GATHER_RESET is no
+ * longer launched (a gather clears its counters in its finalize kernel); it
+ * keeps its place so that the indices after it do not change. */
 enum {
     RO_K_EXPAND_SCAN = 0, RO_K_EXPAND_TAGS, RO_K_BATCH_SAMPLES, RO_K_BATCH,
     RO_K_GATHER_SCATTER, RO_K_GATHER_SCAN, RO_K_GATHER_FINALIZE, RO_K_GATHER_COPY,

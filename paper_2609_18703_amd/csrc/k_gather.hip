@@ -80,10 +80,9 @@ __global__ __launch_bounds__(kBlock) void k_gather_scatter(
     const int64_t *__restrict__ roff, const uint8_t *data, int64_t n,
     const int64_t *__restrict__ offsets, int64_t P, Canon *__restrict__ canon, int64_t canon_cap,
     int32_t *__restrict__ ns, int32_t *__restrict__ nf, int32_t *__restrict__ nk,
-    const uint8_t *__restrict__ barrier, const uint64_t *__restrict__ gkey, Ctl *ctl)
+    const uint8_t *__restrict__ barrier, const uint64_t *__restrict__ gkey, uint32_t epoch, Ctl *ctl)
 {
     __shared__ int64_t s_wave[kBlock / 64];
-    const uint32_t epoch = ctl->canon_epoch;
     const int64_t N = offsets[P];
     const bool cap_ok = N <= canon_cap;
     const int64_t gtid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
@@ -189,9 +188,8 @@ __global__ __launch_bounds__(kBlock) void k_gather_scan(
     const int64_t *__restrict__ offsets, int64_t P, const Canon *__restrict__ canon, int64_t canon_cap,
     int64_t *__restrict__ out_off, int32_t *__restrict__ ns, int32_t *__restrict__ nf,
     int32_t *__restrict__ nk, int64_t *__restrict__ cdst, int64_t *__restrict__ sub_base, const uint8_t *out,
-    Ctl *ctl, uint64_t *desc, int64_t desc_cap)
+    uint32_t epoch, Ctl *ctl, uint64_t *desc, int64_t desc_cap)
 {
-    const uint32_t epoch = ctl->canon_epoch;
     const uint32_t sepoch = scan_epoch(ctl);
     __shared__ int64_t s_wave[kBlock / 64];
     __shared__ uint64_t s_b;
@@ -438,9 +436,8 @@ __global__ __launch_bounds__(kBlock) void k_gather_finalize(
     int64_t out_cap, int has_data, const int32_t *__restrict__ ns, const int32_t *__restrict__ nf,
     const int32_t *__restrict__ nk, uint8_t *__restrict__ complete, uint8_t *__restrict__ pstate,
     int64_t *__restrict__ cdst, uint8_t *__restrict__ barrier, const uint64_t *__restrict__ gkey,
-    int64_t *n_rejected, Ctl *ctl)
+    int64_t *n_rejected, uint32_t epoch, Ctl *ctl)
 {
-    const uint32_t epoch = ctl->canon_epoch;
     const int64_t N0 = offsets[P];
     const int64_t N = N0 <= canon_cap ? N0 : 0;
     const int64_t total = N > 0 ? ctl->total : 0;
@@ -451,6 +448,11 @@ __global__ __launch_bounds__(kBlock) void k_gather_finalize(
         if (n_rejected) *n_rejected = ctl->n_rejected;
         if (ctl->n_filled != ctl->n_valid) raise_err(ctl, RO_EDUP);
         if (has_data && total > out_cap) raise_err(ctl, RO_ECAP);
+        // the call's counters are read only here: cleared for the next
+        // gather (the byte total is rewritten by every scan with children)
+        ctl->n_valid = 0;
+        ctl->n_filled = 0;
+        ctl->n_rejected = 0;
     }
     for (int64_t p = gtid; p < P; p += (int64_t)gridDim.x * kBlock) {
         const int64_t st = offsets[p];
@@ -472,18 +474,6 @@ __global__ __launch_bounds__(kBlock) void k_gather_finalize(
 // finalize needs all three counters even if the caller wants none of them;
 // the runtime passes workspace arrays in that case.
 
-// End of a gather: clear the per-call counters and advance the canonical epoch.
-__global__ void k_gather_reset(Ctl *ctl)
-{
-    if (threadIdx.x == 0) {
-        ctl->n_valid = 0;
-        ctl->n_filled = 0;
-        ctl->total = 0;
-        ctl->n_rejected = 0;
-        ctl->canon_epoch = ctl->canon_epoch + 1;
-    }
-}
-
 // ---------------------------------------------------------------- copy
 // First sub-tile whose output holds byte `lo`: the largest s in [0, nsub)
 // with sub_base[s] <= lo (sub_base[0] = 0).
@@ -501,10 +491,9 @@ __device__ __forceinline__ int64_t find_sub_tile(const int64_t *__restrict__ sub
 // long, and few parents or many.
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RO_COPY_WAVES))) void k_gather_copy(
     const int64_t *__restrict__ offsets, int64_t P, const Canon *__restrict__ canon, int64_t canon_cap,
-    const int64_t *__restrict__ sub_base, uint8_t *__restrict__ out, Ctl *ctl)
+    const int64_t *__restrict__ sub_base, uint8_t *__restrict__ out, uint32_t epoch, Ctl *ctl)
 {
     constexpr int kWaves = kBlock / 64;
-    const uint32_t epoch = ctl->canon_epoch;
     __shared__ int32_t s_dst_all[kWaves][kSub + 1];     // clipped destination offset of each record
     __shared__ uint64_t s_src_all[kWaves][kSub];        // source address of its first clipped byte
     __shared__ int32_t s_edge_all[kWaves][kEdgeCap];    // edge chunks of the window
@@ -585,7 +574,7 @@ hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w
     const int64_t grid_r = (int64_t)L.num_cus * 8;
     RO_LAUNCH(L, RO_K_GATHER_SCATTER, k_gather_scatter, dim3((unsigned)grid_r), dim3(kBlock), 0, L.stream,
               a.rp, a.ro, a.rs, a.roff, a.data, a.n, a.offsets, a.P, w.canon, w.canon_cap, a.ns, a.nf,
-              a.nk, a.barrier, w.gkey, L.ctl);
+              a.nk, a.barrier, w.gkey, epoch, L.ctl);
     // three workgroups per CU drew tickets faster than four (fewer waiting
     // on the look-back at once) and two left the largest scans short of work
     const int64_t grid_s = (int64_t)L.num_cus * RO_SCAN_WG;
@@ -595,25 +584,24 @@ hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w
     if (in_place) {
         RO_LAUNCH(L, RO_K_GATHER_SCAN, k_gather_scan<true>, dim3((unsigned)grid_s), dim3(kBlock), 0, L.stream,
                   a.offsets, a.P, w.canon, w.canon_cap, a.out_off, a.ns, a.nf, a.nk, a.cdst, w.sub_base, a.out_data,
-                  L.ctl, L.desc, L.desc_cap);
+                  epoch, L.ctl, L.desc, L.desc_cap);
     } else {
         RO_LAUNCH(L, RO_K_GATHER_SCAN, k_gather_scan<false>, dim3((unsigned)grid_s), dim3(kBlock), 0, L.stream,
                   a.offsets, a.P, w.canon, w.canon_cap, a.out_off, a.ns, a.nf, a.nk, a.cdst, w.sub_base, nullptr,
-                  L.ctl, L.desc, L.desc_cap);
+                  epoch, L.ctl, L.desc, L.desc_cap);
     }
     int64_t grid_f = (a.P + kBlock - 1) / kBlock;
     grid_f = grid_f < 1 ? 1 : (grid_f > (int64_t)L.num_cus * 8 ? (int64_t)L.num_cus * 8 : grid_f);
     RO_LAUNCH(L, RO_K_GATHER_FINALIZE, k_gather_finalize, dim3((unsigned)grid_f), dim3(kBlock), 0, L.stream, a.offsets,
                        a.P, w.canon_cap, a.out_off, a.out_cap, a.out_data != nullptr ? 1 : 0, a.ns, a.nf,
-                       a.nk, a.complete, a.pstate, a.cdst, a.barrier, w.gkey, a.n_rejected, L.ctl);
+                       a.nk, a.complete, a.pstate, a.cdst, a.barrier, w.gkey, a.n_rejected, epoch, L.ctl);
     if (a.out_data != nullptr && !in_place) {
         // many small workgroups: a unit's cost varies with the records it
         // meets, and a deep queue of workgroups evens out the tail
         const int64_t grid_c = (int64_t)L.num_cus * RO_COPY_GRID;
         RO_LAUNCH(L, RO_K_GATHER_COPY, k_gather_copy, dim3((unsigned)grid_c), dim3(kBlock), 0, L.stream, a.offsets,
-                  a.P, w.canon, w.canon_cap, w.sub_base, a.out_data, L.ctl);
+                  a.P, w.canon, w.canon_cap, w.sub_base, a.out_data, epoch, L.ctl);
     }
-    RO_LAUNCH(L, RO_K_GATHER_RESET, k_gather_reset, dim3(1), dim3(64), 0, L.stream, L.ctl);
     return hipGetLastError();
 }
 

@@ -6,31 +6,13 @@ namespace ro {
 
 __global__ void k_ctl_init(Ctl *ctl)
 {
-    if (threadIdx.x == 0) {
-        ctl->scan_epoch = 1;
-        ctl->canon_epoch = 1;
-    }
+    if (threadIdx.x == 0) ctl->scan_epoch = 1;
 }
 
 // Clears the error word (after the host has read it), in stream order.
 __global__ void k_clear_err(Ctl *ctl)
 {
     if (threadIdx.x == 0) ctl->err = 0;
-}
-
-// Moves the canonical epoch forward (a test aid: slots of earlier epochs
-// read as unreported at any later epoch).
-__global__ void k_set_canon_epoch(Ctl *ctl, uint32_t e)
-{
-    if (threadIdx.x == 0) ctl->canon_epoch = e;
-}
-
-// Clears every canonical slot's tag and restarts the canonical epoch at 1.
-__global__ void k_reset_canon(Ctl *ctl, Canon *canon, int64_t n)
-{
-    const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    for (int64_t i = g; i < n; i += (int64_t)gridDim.x * blockDim.x) canon[i].tag = 0;
-    if (g == 0) ctl->canon_epoch = 1;
 }
 
 // Zero-fill (a kernel, so that a captured graph holds no memset node).
@@ -40,7 +22,8 @@ __global__ void k_fill_u64(uint64_t *p, int64_t n)
         p[i] = 0;
 }
 
-// Clears the canonical slot tags of a stream (its run epoch wrapped).
+// Clears canonical slot tags: a context's when its canonical epoch wraps, a
+// stream's when its run epoch wraps.
 __global__ void k_clear_tags(Canon *canon, int64_t n)
 {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
@@ -68,19 +51,6 @@ hipError_t launch_ctl_init(const Launch &L)
 hipError_t launch_clear_err(const Launch &L)
 {
     RO_LAUNCH(L, RO_K_MISC, k_clear_err, dim3(1), dim3(64), 0, L.stream, L.ctl);
-    return hipGetLastError();
-}
-
-hipError_t launch_set_canon_epoch(const Launch &L, uint32_t e)
-{
-    RO_LAUNCH(L, RO_K_MISC, k_set_canon_epoch, dim3(1), dim3(64), 0, L.stream, L.ctl, e);
-    return hipGetLastError();
-}
-
-hipError_t launch_reset_canon(const Launch &L, Canon *canon, int64_t n)
-{
-    RO_LAUNCH(L, RO_K_MISC, k_reset_canon, dim3((unsigned)L.num_cus * 4), dim3(256), 0, L.stream, L.ctl,
-                       canon, n);
     return hipGetLastError();
 }
 

@@ -69,7 +69,7 @@ struct ro_ctx {
     int32_t *cnt;             // [3 * cnt_cap] counters used when the caller passes none
     uint64_t *gkey;           // [cnt_cap] first group failure per parent (gather)
     int64_t cnt_cap;
-    int64_t gathers;          // host shadow of the device canonical epoch
+    int64_t gathers;          // canonical epoch of the next gather (1..2^30-1)
     PbWs pb;                  // parent-bound reservation workspace
     int64_t pb_cap, pb_pcap;  // its queue entries and parents
     void *pb_block;
@@ -271,7 +271,7 @@ int ensure_pb(ro_ctx *c, int64_t q, int64_t p)
 int before_gather(ro_ctx *c)
 {
     if (c->gathers + 1 > (int64_t)kMaxCanonEpoch) {
-        if (launch_reset_canon(launch_of(c), c->canon, c->canon_cap) != hipSuccess) return RO_EHIP;
+        if (launch_clear_tags(launch_of(c), c->canon, c->canon_cap) != hipSuccess) return RO_EHIP;
         // group-failure keys carry the same epoch
         if (c->gkey && launch_zero_u64(launch_of(c), c->gkey, c->cnt_cap) != hipSuccess) return RO_EHIP;
         c->gathers = 1;
@@ -305,7 +305,7 @@ int ro_ctx_create(ro_ctx **out, void *hip_stream)
         ro_ctx_destroy(c);
         return RO_EHIP;
     }
-    c->gathers = 1;           // device canonical epoch starts at 1
+    c->gathers = 1;           // the first gather runs at canonical epoch 1
     *out = c;
     return RO_OK;
 }
@@ -746,10 +746,7 @@ int ro_debug_epochs(ro_ctx *c, ro_stream *s, ro_grains *g, int64_t canon_left, i
     if (canon_left >= 1 && canon_left < (int64_t)kMaxCanonEpoch) {
         // the next gather runs at epoch max - canon_left + 1
         const uint32_t e = (uint32_t)((int64_t)kMaxCanonEpoch - canon_left + 1);
-        if (e > (uint32_t)c->gathers) {
-            if (launch_set_canon_epoch(launch_of(c), e) != hipSuccess) return RO_EHIP;
-            c->gathers = e;
-        }
+        if (e > (uint32_t)c->gathers) c->gathers = e;
     }
     if (s) {
         if (run_left >= 1 && run_left < (int64_t)kMaxCanonEpoch &&

@@ -37,7 +37,7 @@ struct Ctl {
     int64_t n_virtual;       // emit: children of emitted parents
     int64_t n_rejected;      // gather: reports rejected by a group-failure barrier
     uint32_t scan_epoch;     // look-back descriptor epoch of the next ticketed launch (1..65535)
-    uint32_t canon_epoch;    // canonical-slot epoch of the next gather (1..2^30-1)
+    uint32_t pad32;
     int64_t pad[7];
 };
 
@@ -66,9 +66,6 @@ void trace_end(const Launch &L, int kernel);
 constexpr uint32_t kMaxScanEpoch = 65535;
 constexpr uint32_t kMaxCanonEpoch = (1u << 30) - 1;
 
-// Reset kernels the host enqueues when a device epoch is about to wrap.
-hipError_t launch_reset_canon(const Launch &L, Canon *canon, int64_t n);
-hipError_t launch_set_canon_epoch(const Launch &L, uint32_t e);
 hipError_t launch_clear_err(const Launch &L);
 hipError_t launch_ctl_init(const Launch &L);
 hipError_t launch_zero_u64(const Launch &L, uint64_t *p, int64_t n);
@@ -138,8 +135,9 @@ struct GatherWs {
     uint64_t *gkey;          // [P] first group failure per parent (epoch << 32 | ~report index)
 };
 
-// epoch: the canonical epoch of this gather (the host's shadow of the device
-// one), which also tags its group-failure keys
+// epoch: the canonical epoch of this gather (kept by the host: 1..2^30-1,
+// one more per gather, every slot tag cleared when it wraps), which tags its
+// slots and its group-failure keys
 hipError_t launch_gather(const Launch &L, const GatherArgs &a, const GatherWs &w, uint32_t epoch);
 
 // grain phases and the generation fence.  One 16-byte record per Grain:

@@ -36,7 +36,6 @@ __global__ void k_noalloc_begin(uint64_t *ws, int first)
             ctl->done = 0;
             ctl->ticket = 0;
             ctl->scan_epoch = 1;
-            ctl->canon_epoch = 1;
         }
     }
     if (blockIdx.x == 0 && threadIdx.x == 0) ctl->err = 0;

@@ -286,6 +286,60 @@ def test_gather_errors(ctx):
                  np.arange(10, dtype=np.uint8))
 
 
+@pytest.mark.parametrize("case", ["short_runs", "empty_runs"])
+def test_gather_in_place(ctx, case):
+    """Output = the reports' own bytes.  With every surviving record already
+    at its output position (reports in canonical order, non-surviving ones
+    without bytes) nothing moves and the result is the oracle's; one failed
+    report holding bytes shifts every later record, which is RO_EINVAL.  The
+    runs of empty parents send some scan tiles to their global-memory parent
+    search."""
+    rng = np.random.default_rng(21 if case == "short_runs" else 22)
+    if case == "short_runs":
+        counts = rng.integers(0, 9, 5000).astype(np.int32)
+    else:
+        counts = np.concatenate([rng.integers(1, 30, 400), np.zeros(9000), rng.integers(0, 4, 3000),
+                                 np.zeros(6000), [3000], rng.integers(0, 6, 1000)]).astype(np.int32)
+    offs = O.expand(counts, tags=False)
+    P, N = len(counts), int(offs[-1])
+    par = np.repeat(np.arange(P), counts).astype(np.uint32)
+    ordi = np.concatenate([np.arange(k) for k in counts]).astype(np.uint32)
+    st = rng.choice(np.array([0, 0, 0, 0, 1, 2], np.uint8), N)
+    lens = np.where(st == 0, rng.integers(0, 70, N), 0).astype(np.int64)
+    bad = int(np.nonzero(st == 1)[0][N // 10 % max(1, int((st == 1).sum()))])   # a failed report
+    for moved in (False, True):
+        ln = lens.copy()
+        if moved:
+            ln[bad] = 5                      # failed, yet holding bytes
+        off = np.concatenate([[0], np.cumsum(ln)]).astype(np.int64)
+        data = rng.integers(0, 256, int(off[-1]) + 16, dtype=np.uint8)
+        want = O.gather(par, ordi, st, off, data, offs)
+        d_data = D.to_dev(data)
+        o_off = torch.empty(P + 1, dtype=torch.int64, device="cuda")
+        ns = torch.empty(P, dtype=torch.int32, device="cuda")
+        nf, nk = ns.clone(), ns.clone()
+        comp = torch.empty(P, dtype=torch.uint8, device="cuda")
+        pst = comp.clone()
+        _say("gather in place", case, N, "moved" if moved else "in place")
+        ctx.gather(D.to_dev(par.view(np.int32)), D.to_dev(ordi.view(np.int32)), D.to_dev(st), D.to_dev(off),
+                   d_data, D.to_dev(offs), o_off, d_data, ns, nf, nk, comp, pst, n=N, out_cap=d_data.numel())
+        rc = ctx.status()
+        if moved:
+            assert rc == O.EINVAL
+            continue
+        assert rc == O.OK
+        tot = int(want["out_off"][-1])
+        assert tot == int(off[-1])
+        assert np.array_equal(o_off.cpu().numpy(), want["out_off"])
+        assert np.array_equal(ns.cpu().numpy(), want["n_success"])
+        assert np.array_equal(nf.cpu().numpy(), want["n_failed"])
+        assert np.array_equal(nk.cpu().numpy(), want["n_skipped"])
+        assert np.array_equal(comp.cpu().numpy(), want["complete"])
+        assert np.array_equal(pst.cpu().numpy(), want["parent_state"])
+        got = d_data.cpu().numpy()
+        assert np.array_equal(got[:tot], want["out_data"]) and np.array_equal(got, data)
+
+
 def test_gather_repeated_calls_reuse_workspace(ctx):
     """Canonical slots of an earlier call never leak into a later one."""
     rng = np.random.default_rng(4)

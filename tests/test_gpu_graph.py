@@ -1,13 +1,14 @@
-"""A streaming step captured in one HIP graph.
+"""Steps of the library captured in one HIP graph.
 
-The step is the streaming sequence of the library: expand, stream reset, then
-per wave the stream's batch, report and emission (Sec. 1 and Sec. 4: a parent
-proceeds once all its children are terminal, in parent order).  It is
-captured on the context's stream with a torch CUDA graph.  Every replay, with
-eager steps and synchronisations between replays, must leave the same outputs
-as an eager step, and the last wave's emission must equal the oracle's.  The
-outputs are overwritten before each replay, so a replay that writes nothing
-fails.
+A streaming step (expand, stream reset, then per wave the stream's batch,
+report and emission: Sec. 1 and Sec. 4, a parent proceeds once all its
+children are terminal, in parent order) and a nested documents step (two
+expansions, two batches, a gather into the mid slots and an in-place gather
+into the top slots: Sec. 4, nested F.expand / F.reduce) are each captured on
+the context's stream with a torch CUDA graph.  Every replay, with eager steps
+and synchronisations between replays, must leave the same outputs as an eager
+step, and the eager step must equal the oracle.  The outputs are overwritten
+before each replay, so a replay that writes nothing fails.
 """
 import sys
 
@@ -122,4 +123,77 @@ def test_stream_step_in_a_graph():
             del g
             torch.cuda.synchronize()
             st.close()
+            ctx.close()
+
+
+_NESTED_INPUTS = ("counts1", "queue1", "counts2", "queue2", "leaf_state", "leaf_off", "leaf_data")
+
+
+def _nested_outputs(b):
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy().copy() for k, v in vars(b).items()
+            if isinstance(v, torch.Tensor) and k not in _NESTED_INPUTS}
+
+
+def test_nested_step_in_a_graph():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_18703_amd as R
+    from paper_2609_18703_amd import pipeline as PL
+
+    n = W.config3(n_docs=300)
+    r = n.reports
+    data = r.data()
+    want = O.nested(n.counts1, n.queue1, None, n.batch1, n.counts2, n.queue2, None, n.batch2,
+                    r.state, r.off, data)
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        ctx = R.Context()
+        b = PL.NestedBuffers(D.to_dev(n.counts1), D.to_dev(n.queue1.view(np.int32)), n.batch1,
+                             D.to_dev(n.counts2), D.to_dev(n.queue2.view(np.int32)), n.batch2,
+                             D.to_dev(r.state), D.to_dev(r.off), D.to_dev(data), len(n.queue1),
+                             len(n.queue2), upper_in_place=True)
+        ctx.reserve(b.N2, b.N1, b.N2)
+
+        def step():
+            PL.nested(ctx, b)
+
+        _say("graph: nested eager steps", b.P1, b.N1, b.N2)
+        step()
+        step()
+        ctx.check("eager")
+        eager = _nested_outputs(b)
+        N1, P1 = b.N1, b.P1
+        low, up = want["low"], want["up"]
+        assert np.array_equal(eager["offsets1"][:P1 + 1], want["offsets1"])
+        assert np.array_equal(eager["offsets2"][:N1 + 1], want["offsets2"])
+        assert np.array_equal(eager["mid_off"][:N1 + 1], low["out_off"])
+        assert np.array_equal(eager["mid_data"][:int(low["out_off"][-1])], low["out_data"])
+        assert np.array_equal(eager["top_off"][:P1 + 1], up["out_off"])
+        assert np.array_equal(eager["top_state"][:P1], up["parent_state"])
+        assert np.array_equal(eager["top_cnt"][:P1], up["n_success"])
+
+        _say("graph: nested capture")
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            step()
+        torch.cuda.synchronize()
+        try:
+            for k in range(3):
+                for name in eager:
+                    getattr(b, name).fill_(7)
+                g.replay()
+                ctx.check(f"nested replay {k}")
+                _say("graph: nested replay", k)
+                got = _nested_outputs(b)
+                assert all(np.array_equal(got[x], eager[x]) for x in eager), k
+                for name in eager:
+                    getattr(b, name).fill_(7)
+                step()
+                ctx.check(f"nested eager after replay {k}")
+                got = _nested_outputs(b)
+                assert all(np.array_equal(got[x], eager[x]) for x in eager), k
+        finally:
+            del g
+            torch.cuda.synchronize()
             ctx.close()

@@ -259,6 +259,89 @@ static void free_expansion(expansion *x)
     free(x->counts); free(x->offs); free(x->cp); free(x->co);
 }
 
+/* A gather whose output is its own report bytes: reports in canonical order,
+ * failed and skipped ones without bytes, so every record already sits at its
+ * output position; the result equals the oracle's and nothing moves.  Then
+ * one failed report holding bytes shifts every later record: RO_EINVAL. */
+static void case_in_place(ro_ctx *ctx, int64_t P)
+{
+    expansion x = make_expansion(P, 9);
+    const int64_t N = x.N;
+    uint8_t *rs = xmalloc((size_t)N);
+    int64_t *roff = xmalloc((size_t)(N + 1) * 8);
+    static const uint8_t states[5] = {RO_SUCCESS, RO_SUCCESS, RO_SUCCESS, RO_FAILED, RO_SKIPPED};
+    int64_t bad = -1;
+    for (int64_t c = 0; c < N; ++c) {
+        rs[c] = states[below(5)];
+        if (rs[c] == RO_FAILED && bad < 0 && c >= N / 3) bad = c;
+    }
+    uint32_t *d_rp = dmalloc((size_t)N * 4), *d_ro = dmalloc((size_t)N * 4);
+    uint8_t *d_rs = dmalloc((size_t)N);
+    int64_t *d_roff = dmalloc((size_t)(N + 1) * 8), *d_oo = dmalloc((size_t)(P + 1) * 8);
+    int32_t *d_cnt = dmalloc((size_t)P * 12);
+    uint8_t *d_comp = dmalloc((size_t)P), *d_pst = dmalloc((size_t)P);
+    up(d_rp, x.cp, (size_t)N * 4);
+    up(d_ro, x.co, (size_t)N * 4);
+    up(d_rs, rs, (size_t)N);
+    for (int moved = 0; moved < 2; ++moved) {
+        roff[0] = 0;
+        for (int64_t c = 0; c < N; ++c)
+            roff[c + 1] = roff[c] + (rs[c] == RO_SUCCESS ? below(50) : (moved && c == bad ? 5 : 0));
+        const int64_t bytes = roff[N];
+        uint8_t *data = xmalloc((size_t)bytes + 16);
+        for (int64_t i = 0; i < bytes + 16; ++i) data[i] = (uint8_t)rnd();
+        uint8_t *d_data = dmalloc((size_t)bytes + 16);
+        up(d_data, data, (size_t)bytes + 16);
+        up(d_roff, roff, (size_t)(N + 1) * 8);
+        ro_reports r = {d_rp, d_ro, d_rs, d_roff, d_data, N};
+        ro_gather_out o;
+        memset(&o, 0, sizeof o);
+        o.out_off = d_oo;
+        o.out_data = d_data;                 /* the report bytes themselves */
+        o.out_cap = bytes + 16;
+        o.n_success = d_cnt;
+        o.n_failed = d_cnt + P;
+        o.n_skipped = d_cnt + 2 * P;
+        o.complete = d_comp;
+        o.parent_state = d_pst;
+        RO_OK_(ro_gather(ctx, &r, x.d_offs, P, &o));
+        const int status = ro_ctx_status(ctx);
+        if (moved) {
+            EXPECT(bad < 0 || status == RO_EINVAL, "in-place gather with a record to move is RO_EINVAL");
+        } else {
+            EXPECT(status == RO_OK, "in-place gather status");
+            int64_t *w_oo = xmalloc((size_t)(P + 1) * 8), *g_oo = xmalloc((size_t)(P + 1) * 8);
+            uint8_t *w_od = xmalloc((size_t)bytes + 1), *g_od = xmalloc((size_t)bytes + 16);
+            int32_t *w_cnt = xmalloc((size_t)P * 12), *g_cnt = xmalloc((size_t)P * 12);
+            uint8_t *w_comp = xmalloc((size_t)P), *w_pst = xmalloc((size_t)P);
+            uint8_t *g_comp = xmalloc((size_t)P), *g_pst = xmalloc((size_t)P);
+            if (oracle_gather(x.cp, x.co, rs, roff, data, N, x.offs, P, w_oo, w_od, bytes, w_cnt, w_cnt + P,
+                              w_cnt + 2 * P, w_comp, w_pst, NULL, NULL, NULL) != 0)
+                exit(4);
+            down(g_oo, d_oo, (size_t)(P + 1) * 8);
+            down(g_od, d_data, (size_t)bytes + 16);
+            down(g_cnt, d_cnt, (size_t)P * 12);
+            down(g_comp, d_comp, (size_t)P);
+            down(g_pst, d_pst, (size_t)P);
+            EXPECT(memcmp(g_oo, w_oo, (size_t)(P + 1) * 8) == 0 && w_oo[P] == bytes, "in-place slot offsets");
+            EXPECT(memcmp(g_cnt, w_cnt, (size_t)P * 12) == 0, "in-place counts");
+            EXPECT(memcmp(g_comp, w_comp, (size_t)P) == 0 && memcmp(g_pst, w_pst, (size_t)P) == 0,
+                   "in-place completion");
+            EXPECT(memcmp(g_od, w_od, (size_t)bytes) == 0 && memcmp(g_od, data, (size_t)bytes + 16) == 0,
+                   "in-place bytes: the oracle's slots, nothing moved");
+            free(w_oo); free(g_oo); free(w_od); free(g_od); free(w_cnt); free(g_cnt);
+            free(w_comp); free(w_pst); free(g_comp); free(g_pst);
+        }
+        HIP_OK(hipStreamSynchronize(g_st));
+        HIP_OK(hipFree(d_data));
+        free(data);
+    }
+    HIP_OK(hipFree(d_rp)); HIP_OK(hipFree(d_ro)); HIP_OK(hipFree(d_rs)); HIP_OK(hipFree(d_roff));
+    HIP_OK(hipFree(d_oo)); HIP_OK(hipFree(d_cnt)); HIP_OK(hipFree(d_comp)); HIP_OK(hipFree(d_pst));
+    free(rs); free(roff);
+    free_expansion(&x);
+}
+
 /* Parent-bound reservations against the oracle. */
 static void case_batch_parent(ro_ctx *ctx, int64_t P, int32_t B)
 {
@@ -568,6 +651,10 @@ int main(void)
     printf("case %d: after the error\n", case_id);
     fflush(stdout);
     one_case(ctx, st, 800, 5, 0);
+    ++case_id;
+    printf("case %d: gather in place\n", case_id);
+    fflush(stdout);
+    case_in_place(ctx, 4000);
     ++case_id;
     printf("case %d: parent-bound reservation\n", case_id);
     fflush(stdout);
